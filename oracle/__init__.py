@@ -1,0 +1,174 @@
+"""CPU oracle for the Progressive Tree Drafting hot path (fp64, plain C).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by the smoke check and by the
+CPU-baseline leg of the benchmark.  The product library never imports or links
+it, and it shares no code with the GPU path.
+
+Thin ctypes wrappers over ``libptd_oracle.so`` built from ``ptd_oracle.c``
+(see ``oracle/build.py``).  Inputs are the workload arrays exactly as the GPU
+receives them (bf16 as uint16 bits, or float32); the C code widens them to
+fp64 exactly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libptd_oracle.so")
+_lib = None
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
+    lib.oracle_tree_mask.argtypes = [vp, vp, i, i, vp, vp]
+    lib.oracle_attention_row.argtypes = [vp, vp, vp, i, vp, vp, i, i, i, i, i, i,
+                                         d, i, i, i, vp]
+    lib.oracle_tree_attention.argtypes = [vp, vp, vp, i, vp, vp, i, i, i, i, i, i,
+                                          d, vp]
+    lib.oracle_topk.argtypes = [vp, i, i, i, ctypes.c_longlong, i, vp, vp, vp]
+    lib.oracle_verify.argtypes = [vp, vp, vp, vp, i, i, vp, vp, vp]
+    lib.oracle_expand.argtypes = [vp, vp, vp, i, i, vp, i, vp, i, i, vp, vp, vp]
+    for f in ("oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
+              "oracle_topk", "oracle_verify", "oracle_expand"):
+        getattr(lib, f).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+def _check(st: int):
+    if st != 0:
+        raise OracleError({2: "bad sizes", 7: "malformed tree"}.get(st, st))
+
+
+def _dtype_code(arr: np.ndarray) -> int:
+    if arr.dtype == np.uint16:
+        return 1
+    if arr.dtype == np.float32:
+        return 0
+    raise TypeError("oracle inputs are bf16 bits (uint16) or float32")
+
+
+def tree_mask(parent: np.ndarray, tree_len: Optional[np.ndarray] = None):
+    """parent int32 [B][T] -> (mask uint64 [B][T][W], depth int32 [B][T])."""
+    parent = _c(parent, np.int32)
+    B, T = parent.shape
+    W = (T + 63) // 64
+    mask = np.zeros((B, T, W), np.uint64)
+    depth = np.zeros((B, T), np.int32)
+    tl = None if tree_len is None else _c(tree_len, np.int32)
+    _check(_load().oracle_tree_mask(_p(parent), _p(tl), B, T, _p(mask), _p(depth)))
+    return mask, depth
+
+
+def _attn_args(q, k_cache, v_cache, kv_len, parent):
+    q = np.ascontiguousarray(q)
+    k_cache = np.ascontiguousarray(k_cache)
+    v_cache = np.ascontiguousarray(v_cache)
+    dt = _dtype_code(q)
+    if _dtype_code(k_cache) != dt or _dtype_code(v_cache) != dt:
+        raise TypeError("q/k/v dtypes differ")
+    B, T, Hq, D = q.shape
+    _, Hkv, L_cap, _ = k_cache.shape
+    return (q, k_cache, v_cache, dt, _c(kv_len, np.int32), _c(parent, np.int32),
+            B, T, Hq, Hkv, D, L_cap)
+
+
+def tree_attention(q, k_cache, v_cache, kv_len, parent, scale: float) -> np.ndarray:
+    """All outputs [B][T][Hq][D] in float64."""
+    q, kc, vc, dt, kvl, par, B, T, Hq, Hkv, D, L = _attn_args(
+        q, k_cache, v_cache, kv_len, parent)
+    out = np.zeros((B, T, Hq, D), np.float64)
+    _check(_load().oracle_tree_attention(_p(q), _p(kc), _p(vc), dt, _p(kvl),
+                                         _p(par), B, T, Hq, Hkv, D, L,
+                                         float(scale), _p(out)))
+    return out
+
+
+def attention_rows(q, k_cache, v_cache, kv_len, parent, scale: float, rows):
+    """Selected outputs: rows is a list of (b, h, i); returns [len(rows)][D]."""
+    q, kc, vc, dt, kvl, par, B, T, Hq, Hkv, D, L = _attn_args(
+        q, k_cache, v_cache, kv_len, parent)
+    lib = _load()
+    out = np.zeros((len(rows), D), np.float64)
+    for n, (b, h, i) in enumerate(rows):
+        _check(lib.oracle_attention_row(
+            _p(q), _p(kc), _p(vc), dt, _p(kvl), _p(par), B, T, Hq, Hkv, D, L,
+            float(scale), int(b), int(h), int(i),
+            out[n].ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def topk(logits: np.ndarray, k: int):
+    """logits [R][V] (or [..][V]) -> (argmax int32 [R], idx int32 [R][k],
+    val float64 [R][k])."""
+    lg = np.ascontiguousarray(logits)
+    V = lg.shape[-1]
+    lg2 = lg.reshape(-1, V)
+    R = lg2.shape[0]
+    am = np.zeros(R, np.int32)
+    idx = np.zeros((R, k), np.int32)
+    val = np.zeros((R, k), np.float64)
+    _check(_load().oracle_topk(_p(lg2), _dtype_code(lg2), R, V, V, k, _p(am),
+                               _p(idx), _p(val)))
+    return am, idx, val
+
+
+def verify(argmax, tokens, parent, tree_len=None):
+    """-> (accept_len [B], accept_nodes [B][T], out_tokens [B][T+1])."""
+    tokens = _c(tokens, np.int32)
+    parent = _c(parent, np.int32)
+    B, T = parent.shape
+    am = _c(argmax, np.int32).reshape(B, T + 1)
+    al = np.zeros(B, np.int32)
+    an = np.zeros((B, T), np.int32)
+    ot = np.zeros((B, T + 1), np.int32)
+    tl = None if tree_len is None else _c(tree_len, np.int32)
+    _check(_load().oracle_verify(_p(am), _p(tokens), _p(parent), _p(tl), B, T,
+                                 _p(al), _p(an), _p(ot)))
+    return al, an, ot
+
+
+def expand(parent, tokens, topk_idx, width_sched, d_max: int, T_max: int,
+           tree_len=None):
+    """-> (parent_next [B][T_max], tokens_next [B][T_max], tree_len_next [B])."""
+    parent = _c(parent, np.int32)
+    tokens = _c(tokens, np.int32)
+    B, T = parent.shape
+    ti = _c(topk_idx, np.int32)
+    k = ti.shape[-1]
+    ti = ti.reshape(B, T + 1, k)
+    ws = _c(width_sched, np.int32)
+    if ws.shape[0] < d_max:
+        raise ValueError("width_sched needs d_max entries")
+    pn = np.zeros((B, T_max), np.int32)
+    tn = np.zeros((B, T_max), np.int32)
+    ln = np.zeros(B, np.int32)
+    tl = None if tree_len is None else _c(tree_len, np.int32)
+    _check(_load().oracle_expand(_p(parent), _p(tokens), _p(tl), B, T, _p(ti), k,
+                                 _p(ws), d_max, T_max, _p(pn), _p(tn), _p(ln)))
+    return pn, tn, ln

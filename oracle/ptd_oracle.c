@@ -1,0 +1,357 @@
+/*
+ * Plain fp64 CPU oracle for one Progressive Tree Drafting step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, includes
+ * or calls this file; only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark load it.  It shares no code with the GPU path.
+ *
+ * Every function is the plain definition of its result, written for a reader
+ * to check against the paper by eye: no blocking, no fusion, no reordering.
+ * Floating point is fp64 throughout; bf16/fp32 inputs are widened exactly.
+ *
+ *   oracle_tree_mask       Sec. 3.1 "Tree Construction": pi(v) = {v} u pi(P(v)),
+ *                          position from |pi(v)|.
+ *   oracle_attention_row   Sec. 3.1 + Sec. 3.2: a node attends to the committed
+ *   oracle_tree_attention  prefix X and to its own ancestors only (softmax of
+ *                          scaled dot products, plain two-pass form).
+ *   oracle_topk            Sec. 3.2 greedy verification tokens (argmax), App. A
+ *                          top-k candidates; order (value desc, index asc).
+ *   oracle_verify          Sec. 3.2 eligible edges I and accepted sequence X';
+ *                          Alg. 1 step 5-6.
+ *   oracle_expand          Sec. 3.1 "Progressive Expansion" (V^t, E^t) with the
+ *                          width limit of "Overhead Constraints", top-k children.
+ *
+ * Error returns: 0 = ok, 7 = malformed tree (parent[i] outside [-1, i)),
+ * 2 = bad sizes.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_BAD_SIZE 2
+#define ORC_BAD_TREE 7
+
+/* element widening: dtype 0 = fp32, 1 = bf16 (upper half of an fp32) */
+static double load_elem(const void* base, int dtype, size_t idx) {
+  if (dtype == 1) {
+    uint16_t h = ((const uint16_t*)base)[idx];
+    uint32_t u = ((uint32_t)h) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+  }
+  return (double)((const float*)base)[idx];
+}
+
+static int node_count(const int32_t* tree_len, int b, int T) {
+  if (!tree_len) return T;
+  int n = tree_len[b];
+  return n < 0 ? 0 : (n > T ? T : n);
+}
+
+static int tree_is_valid(const int32_t* par, int n) {
+  for (int i = 0; i < n; ++i)
+    if (par[i] < -1 || par[i] >= i) return 0;
+  return 1;
+}
+
+/* ---------------------------------------------------------------------------
+ * Ancestor sets.  Sec. 3.1: pi(v) = {v} u pi(P(v)); a root's parent is the last
+ * committed token, which is outside the tree.  Bit j of row i lives in word
+ * j/64, bit j%64.  depth[i] = |pi(i)|.  Rows at or beyond tree_len are zero.
+ * ------------------------------------------------------------------------- */
+int oracle_tree_mask(const int32_t* parent, const int32_t* tree_len, int B, int T,
+                     uint64_t* mask, int32_t* depth) {
+  if (B < 0 || T < 1) return ORC_BAD_SIZE;
+  const int W = (T + 63) / 64;
+  int status = ORC_OK;
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int n = node_count(tree_len, b, T);
+    memset(mask + (size_t)b * T * W, 0, sizeof(uint64_t) * (size_t)T * W);
+    memset(depth + (size_t)b * T, 0, sizeof(int32_t) * (size_t)T);
+    if (!tree_is_valid(par, n)) { status = ORC_BAD_TREE; continue; }
+    for (int i = 0; i < n; ++i) {
+      uint64_t* row = mask + ((size_t)b * T + i) * W;
+      int count = 0;
+      for (int a = i; a != -1; a = par[a]) {  /* v, then P(v), then P(P(v)) ... */
+        row[a / 64] |= (uint64_t)1 << (a % 64);
+        ++count;
+      }
+      depth[(size_t)b * T + i] = count;
+    }
+  }
+  return status;
+}
+
+/* ---------------------------------------------------------------------------
+ * Tree attention for one (sequence b, query head h, node i).
+ * Keys: every committed position j in [0, kv_len[b]) and the cache row
+ * kv_len[b] + a of every a in pi(i).  KV head g = h / (Hq / Hkv).
+ *   s_j = scale * <q, k_j>;  m = max_j s_j;  p_j = exp(s_j - m);
+ *   out = sum_j p_j v_j / sum_j p_j.
+ * Layouts: q [B][T][Hq][D], caches [B][Hkv][L_cap][D], out row of D doubles.
+ * ------------------------------------------------------------------------- */
+int oracle_attention_row(const void* q, const void* k_cache, const void* v_cache,
+                         int dtype, const int32_t* kv_len, const int32_t* parent,
+                         int B, int T, int Hq, int Hkv, int D, int L_cap,
+                         double scale, int b, int h, int i, double* out) {
+  if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= T || Hkv <= 0 ||
+      Hq % Hkv)
+    return ORC_BAD_SIZE;
+  const int32_t* par = parent + (size_t)b * T;
+  if (!tree_is_valid(par, T)) return ORC_BAD_TREE;
+  const int n = kv_len[b];
+  if (n < 0 || n + T > L_cap) return ORC_BAD_SIZE;
+  const int g = h / (Hq / Hkv);
+
+  /* the key rows node i may see */
+  int nkeys = n;
+  for (int a = i; a != -1; a = par[a]) ++nkeys;
+  int* rows = (int*)malloc(sizeof(int) * (size_t)nkeys);
+  double* s = (double*)malloc(sizeof(double) * (size_t)nkeys);
+  if (!rows || !s) { free(rows); free(s); return ORC_BAD_SIZE; }
+  int c = 0;
+  for (int j = 0; j < n; ++j) rows[c++] = j;
+  for (int a = i; a != -1; a = par[a]) rows[c++] = n + a;
+
+  const size_t qoff = (((size_t)b * T + i) * Hq + h) * D;
+  const size_t kvoff = ((size_t)b * Hkv + g) * L_cap;
+  for (int j = 0; j < nkeys; ++j) {
+    double dot = 0.0;
+    for (int d = 0; d < D; ++d)
+      dot += load_elem(q, dtype, qoff + d) *
+             load_elem(k_cache, dtype, (kvoff + rows[j]) * D + d);
+    s[j] = scale * dot;
+  }
+  double m = s[0];
+  for (int j = 1; j < nkeys; ++j)
+    if (s[j] > m) m = s[j];
+  double denom = 0.0;
+  for (int j = 0; j < nkeys; ++j) {
+    s[j] = exp(s[j] - m);
+    denom += s[j];
+  }
+  for (int d = 0; d < D; ++d) {
+    double acc = 0.0;
+    for (int j = 0; j < nkeys; ++j)
+      acc += s[j] * load_elem(v_cache, dtype, (kvoff + rows[j]) * D + d);
+    out[d] = acc / denom;
+  }
+  free(rows);
+  free(s);
+  return ORC_OK;
+}
+
+/* All rows; out is [B][T][Hq][D] doubles. */
+int oracle_tree_attention(const void* q, const void* k_cache, const void* v_cache,
+                          int dtype, const int32_t* kv_len, const int32_t* parent,
+                          int B, int T, int Hq, int Hkv, int D, int L_cap,
+                          double scale, double* out) {
+  for (int b = 0; b < B; ++b)
+    for (int i = 0; i < T; ++i)
+      for (int h = 0; h < Hq; ++h) {
+        int st = oracle_attention_row(q, k_cache, v_cache, dtype, kv_len, parent,
+                                      B, T, Hq, Hkv, D, L_cap, scale, b, h, i,
+                                      out + (((size_t)b * T + i) * Hq + h) * D);
+        if (st) return st;
+      }
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * Top-k / argmax per row: sort positions by value descending, ties by the
+ * lower position (values compared as fp64, so -0.0 and +0.0 are equal).
+ * idx/val may be NULL; val receives the row's own values.
+ * ------------------------------------------------------------------------- */
+typedef struct { double v; int32_t i; } orc_entry;
+
+static int orc_cmp(const void* pa, const void* pb) {
+  const orc_entry* a = (const orc_entry*)pa;
+  const orc_entry* b = (const orc_entry*)pb;
+  if (a->v > b->v) return -1;
+  if (a->v < b->v) return 1;
+  return (a->i > b->i) - (a->i < b->i);
+}
+
+int oracle_topk(const void* logits, int dtype, int R, int V, long long ld, int k,
+                int32_t* argmax, int32_t* idx, double* val) {
+  if (R < 0 || V < 1 || k < 1 || k > V || ld < V) return ORC_BAD_SIZE;
+  orc_entry* e = (orc_entry*)malloc(sizeof(orc_entry) * (size_t)V);
+  if (!e) return ORC_BAD_SIZE;
+  for (int r = 0; r < R; ++r) {
+    for (int j = 0; j < V; ++j) {
+      e[j].v = load_elem(logits, dtype, (size_t)r * (size_t)ld + j);
+      e[j].i = j;
+    }
+    qsort(e, (size_t)V, sizeof(orc_entry), orc_cmp);
+    if (argmax) argmax[r] = e[0].i;
+    for (int t = 0; t < k; ++t) {
+      if (idx) idx[(size_t)r * k + t] = e[t].i;
+      if (val) val[(size_t)r * k + t] = e[t].v;
+    }
+  }
+  free(e);
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * Greedy verification (Sec. 3.2).  Verification token of node n is the argmax
+ * of its logits row (row n+1; row 0 belongs to the last committed token, the
+ * parent of every root).  Edge (P(c), c) is eligible iff the parent's
+ * verification token equals token[c].  A node is accepted iff every edge on
+ * its root path is eligible.  The accepted length k is the largest depth of an
+ * accepted node; the terminal is the lowest-index accepted node of that depth.
+ * X' = tokens of the terminal's root path (shallowest first) followed by the
+ * terminal's verification token (argmax[0] when nothing is accepted).
+ * accept_nodes [B][T] and out_tokens [B][T+1] are padded with -1.
+ * ------------------------------------------------------------------------- */
+int oracle_verify(const int32_t* argmax, const int32_t* tokens,
+                  const int32_t* parent, const int32_t* tree_len, int B, int T,
+                  int32_t* accept_len, int32_t* accept_nodes, int32_t* out_tokens) {
+  if (B < 0 || T < 1) return ORC_BAD_SIZE;
+  int status = ORC_OK;
+  int* ok = (int*)malloc(sizeof(int) * (size_t)T);
+  int* dep = (int*)malloc(sizeof(int) * (size_t)T);
+  if (!ok || !dep) { free(ok); free(dep); return ORC_BAD_SIZE; }
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int32_t* tok = tokens + (size_t)b * T;
+    const int32_t* am = argmax + (size_t)b * (T + 1);
+    int32_t* an = accept_nodes + (size_t)b * T;
+    int32_t* ot = out_tokens + (size_t)b * (T + 1);
+    for (int i = 0; i < T; ++i) an[i] = -1;
+    for (int i = 0; i <= T; ++i) ot[i] = -1;
+    accept_len[b] = 0;
+    const int n = node_count(tree_len, b, T);
+    if (!tree_is_valid(par, n)) { status = ORC_BAD_TREE; continue; }
+
+    int best = -1;
+    for (int i = 0; i < n; ++i) {
+      /* accepted iff every edge from the committed token down to i is eligible */
+      int acc = 1, d = 0;
+      for (int c = i; c != -1; c = par[c]) {
+        if (tok[c] != am[par[c] + 1]) acc = 0;
+        ++d;
+      }
+      ok[i] = acc;
+      dep[i] = d;
+      if (acc && (best < 0 || d > dep[best])) best = i;
+    }
+    if (best < 0) {
+      ot[0] = am[0];
+      continue;
+    }
+    const int k = dep[best];
+    accept_len[b] = k;
+    int pos = k - 1;
+    for (int c = best; c != -1; c = par[c]) {
+      an[pos] = c;
+      ot[pos] = tok[c];
+      --pos;
+    }
+    ot[k] = am[best + 1];
+  }
+  free(ok);
+  free(dep);
+  return status;
+}
+
+/* ---------------------------------------------------------------------------
+ * Progressive expansion with top-k children (Sec. 3.1; App. A top-k).
+ *   1. Node v (index order) offers topk_idx[v+1][0..k-1] as children.
+ *      A node at depth d only grows if d + 1 <= d_max; it stops once it has
+ *      width_sched[d] children (existing ones included).  A candidate equal to
+ *      the token of a child v already has (old or just added) is the same node
+ *      and is skipped.  The committed token (row 0) is not expanded.
+ *   2. The grown tree is renumbered breadth-first: by depth; within a depth,
+ *      by the new number of the parent; within a parent, old children in old
+ *      index order, then new children in candidate order.  Roots keep their
+ *      old relative order.
+ *   3. The first T_max nodes are kept (a breadth-first prefix keeps every
+ *      kept node's parent).  Slots beyond tree_len_next hold -1.
+ * width_sched has d_max entries (entry 0 would be the number of roots and is
+ * not used here).
+ * ------------------------------------------------------------------------- */
+int oracle_expand(const int32_t* parent, const int32_t* tokens,
+                  const int32_t* tree_len, int B, int T, const int32_t* topk_idx,
+                  int k, const int32_t* width_sched, int d_max, int T_max,
+                  int32_t* parent_next, int32_t* tokens_next,
+                  int32_t* tree_len_next) {
+  if (B < 0 || T < 1 || k < 1 || d_max < 1 || T_max < 1) return ORC_BAD_SIZE;
+  int status = ORC_OK;
+  const int cap = T * (k + 1);
+  /* grown tree: old nodes 0..n-1, then new nodes */
+  int* gpar = (int*)malloc(sizeof(int) * (size_t)cap);
+  int* gtok = (int*)malloc(sizeof(int) * (size_t)cap);
+  int* gdep = (int*)malloc(sizeof(int) * (size_t)cap);
+  int* newid = (int*)malloc(sizeof(int) * (size_t)cap);
+  int* order = (int*)malloc(sizeof(int) * (size_t)cap);
+  if (!gpar || !gtok || !gdep || !newid || !order) {
+    free(gpar); free(gtok); free(gdep); free(newid); free(order);
+    return ORC_BAD_SIZE;
+  }
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int32_t* tok = tokens + (size_t)b * T;
+    int32_t* pn = parent_next + (size_t)b * T_max;
+    int32_t* tn = tokens_next + (size_t)b * T_max;
+    for (int i = 0; i < T_max; ++i) { pn[i] = -1; tn[i] = -1; }
+    tree_len_next[b] = 0;
+    const int n = node_count(tree_len, b, T);
+    if (!tree_is_valid(par, n)) { status = ORC_BAD_TREE; continue; }
+
+    int total = 0;
+    for (int i = 0; i < n; ++i) {
+      gpar[total] = par[i];
+      gtok[total] = tok[i];
+      gdep[total] = (par[i] < 0) ? 1 : gdep[par[i]] + 1;
+      ++total;
+    }
+    /* step 1: candidate children */
+    for (int v = 0; v < n; ++v) {
+      const int d = gdep[v];
+      if (d + 1 > d_max) continue;
+      int nchild = 0;
+      for (int c = 0; c < total; ++c)
+        if (gpar[c] == v) ++nchild;
+      for (int r = 0; r < k; ++r) {
+        if (nchild >= width_sched[d]) break;
+        const int cand = topk_idx[((size_t)b * (T + 1) + v + 1) * k + r];
+        int dup = 0;
+        for (int c = 0; c < total; ++c)
+          if (gpar[c] == v && gtok[c] == cand) dup = 1;
+        if (dup) continue;
+        gpar[total] = v;
+        gtok[total] = cand;
+        gdep[total] = d + 1;
+        ++total;
+        ++nchild;
+      }
+    }
+    /* step 2: breadth-first renumbering.  Grown-tree ids of a parent's
+     * children increase in exactly the stated order (old children have
+     * ids < n in index order, new ones follow in candidate order), so a stable
+     * pass over ids in increasing order per parent gives the order. */
+    int cnt = 0;
+    for (int c = 0; c < total; ++c)
+      if (gpar[c] == -1) { order[cnt] = c; newid[c] = cnt; ++cnt; }
+    for (int head = 0; head < cnt; ++head) {
+      const int p = order[head];
+      for (int c = 0; c < total; ++c)
+        if (gpar[c] == p) { order[cnt] = c; newid[c] = cnt; ++cnt; }
+    }
+    /* step 3: keep the first T_max */
+    const int keep = cnt < T_max ? cnt : T_max;
+    for (int t = 0; t < keep; ++t) {
+      const int c = order[t];
+      pn[t] = gpar[c] < 0 ? -1 : newid[gpar[c]];
+      tn[t] = gtok[c];
+    }
+    tree_len_next[b] = keep;
+  }
+  free(gpar); free(gtok); free(gdep); free(newid); free(order);
+  return status;
+}

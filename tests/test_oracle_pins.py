@@ -1,0 +1,463 @@
+"""Pins for the CPU oracle: each check compares it with something other than
+itself (closed forms, torch SDPA / numpy library routines on special cases,
+brute force on tiny inputs, the generator's planted path, hand-derived
+fixtures in tests/golden/).  CPU only."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _bits(mask_row):
+    out = set()
+    for w, word in enumerate(mask_row):
+        word = int(word)
+        for j in range(64):
+            if word >> j & 1:
+                out.add(64 * w + j)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# ancestor masks
+# ---------------------------------------------------------------------------
+def test_mask_chain_closed_form():
+    T = 130  # spans three 64-bit words
+    parent, _ = W.tree_chain(T)
+    mask, depth = O.tree_mask(parent[None])
+    for i in range(T):
+        assert _bits(mask[0, i]) == set(range(i + 1))
+    assert (depth[0] == np.arange(1, T + 1)).all()
+
+
+def test_mask_star_identity():
+    T = 70
+    parent, _ = W.tree_star(T)
+    mask, depth = O.tree_mask(parent[None])
+    for i in range(T):
+        assert _bits(mask[0, i]) == {i}
+    assert (depth == 1).all()
+
+
+def test_mask_heap_binary_tree_closed_form():
+    # heap numbering: node i > 0 has parent (i-1)//2; the ancestors of i are
+    # ((i+1) >> s) - 1 for s = 0..bit_length(i+1)-1
+    T = 127
+    parent = np.array([-1] + [(i - 1) // 2 for i in range(1, T)], np.int32)
+    mask, depth = O.tree_mask(parent[None])
+    for i in range(T):
+        n = i + 1
+        expect = {(n >> s) - 1 for s in range(n.bit_length())}
+        assert _bits(mask[0, i]) == expect
+        assert depth[0, i] == n.bit_length()
+
+
+def test_mask_golden_and_tree_len():
+    g = _golden("verify_example.json")
+    for case in g["cases"]:
+        par = np.array(case["parent"], np.int32)[None]
+        mask, depth = O.tree_mask(par)
+        assert mask[0, :, 0].tolist() == case["mask"]
+        assert depth[0].tolist() == case["depth"]
+    par = np.array([[-1, 0, 1, 2]], np.int32)
+    mask, depth = O.tree_mask(par, tree_len=np.array([2], np.int32))
+    assert mask[0, :, 0].tolist() == [1, 3, 0, 0]
+    assert depth[0].tolist() == [1, 2, 0, 0]
+
+
+@pytest.mark.parametrize("bad", [[-1, 1], [0, -1], [-1, -2], [-1, 0, 5]])
+def test_mask_rejects_bad_tree(bad):
+    with pytest.raises(O.OracleError):
+        O.tree_mask(np.array([bad], np.int32))
+
+
+def test_mask_random_invariants():
+    rng = np.random.default_rng(5)
+    for T in (1, 2, 63, 64, 65, 200):
+        par, level = W.tree_uniform(rng, T)
+        mask, depth = O.tree_mask(par[None])
+        assert (depth[0] == level).all()  # generator's own level count
+        for i in range(T):
+            s = _bits(mask[0, i])
+            assert i in s and max(s) == i
+            if par[i] >= 0:
+                assert _bits(mask[0, par[i]]) < s
+
+
+# ---------------------------------------------------------------------------
+# tree attention: special cases that reduce to plain decode attention
+# (torch SDPA in fp64 on the CPU, no mask, keys selected per query)
+# ---------------------------------------------------------------------------
+def _sdpa_one(q, K, V, scale):
+    # q [D], K/V [n][D] -> [D]
+    qt = torch.from_numpy(q)[None, None, None]
+    kt = torch.from_numpy(np.ascontiguousarray(K))[None, None]
+    vt = torch.from_numpy(np.ascontiguousarray(V))[None, None]
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=scale)
+    return o[0, 0, 0].numpy()
+
+
+def _spec(**kw):
+    base = dict(B=1, Hq=2, Hkv=2, D=16, kv_len=20, T=6, tree="uniform", V=50,
+                dtype="f32", plant=None, k=2)
+    base.update(kw)
+    return base
+
+
+def _check_against_key_sets(w, keysets, scale=None, tol=1e-12):
+    """keysets(b, i) -> list of cache rows node i of sequence b sees."""
+    scale = w.scale if scale is None else scale
+    out = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, scale)
+    q = W.to_f64(w.q, w.dtype)
+    kc = W.to_f64(w.k_cache, w.dtype)
+    vc = W.to_f64(w.v_cache, w.dtype)
+    G = w.Hq // w.Hkv
+    for b in range(w.B):
+        for i in range(w.T):
+            rows = keysets(b, i)
+            for h in range(w.Hq):
+                g = h // G
+                ref = _sdpa_one(q[b, i, h], kc[b, g, rows], vc[b, g, rows], scale)
+                np.testing.assert_allclose(out[b, i, h], ref, rtol=0, atol=tol)
+
+
+def test_attention_chain_is_causal_decode():
+    w = W.make_workload(_spec(tree="chain", T=9, kv_len=17), seed=1)
+    n = int(w.kv_len[0])
+    _check_against_key_sets(w, lambda b, i: list(range(n + i + 1)))
+
+
+def test_attention_single_node_is_decode():
+    w = W.make_workload(_spec(tree="chain", T=1, kv_len=33, Hq=4, Hkv=4), seed=2)
+    n = int(w.kv_len[0])
+    _check_against_key_sets(w, lambda b, i: list(range(n + 1)))
+
+
+def test_attention_star_is_independent_queries():
+    w = W.make_workload(_spec(tree="star", T=7, kv_len=12), seed=3)
+    n = int(w.kv_len[0])
+    _check_against_key_sets(w, lambda b, i: list(range(n)) + [n + i])
+
+
+def test_attention_gqa_ragged_bf16_chain():
+    # 4 query heads share 2 KV heads; two sequences with different prefixes;
+    # bf16 inputs widened exactly; non-default scale
+    w = W.make_workload(_spec(B=2, Hq=4, Hkv=2, tree="chain", T=5,
+                              kv_len=[9, 0], dtype="bf16"), seed=4)
+    _check_against_key_sets(
+        w, lambda b, i: list(range(int(w.kv_len[b]) + i + 1)), scale=0.37)
+
+
+def test_attention_heap_tree_selected_keys():
+    # binary heap tree: node i sees the prefix and its heap ancestors
+    T = 15
+    w = W.make_workload(_spec(tree="star", T=T, kv_len=5), seed=6)
+    w.parent[0] = np.array([-1] + [(i - 1) // 2 for i in range(1, T)], np.int32)
+    n = int(w.kv_len[0])
+
+    def rows(b, i):
+        m = i + 1
+        return list(range(n)) + sorted(n + (m >> s) - 1 for s in range(m.bit_length()))
+    _check_against_key_sets(w, rows)
+
+
+def test_attention_relabel_invariance():
+    # renumbering the tree in another topological order (and moving the tree
+    # rows of the cache with it) permutes the outputs the same way
+    w = W.make_workload(_spec(T=12, kv_len=8, Hq=4, Hkv=2), seed=7)
+    par = w.parent[0]
+    T = w.T
+    # random topological order: repeatedly pick a random node whose parent is placed
+    rng = np.random.default_rng(0)
+    placed, order = set(), []
+    while len(order) < T:
+        ready = [i for i in range(T) if i not in placed and (par[i] < 0 or par[i] in placed)]
+        c = ready[rng.integers(len(ready))]
+        order.append(c)
+        placed.add(c)
+    new_of = {old: new for new, old in enumerate(order)}
+    par2 = np.array([-1 if par[o] < 0 else new_of[int(par[o])] for o in order], np.int32)
+    n = int(w.kv_len[0])
+    q2 = w.q[:, order]
+    k2 = w.k_cache.copy()
+    v2 = w.v_cache.copy()
+    k2[:, :, n:n + T] = w.k_cache[:, :, n + np.array(order)]
+    v2[:, :, n:n + T] = w.v_cache[:, :, n + np.array(order)]
+    o1 = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    o2 = O.tree_attention(q2, k2, v2, w.kv_len, par2[None], w.scale)
+    np.testing.assert_allclose(o2[0], o1[0, order], rtol=0, atol=1e-13)
+
+
+def test_attention_rows_match_full():
+    w = W.make_workload(_spec(B=2, kv_len=[4, 11], Hq=4, Hkv=1), seed=8)
+    full = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    rows = [(0, 3, 2), (1, 0, 5), (1, 2, 0)]
+    part = O.attention_rows(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale, rows)
+    for n, (b, h, i) in enumerate(rows):
+        assert np.array_equal(part[n], full[b, i, h])
+
+
+# ---------------------------------------------------------------------------
+# top-k / argmax
+# ---------------------------------------------------------------------------
+def test_topk_golden_ties():
+    g = _golden("topk_ties.json")
+    rows = np.array(g["rows"], np.float32)
+    am, idx, val = O.topk(rows, g["k"])
+    assert am.tolist() == g["argmax"]
+    assert idx.tolist() == g["topk_idx"]
+    assert np.array_equal(val, np.array(g["topk_val"]))
+    assert np.signbit(val[0, 4])  # the row's own -0.0 is returned
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_topk_matches_lexsort_and_argmax(dtype):
+    rng = np.random.default_rng(11)
+    R, V, k = 9, 3001, 16
+    x = rng.standard_normal((R, V), dtype=np.float32) * np.float32(1.4)
+    x[:, rng.integers(0, V, 40)] = np.float32(0.0)  # ties, incl. signed zeros
+    x[2, 100:140] = np.float32(-0.0)
+    x[4, :] = np.float32(1.0)
+    arr = W.f32_to_bf16_bits(x) if dtype == "bf16" else x
+    am, idx, val = O.topk(arr, k)
+    xv = W.to_f64(arr, dtype)
+    for r in range(R):
+        order = np.lexsort((np.arange(V), -xv[r]))
+        assert idx[r].tolist() == order[:k].tolist()
+        assert am[r] == np.argmax(xv[r])
+        assert np.array_equal(val[r], xv[r, order[:k]])
+
+
+# ---------------------------------------------------------------------------
+# verification
+# ---------------------------------------------------------------------------
+def _brute_accept(parent, tokens, argmax):
+    """Enumerate every root-to-leaf path; along each path count the eligible
+    prefix; the answer is the longest, lowest terminal index on ties."""
+    T = len(parent)
+    children = {p: [c for c in range(T) if parent[c] == p] for p in range(-1, T)}
+    best = (0, None)
+    paths = []
+
+    def walk(node, path):
+        kids = children[node]
+        if not kids:
+            paths.append(path)
+        for c in kids:
+            walk(c, path + [c])
+    walk(-1, [])
+    for path in paths:
+        depth, prev = 0, -1
+        for c in path:
+            if tokens[c] != argmax[prev + 1]:
+                break
+            depth += 1
+            prev = c
+        if depth == 0:
+            continue
+        term = path[depth - 1]
+        if depth > best[0] or (depth == best[0] and term < best[1]):
+            best = (depth, term)
+    return best
+
+
+def test_verify_golden():
+    g = _golden("verify_example.json")
+    for c in g["cases"]:
+        par = np.array([c["parent"]], np.int32)
+        tok = np.array([c["tokens"]], np.int32)
+        am = np.array([c["argmax"]], np.int32)
+        al, an, ot = O.verify(am, tok, par)
+        assert al[0] == c["accept_len"]
+        assert an[0].tolist() == c["accept_nodes"]
+        assert ot[0].tolist() == c["out_tokens"]
+
+
+def test_verify_brute_force_small_trees():
+    rng = np.random.default_rng(21)
+    for trial in range(400):
+        T = int(rng.integers(1, 9))
+        par, _ = W.tree_uniform(rng, T)
+        V = 3  # tiny vocabulary: many eligible edges and duplicate siblings
+        tok = rng.integers(0, V, T).astype(np.int32)
+        am = rng.integers(0, V, T + 1).astype(np.int32)
+        al, an, ot = O.verify(am[None], tok[None], par[None])
+        depth, term = _brute_accept(par, tok, am)
+        assert al[0] == depth, trial
+        if depth:
+            path = []
+            a = term
+            while a != -1:
+                path.append(a)
+                a = par[a]
+            assert an[0, :depth].tolist() == path[::-1]
+            assert ot[0, depth] == am[term + 1]
+        else:
+            assert ot[0, 0] == am[0]
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama2-7b", "llama2-13b"])
+def test_verify_planted_paths(name):
+    w = W.make_workload(name, kv=False)
+    am, idx, _ = O.topk(w.logits, w.k)
+    al, an, ot = O.verify(am.reshape(w.B, -1), w.tokens, w.parent)
+    for b in range(w.B):
+        d = int(w.planted_depth[b])
+        assert al[b] == d
+        assert an[b, :d].tolist() == w.planted_path[b]
+        assert ot[b, d] == w.planted_bonus[b]
+
+
+def test_verify_ragged_planted():
+    spec = dict(W.CONFIGS["ragged-16"], V=5000, kv_len=4)
+    w = W.make_workload(spec, kv=False)
+    am, _, _ = O.topk(w.logits, 1)
+    al, an, _ = O.verify(am.reshape(w.B, -1), w.tokens, w.parent)
+    assert al.tolist() == w.planted_depth.tolist()
+
+
+def test_verify_tree_len_ignores_tail():
+    par = np.array([[-1, 0, 1, 2]], np.int32)
+    tok = np.array([[1, 2, 3, 4]], np.int32)
+    am = np.array([[1, 2, 3, 4, 9]], np.int32)
+    al, _, ot = O.verify(am, tok, par)
+    assert al[0] == 4 and ot[0, 4] == 9
+    al, an, ot = O.verify(am, tok, par, tree_len=np.array([2], np.int32))
+    assert al[0] == 2 and an[0].tolist() == [0, 1, -1, -1] and ot[0, 2] == 3
+
+
+# ---------------------------------------------------------------------------
+# expansion
+# ---------------------------------------------------------------------------
+def test_expand_golden():
+    g = _golden("expand_example.json")
+    par = np.array([g["parent"]], np.int32)
+    tok = np.array([g["tokens"]], np.int32)
+    ti = np.array([g["topk_idx"]], np.int32)
+    for c in g["cases"]:
+        pn, tn, ln = O.expand(par, tok, ti, g["width_sched"], c["d_max"], c["T_max"])
+        assert pn[0].tolist() == c["parent_next"]
+        assert tn[0].tolist() == c["tokens_next"]
+        assert ln[0] == c["tree_len_next"]
+
+
+def _token_paths(parent, tokens, n):
+    paths = set()
+    for i in range(n):
+        p, a = [], i
+        while a != -1:
+            p.append(int(tokens[a]))
+            a = int(parent[a])
+        paths.add(tuple(p[::-1]))
+    return paths
+
+
+def test_expand_top1_unbounded_is_progressive_expansion():
+    # k=1 with no width or depth limit: every node v gains exactly the child
+    # d_v (its top-1 token) -- V^t = V^{t-1} u {d_v} -- unless a child with
+    # that token exists already; compared as sets of root-to-node token paths
+    rng = np.random.default_rng(31)
+    for trial in range(200):
+        T = int(rng.integers(1, 12))
+        par, _ = W.tree_uniform(rng, T)
+        tok = W.sibling_distinct_tokens(rng, par, 6)
+        d_v = rng.integers(0, 6, T + 1).astype(np.int32)
+        ti = d_v[:, None][None]
+        pn, tn, ln = O.expand(par[None], tok[None], ti, [1000] * 64, 64, 4 * T)
+        n = int(ln[0])
+        old = _token_paths(par, tok, T)
+        grown = set(old)
+        for v in range(T):
+            pv, a = [], v
+            while a != -1:
+                pv.append(int(tok[a]))
+                a = int(par[a])
+            grown.add(tuple(pv[::-1]) + (int(d_v[v + 1]),))
+        assert _token_paths(pn[0], tn[0], n) == grown, trial
+        assert n == len(grown)  # merged-by-value: one node per token path
+
+
+def test_expand_bfs_order_caps_and_truncation():
+    rng = np.random.default_rng(41)
+    for trial in range(200):
+        T = int(rng.integers(1, 14))
+        par, lev = W.tree_uniform(rng, T)
+        tok = W.sibling_distinct_tokens(rng, par, 9)
+        k = int(rng.integers(1, 5))
+        ti = rng.integers(0, 9, (1, T + 1, k)).astype(np.int32)
+        d_max = int(rng.integers(1, 6))
+        width = rng.integers(1, 4, d_max).astype(np.int32)
+        pn, tn, ln = O.expand(par[None], tok[None], ti, width, d_max, 10 * T)
+        n = int(ln[0])
+        p, t = pn[0, :n], tn[0, :n]
+        assert (pn[0, n:] == -1).all() and (tn[0, n:] == -1).all()
+        # parents precede children; parents are non-decreasing (breadth-first)
+        assert all(p[i] < i for i in range(n))
+        assert (np.diff(p) >= 0).all()
+        depth = np.zeros(n, int)
+        for i in range(n):
+            depth[i] = 1 if p[i] < 0 else depth[p[i]] + 1
+        assert (np.diff(depth) >= 0).all()
+        old = _token_paths(par, tok, T)
+        assert old <= _token_paths(p, t, n)
+        for i in range(n):  # depth and width caps hold wherever a node grew
+            kids = [c for c in range(n) if p[c] == i]
+            added = [c for c in kids if tuple(_path_tokens(p, t, c)) not in old]
+            if added:
+                assert depth[i] + 1 <= d_max
+                assert len(kids) <= width[depth[i]]
+        # truncation keeps a breadth-first prefix
+        for T_max in (1, max(1, n // 2), n):
+            pn2, tn2, ln2 = O.expand(par[None], tok[None], ti, width, d_max, T_max)
+            assert ln2[0] == min(n, T_max)
+            assert pn2[0].tolist() == pn[0, :T_max].tolist()
+            assert tn2[0].tolist() == tn[0, :T_max].tolist()
+
+
+def _path_tokens(parent, tokens, i):
+    out, a = [], i
+    while a != -1:
+        out.append(int(tokens[a]))
+        a = int(parent[a])
+    return out[::-1]
+
+
+# ---------------------------------------------------------------------------
+# generator invariants
+# ---------------------------------------------------------------------------
+def test_generator_shapes_and_bfs_truncation():
+    for name, levels in [("llama2-7b", [4, 12, 24, 24]), ("llama2-13b", [5, 20, 60, 11])]:
+        w = W.make_workload(name, kv=False, logits=False)
+        _, depth = O.tree_mask(w.parent)
+        counts = np.bincount(depth[0])[1:]
+        assert counts.tolist() == levels
+    w = W.make_workload("tiny")
+    assert w.q.dtype == np.float32 and w.k_cache.shape == (1, 2, 144, 64)
+    w = W.make_workload(dict(W.CONFIGS["ragged-16"], V=64), logits=True)
+    assert w.kv_len.min() >= 512 and w.kv_len.max() <= 8192
+    assert w.k_cache.dtype == np.uint16
+
+
+def test_bf16_rounding_is_rne():
+    x = np.array([1.0, 1.00390625, 1.01171875, -2.5, 3.0e-3], np.float32)
+    b = W.f32_to_bf16_bits(x)
+    back = W.bf16_bits_to_f32(b)
+    # 1 + 2^-8 is a tie between 1 and 1 + 2^-7: rounds to even (1.0);
+    # 1 + 3*2^-8 is a tie between 1+2^-7 and 1+2^-6: rounds to even (1+2^-6)
+    assert back.tolist()[:4] == [1.0, 1.0, 1.015625, -2.5]
+    assert abs(back[4] - 3.0e-3) <= 3.0e-3 * 2 ** -8
+    assert np.array_equal(W.f32_to_bf16_bits(
+        torch.from_numpy(x).to(torch.bfloat16).float().numpy()), b)
