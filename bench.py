@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Benchmark of one Progressive Tree Drafting step on one MI355X.
+
+A step = the whole hot path over one batch of synthetic inputs, on one stream:
+ptd_build_tree_mask -> ptd_tree_attention (one layer) -> ptd_topk_argmax ->
+ptd_verify -> ptd_expand.  Inputs are seeded synthetic tensors shaped like the
+paper's workloads (Llama-2-7B attention shape by default), resident in HBM
+before timing starts; R input sets totalling >= 1 GiB are rotated so the
+256 MB MALL cannot serve the KV cache from one step to the next.
+
+Prints one JSON line: tree tokens/s (value), us/step, the attention stage's
+achieved HBM bandwidth against the 8 TB/s peak, and the CPU oracle's rate on a
+bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+DEFAULT_WORKLOAD = "llama2-7b"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--rotate-bytes", type=float, default=1.0 * 2**30,
+                    help="total bytes of rotated input sets (cold-cache timing)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU time of the oracle sample (0 disables)")
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_2607_10661_amd", "csrc", "tree_attention.hip")
+    with open(src, "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload, per_launch_alg):
+    """HBM bytes per attention launch from committed rocprofv3 --pmc summaries
+    (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel calibration); None if
+    absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_tree_attention_{workload}.json")
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except OSError:
+        return None
+    if d.get("kernel_source_sha") != kernel_source_hash():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_10661_amd as P
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.make_workload(args.workload)
+    B, T, k = w.B, w.T, w.k
+
+    def cu(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    base = dict(q=cu(w.q), k=cu(w.k_cache), v=cu(w.v_cache), logits=cu(w.logits))
+    set_bytes = sum(t.numel() * t.element_size() for t in base.values())
+    R = max(1, min(64, math.ceil(args.rotate_bytes / set_bytes)))
+    sets = [base] + [{n: t.clone() for n, t in base.items()} for _ in range(R - 1)]
+    parent, tokens, kv_len = cu(w.parent), cu(w.tokens), cu(w.kv_len)
+
+    shape = P.attn_shape(base["q"], base["k"], out_dtype=base["q"].dtype)
+    ws_attn = torch.empty(max(1, P.ptd_tree_attention_workspace_bytes(shape, T)),
+                          dtype=torch.uint8, device=dev)
+    R_rows = B * (T + 1)
+    ws_topk = torch.empty(max(1, P.ptd_topk_workspace_bytes(R_rows, w.V, k)),
+                          dtype=torch.uint8, device=dev)
+    mask = torch.empty((B, T, (T + 63) // 64), dtype=torch.int64, device=dev)
+    depth = torch.empty((B, T), dtype=torch.int32, device=dev)
+    out = torch.empty_like(base["q"])
+    am = torch.empty(R_rows, dtype=torch.int32, device=dev)
+    tidx = torch.empty((R_rows, k), dtype=torch.int32, device=dev)
+    tval = torch.empty((R_rows, k), dtype=torch.float32, device=dev)
+    al = torch.empty(B, dtype=torch.int32, device=dev)
+    an = torch.empty((B, T), dtype=torch.int32, device=dev)
+    ot = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+    pn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
+    tn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
+    ln = torch.empty(B, dtype=torch.int32, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    dt_code = P.PTD_BF16 if w.dtype == "bf16" else P.PTD_F32
+
+    def step(i, ev=None):
+        s = sets[i % R]
+        P.ptd_build_tree_mask(parent, None, B, T, mask, depth, status, sp)
+        if ev is not None:
+            ev[0].record(stream)
+        P.ptd_tree_attention(s["q"], s["k"], s["v"], kv_len, parent, T, out, shape, mask,
+                             ws_attn, ws_attn.numel(), status, sp)
+        if ev is not None:
+            ev[1].record(stream)
+        P.ptd_topk_argmax(s["logits"], dt_code, R_rows, w.V, w.V, k, am, tidx, tval,
+                          ws_topk, ws_topk.numel(), sp)
+        P.ptd_verify(am, tokens, parent, None, B, T, al, an, ot, status, sp)
+        P.ptd_expand(parent, tokens, None, B, T, tidx, k, w.width, w.d_max, w.T_max,
+                     pn, tn, ln, status, sp)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    assert status.item() == 0, P.ptd_status_string(status.item())
+    assert al.cpu().tolist() == w.planted_depth.tolist(), "accepted length mismatch"
+
+    K = args.steps
+    att_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    # host enqueue cost per step (Python + ctypes), to size the pre-roll below
+    torch.cuda.synchronize()
+    h0 = time.perf_counter()
+    for i in range(10):
+        step(i, att_ev[i])
+    host_step_s = (time.perf_counter() - h0) / 10
+    torch.cuda.synchronize()
+    # Keep the GPU busy on a spin kernel while the host enqueues all K steps,
+    # so the timed region measures back-to-back GPU execution, not the host.
+    preroll_cycles = int(host_step_s * K * 1.5 * 2.5e9) + 10_000_000
+    if hasattr(torch.cuda, "_sleep"):
+        torch.cuda._sleep(preroll_cycles)
+    t0.record(stream)
+    for i in range(K):
+        step(args.warmup + i, att_ev[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / K
+    att_ms = np.array([a.elapsed_time(b) for a, b in att_ev])
+    att_avg_s = float(att_ms.mean()) * 1e-3
+    assert status.item() == 0, P.ptd_status_string(status.item())
+
+    alg = W.algorithmic_bytes(w)
+    achieved = alg["attention"] / att_avg_s / 1e9
+    flops = W.attention_flops(w)
+    tokens_per_s = B * T / (ms_step * 1e-3)
+    traffic = load_traffic(args.workload, alg["attention"])
+
+    # CPU oracle on a bounded sample of the same workload: whole steps
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle as O
+        done, t_start = 0, time.perf_counter()
+        while True:
+            O.tree_mask(w.parent)
+            O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+            r_am, r_idx, _ = O.topk(w.logits, k)
+            O.verify(r_am.reshape(B, -1), w.tokens, w.parent)
+            O.expand(w.parent, w.tokens, r_idx.reshape(B, T + 1, k), w.width, w.d_max,
+                     w.T_max)
+            done += 1
+            el = time.perf_counter() - t_start
+            if el >= args.cpu_seconds or el * (done + 1) / done > 3 * args.cpu_seconds:
+                break
+        cpu = {"value": round(B * T * done / el, 3), "unit": "tree tokens/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"{done} whole {args.workload} step(s) (all {B * T} nodes x "
+                         f"{w.Hq} heads, single thread), {el:.1f} s",
+               "us_per_step": round(el / done * 1e6, 1)}
+
+    line = {
+        "metric": "tree tokens/s (tree-attn + top-k + verify + expand step)",
+        "value": round(tokens_per_s, 1),
+        "unit": "tree tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6),
+        "us_per_step": round(ms_step * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded), cold cache: %d rotated input sets" % R,
+        "config": {"workload": args.workload, "B": B, "T": T, "Hq": w.Hq, "Hkv": w.Hkv,
+                   "D": w.D, "kv_len": int(w.kv_len.max()) if B == 1 else w.kv_len.tolist(),
+                   "V": w.V, "k": k},
+        "attention_us": round(att_avg_s * 1e6, 3),
+        "host_enqueue_us_per_step": round(host_step_s * 1e6, 1),
+        "attention_TBps": round(achieved / 1000, 3),
+        "attention_mfma_frac": round(flops / att_avg_s / 2.5e15, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic,
+                     "kernel": "ptd_tree_attention (k_attn_mfma + k_attn_combine)",
+                     "alg_bytes_per_launch": alg["attention"]},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

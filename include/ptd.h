@@ -1,0 +1,222 @@
+/*
+ * ptd.h -- C ABI of the Progressive Tree Drafting hot path on MI355X (gfx950).
+ *
+ * One decoding step of Progressive Tree Drafting (PTD) packs a token tree
+ * after the committed prefix and runs the target model once over it (Sec. 3.1,
+ * Sec. 3.2, Alg. 1 step 2).  This library provides the data-parallel part of
+ * that step, as hand-written HIP kernels:
+ *
+ *   ptd_build_tree_mask  ancestor-or-self bitmasks and depths of the tree
+ *   ptd_tree_attention   tree-masked attention over committed KV + ancestors
+ *   ptd_topk_argmax      per-row argmax / top-k of the verification logits
+ *   ptd_verify           greedy longest accepted path (+ bonus token)
+ *   ptd_expand           progressive expansion with top-k children
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers owned by the caller (stream-ordered;
+ *     the library keeps no pointer after the call returns).  Exceptions are
+ *     marked "host".
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
+ *     means the default stream).  No entry point synchronizes the stream or
+ *     allocates device memory; scratch memory comes from a caller workspace.
+ *   - The return value is a ptd_status.  Host-detectable errors (null pointers,
+ *     sizes, alignment, workspace size) are returned before anything is
+ *     launched.  A failed launch returns PTD_ERR_HIP.  Data-dependent errors
+ *     that only the device can see (a malformed parent array, a KV length that
+ *     does not fit the cache) are written to *dev_status (device int32,
+ *     nullable) with first-error-wins semantics; the caller zeroes it.  After
+ *     a device-reported error the outputs are unspecified.
+ *   - Outputs are bitwise reproducible run to run (no float atomics; partial
+ *     results are combined in a fixed order).
+ *   - Tree arrays: node i of a sequence has parent[i] in [-1, i) (topological
+ *     order); -1 means the node's parent is the last committed token.  The tree
+ *     may be a forest.  Sec. 3.1 "Tree Construction".
+ */
+#ifndef PTD_H
+#define PTD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PTD_F32 = 0,  /* IEEE binary32 */
+  PTD_BF16 = 1  /* bfloat16 (upper half of binary32) */
+} ptd_dtype;
+
+typedef enum {
+  PTD_OK = 0,
+  PTD_ERR_NULL = 1,      /* a required pointer is NULL */
+  PTD_ERR_SHAPE = 2,     /* a size is out of range or inconsistent */
+  PTD_ERR_DTYPE = 3,     /* unsupported dtype combination */
+  PTD_ERR_ALIGN = 4,     /* a pointer or leading dimension is misaligned */
+  PTD_ERR_WORKSPACE = 5, /* workspace missing or too small */
+  PTD_ERR_HIP = 6,       /* a HIP runtime call or kernel launch failed */
+  PTD_ERR_BAD_TREE = 7,  /* device-detected: parent[i] outside [-1, i) */
+  PTD_ERR_KV_LEN = 8     /* device-detected: kv_len < 0 or kv_len + T > L_cap */
+} ptd_status;
+
+#define PTD_MAX_T 1024   /* tree nodes per sequence */
+#define PTD_MAX_K 16     /* top-k */
+#define PTD_MAX_DEPTH 64 /* entries of a width schedule */
+
+/* Attention problem description (host struct, read during the call only). */
+typedef struct {
+  int32_t B;          /* sequences, >= 1 */
+  int32_t Hq;         /* query heads, >= 1 */
+  int32_t Hkv;        /* key/value heads; Hq % Hkv == 0 (GQA group Hq/Hkv) */
+  int32_t D;          /* head dim: 64 or 128 */
+  int32_t L_cap;      /* rows per (sequence, KV head) in the caches */
+  ptd_dtype in_dtype; /* dtype of q, k_cache, v_cache */
+  ptd_dtype out_dtype;/* dtype of out */
+  float scale;        /* softmax scale; 0 selects 1/sqrt(D) */
+} ptd_attn_shape;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* ptd_status_string(int status);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int ptd_version(void);
+
+/*
+ * ptd_build_tree_mask -- ancestor sets pi(v) = {v} u pi(P(v)) and positions
+ * |pi(v)| (Sec. 3.1 "Tree Construction").
+ *   parent    int32 [B][T]
+ *   tree_len  int32 [B] or NULL (NULL: all T nodes are live).  Nodes at index
+ *             >= tree_len[b] are padding: their mask rows and depths are 0.
+ *   mask      uint64 [B][T][W], W = ceil(T/64): bit j of word j/64 of row i is
+ *             set iff node j is i or an ancestor of i.
+ *   depth     int32 [B][T]: |pi(i)| (1 for a root).
+ *   dev_status  PTD_ERR_BAD_TREE if some live parent[i] is outside [-1, i).
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE (B < 1, T < 1 or T > PTD_MAX_T).
+ */
+int ptd_build_tree_mask(const int32_t* parent, const int32_t* tree_len, int32_t B,
+                        int32_t T, uint64_t* mask, int32_t* depth,
+                        int32_t* dev_status, void* stream);
+
+/*
+ * Workspace bytes ptd_tree_attention needs for this shape and tree size
+ * (split-KV partial results, plus room for the masks when mask == NULL).
+ * Returns 0 on invalid arguments.
+ */
+size_t ptd_tree_attention_workspace_bytes(const ptd_attn_shape* shape, int32_t T);
+
+/*
+ * ptd_tree_attention -- each tree node attends to the committed prefix and to
+ * its own ancestors only (Sec. 3.1 "Tree Construction"; the joint forward over
+ * [X; T; C_X] of Sec. 3.2 uses the same mask):
+ *   for sequence b, query head h (KV head g = h / (Hq/Hkv)) and node i,
+ *     keys  S = { rows 0 .. kv_len[b]-1 } u { row kv_len[b] + a : a in pi(i) }
+ *     out[b][i][h] = sum_{j in S} softmax_j(scale * q . k_j) v_j
+ *   q        [B][T][Hq][D]           in_dtype
+ *   k_cache  [B][Hkv][L_cap][D]      in_dtype; tree node i's key is row kv_len[b]+i
+ *   v_cache  [B][Hkv][L_cap][D]      in_dtype; likewise
+ *   kv_len   int32 [B]               committed length; needs kv_len+T <= L_cap
+ *   parent   int32 [B][T]            tree (all T nodes live)
+ *   T        nodes per sequence, 1 .. PTD_MAX_T
+ *   out      [B][T][Hq][D]           out_dtype (fp32 accumulation inside)
+ *   shape    host struct above
+ *   mask     uint64 [B][T][ceil(T/64)] from ptd_build_tree_mask, or NULL to
+ *            have it built into the workspace
+ *   workspace, workspace_bytes: device scratch of at least
+ *            ptd_tree_attention_workspace_bytes(shape, T) bytes, 256-byte aligned
+ * Pointers to q/k/v/out must be 16-byte aligned.  in_dtype bf16 runs on MFMA
+ * (v_mfma_f32_16x16x32_bf16); fp32 inputs run on the vector ALUs.
+ * dev_status: PTD_ERR_BAD_TREE, PTD_ERR_KV_LEN.
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_DTYPE, PTD_ERR_ALIGN,
+ * PTD_ERR_WORKSPACE, PTD_ERR_HIP.
+ */
+int ptd_tree_attention(const void* q, const void* k_cache, const void* v_cache,
+                       const int32_t* kv_len, const int32_t* parent, int32_t T,
+                       void* out, const ptd_attn_shape* shape,
+                       const uint64_t* mask, void* workspace,
+                       size_t workspace_bytes, int32_t* dev_status, void* stream);
+
+/* Workspace bytes ptd_topk_argmax needs (0 on invalid arguments). */
+size_t ptd_topk_workspace_bytes(int32_t R, int32_t V, int32_t k);
+
+/*
+ * ptd_topk_argmax -- greedy verification tokens (the highest-probability
+ * prediction of every node, Sec. 3.2) and the top-k candidates used for child
+ * expansion (App. A), per row of logits.
+ *   logits    [R][ld] of dtype; row r's entries are logits[r*ld .. r*ld+V-1]
+ *   R         rows (B*(T+1) for a step: row 0 of each sequence is the last
+ *             committed token, row i+1 is node i)
+ *   V, ld     vocabulary size (1 .. 2^31-1) and row stride in elements (>= V)
+ *   k         1 .. PTD_MAX_K, k <= V
+ *   argmax    int32 [R]            (required)
+ *   topk_idx  int32 [R][k]         (nullable)
+ *   topk_val  float [R][k]         (nullable) the selected entries' own values,
+ *                                  widened exactly to fp32
+ * Order: value descending; equal values by the lower index; -0.0 equals +0.0.
+ * Logits are expected finite (NaN ordering is unspecified).
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_DTYPE, PTD_ERR_WORKSPACE,
+ * PTD_ERR_HIP.
+ */
+int ptd_topk_argmax(const void* logits, ptd_dtype dtype, int32_t R, int32_t V,
+                    int64_t ld, int32_t k, int32_t* argmax, int32_t* topk_idx,
+                    float* topk_val, void* workspace, size_t workspace_bytes,
+                    void* stream);
+
+/*
+ * ptd_verify -- greedy verification (Sec. 3.2; Alg. 1 steps 5-6).  The edge
+ * (P(c), c) is eligible iff the verification token of P(c) -- argmax row
+ * P(c)+1, row 0 for a root -- equals draft_tokens[c].  A node is accepted iff
+ * all edges on its root path are eligible.  accept_len = largest depth of an
+ * accepted node (0 if none); the terminal is the lowest-index accepted node of
+ * that depth.  X' = the draft tokens of the terminal's root path, shallowest
+ * first, then the bonus token argmax[terminal+1] (argmax[0] if nothing is
+ * accepted).
+ *   argmax        int32 [B][T+1]
+ *   draft_tokens  int32 [B][T]
+ *   parent        int32 [B][T]
+ *   tree_len      int32 [B] or NULL (nodes >= tree_len[b] are ignored)
+ *   accept_len    int32 [B]
+ *   accept_nodes  int32 [B][T]   node ids of the path, -1 padded
+ *   out_tokens    int32 [B][T+1] X' without n_0, -1 padded
+ * dev_status: PTD_ERR_BAD_TREE.
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_HIP.
+ */
+int ptd_verify(const int32_t* argmax, const int32_t* draft_tokens,
+               const int32_t* parent, const int32_t* tree_len, int32_t B,
+               int32_t T, int32_t* accept_len, int32_t* accept_nodes,
+               int32_t* out_tokens, int32_t* dev_status, void* stream);
+
+/*
+ * ptd_expand -- progressive expansion V^t = V^{t-1} u {d_v} with top-k
+ * children (Sec. 3.1 "Progressive Expansion" and "Overhead Constraints";
+ * App. A):
+ *   1. node v (index order) offers topk_idx[b][v+1][0..k-1] as children; a
+ *      node of depth d grows only if d+1 <= d_max, and stops once it has
+ *      width_sched[d] children counting existing ones; a candidate equal to
+ *      the token of one of v's children (existing or just added) is skipped
+ *      (same node, as in the merge of Sec. 3.1 "Draft Extraction").  The
+ *      committed token (row 0) is not expanded.
+ *   2. breadth-first renumbering: by depth, then by the parent's new index,
+ *      then old children in index order before new children in candidate
+ *      order; roots keep their relative order.
+ *   3. the first T_max nodes are kept; slots >= tree_len_next[b] hold -1.
+ *   parent, tokens  int32 [B][T];  tree_len int32 [B] or NULL
+ *   topk_idx        int32 [B][T+1][k] (as written by ptd_topk_argmax)
+ *   width_sched     HOST int32 [d_max]; entry 0 (number of roots) is unused
+ *   d_max           1 .. PTD_MAX_DEPTH;  T_max 1 .. PTD_MAX_T;
+ *                   T*(k+1) <= 16384
+ *   parent_next, tokens_next  int32 [B][T_max];  tree_len_next int32 [B]
+ * dev_status: PTD_ERR_BAD_TREE.
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_HIP.
+ */
+int ptd_expand(const int32_t* parent, const int32_t* tokens,
+               const int32_t* tree_len, int32_t B, int32_t T,
+               const int32_t* topk_idx, int32_t k, const int32_t* width_sched,
+               int32_t d_max, int32_t T_max, int32_t* parent_next,
+               int32_t* tokens_next, int32_t* tree_len_next,
+               int32_t* dev_status, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PTD_H */

@@ -1,0 +1,257 @@
+"""Python binding of libptd.so, the MI355X (gfx950) Progressive Tree Drafting
+hot path.
+
+The functions named ``ptd_*`` mirror the C entry points of ``include/ptd.h``
+one to one: they marshal arguments (torch tensors or raw integer device
+addresses, a HIP stream) and raise :class:`PTDError` on a non-zero status.
+Every step of the path runs in the library's HIP kernels; torch only provides
+device memory and the stream.  There is no CPU fallback: without a built
+``libptd.so`` the import fails.
+
+The lower-case helpers (``tree_mask``, ``tree_attention``, ``topk_argmax``,
+``verify``, ``expand``) allocate outputs with torch and call the entry points.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch  # loads the HIP runtime that libptd.so then shares
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libptd.so")
+
+PTD_F32, PTD_BF16 = 0, 1
+PTD_MAX_T, PTD_MAX_K, PTD_MAX_DEPTH = 1024, 16, 64
+STATUS = {0: "PTD_OK", 1: "PTD_ERR_NULL", 2: "PTD_ERR_SHAPE", 3: "PTD_ERR_DTYPE",
+          4: "PTD_ERR_ALIGN", 5: "PTD_ERR_WORKSPACE", 6: "PTD_ERR_HIP",
+          7: "PTD_ERR_BAD_TREE", 8: "PTD_ERR_KV_LEN"}
+
+
+class PTDError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} "
+                         f"({_lib.ptd_status_string(status).decode()})")
+
+
+class AttnShape(ctypes.Structure):
+    """ptd_attn_shape"""
+    _fields_ = [("B", ctypes.c_int32), ("Hq", ctypes.c_int32),
+                ("Hkv", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("L_cap", ctypes.c_int32), ("in_dtype", ctypes.c_int),
+                ("out_dtype", ctypes.c_int), ("scale", ctypes.c_float)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                      "(hipcc --offload-arch=gfx950)")
+_lib = ctypes.CDLL(LIB_PATH)
+
+_vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+_SIGS = {
+    "ptd_status_string": ([ctypes.c_int], ctypes.c_char_p),
+    "ptd_version": ([], ctypes.c_int),
+    "ptd_build_tree_mask": ([_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp], ctypes.c_int),
+    "ptd_tree_attention_workspace_bytes": ([ctypes.POINTER(AttnShape), _i32], _sz),
+    "ptd_tree_attention": ([_vp, _vp, _vp, _vp, _vp, _i32, _vp, ctypes.POINTER(AttnShape),
+                            _vp, _vp, _sz, _vp, _vp], ctypes.c_int),
+    "ptd_topk_workspace_bytes": ([_i32, _i32, _i32], _sz),
+    "ptd_topk_argmax": ([_vp, ctypes.c_int, _i32, _i32, _i64, _i32, _vp, _vp, _vp, _vp,
+                         _sz, _vp], ctypes.c_int),
+    "ptd_verify": ([_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
+    "ptd_expand": ([_vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp,
+                    _vp, _vp], ctypes.c_int),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, torch.Tensor):
+        return x.data_ptr()
+    return int(x)
+
+
+def _stream(s):
+    if s is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, torch.cuda.Stream):
+        return s.cuda_stream
+    return int(s)
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise PTDError(st, where)
+
+
+# ---------------------------------------------------------------------------
+# entry points (same names and argument order as include/ptd.h)
+# ---------------------------------------------------------------------------
+def ptd_status_string(status: int) -> str:
+    return _lib.ptd_status_string(status).decode()
+
+
+def ptd_version() -> int:
+    return _lib.ptd_version()
+
+
+def ptd_build_tree_mask(parent, tree_len, B, T, mask, depth, dev_status=None, stream=None):
+    _check(_lib.ptd_build_tree_mask(_ptr(parent), _ptr(tree_len), B, T, _ptr(mask),
+                                    _ptr(depth), _ptr(dev_status), _stream(stream)),
+           "ptd_build_tree_mask")
+
+
+def ptd_tree_attention_workspace_bytes(shape: AttnShape, T: int) -> int:
+    return _lib.ptd_tree_attention_workspace_bytes(ctypes.byref(shape), T)
+
+
+def ptd_tree_attention(q, k_cache, v_cache, kv_len, parent, T, out, shape: AttnShape,
+                       mask=None, workspace=None, workspace_bytes=0, dev_status=None,
+                       stream=None):
+    _check(_lib.ptd_tree_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_len),
+                                   _ptr(parent), T, _ptr(out), ctypes.byref(shape),
+                                   _ptr(mask), _ptr(workspace), workspace_bytes,
+                                   _ptr(dev_status), _stream(stream)),
+           "ptd_tree_attention")
+
+
+def ptd_topk_workspace_bytes(R: int, V: int, k: int) -> int:
+    return _lib.ptd_topk_workspace_bytes(R, V, k)
+
+
+def ptd_topk_argmax(logits, dtype, R, V, ld, k, argmax, topk_idx=None, topk_val=None,
+                    workspace=None, workspace_bytes=0, stream=None):
+    _check(_lib.ptd_topk_argmax(_ptr(logits), dtype, R, V, ld, k, _ptr(argmax),
+                                _ptr(topk_idx), _ptr(topk_val), _ptr(workspace),
+                                workspace_bytes, _stream(stream)),
+           "ptd_topk_argmax")
+
+
+def ptd_verify(argmax, draft_tokens, parent, tree_len, B, T, accept_len, accept_nodes,
+               out_tokens, dev_status=None, stream=None):
+    _check(_lib.ptd_verify(_ptr(argmax), _ptr(draft_tokens), _ptr(parent), _ptr(tree_len),
+                           B, T, _ptr(accept_len), _ptr(accept_nodes), _ptr(out_tokens),
+                           _ptr(dev_status), _stream(stream)),
+           "ptd_verify")
+
+
+def ptd_expand(parent, tokens, tree_len, B, T, topk_idx, k, width_sched, d_max, T_max,
+               parent_next, tokens_next, tree_len_next, dev_status=None, stream=None):
+    ws = (ctypes.c_int32 * max(1, len(width_sched)))(*[int(x) for x in width_sched])
+    if len(width_sched) < d_max:
+        raise ValueError("width_sched needs d_max entries")
+    _check(_lib.ptd_expand(_ptr(parent), _ptr(tokens), _ptr(tree_len), B, T, _ptr(topk_idx),
+                           k, ctypes.cast(ws, _vp), d_max, T_max, _ptr(parent_next),
+                           _ptr(tokens_next), _ptr(tree_len_next), _ptr(dev_status),
+                           _stream(stream)),
+           "ptd_expand")
+
+
+# ---------------------------------------------------------------------------
+# tensor helpers: allocate outputs, check device/dtype/contiguity, call
+# ---------------------------------------------------------------------------
+def _need_gpu(*ts):
+    for t in ts:
+        if t is not None and (not isinstance(t, torch.Tensor) or not t.is_cuda
+                              or not t.is_contiguous()):
+            raise ValueError("expected contiguous GPU tensors")
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return PTD_BF16
+    if t.dtype == torch.float32:
+        return PTD_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def attn_shape(q: torch.Tensor, k_cache: torch.Tensor, out_dtype=None,
+               scale: float = 0.0) -> AttnShape:
+    B, T, Hq, D = q.shape
+    _, Hkv, L_cap, _ = k_cache.shape
+    od = _dtype_code(q) if out_dtype is None else (
+        PTD_BF16 if out_dtype == torch.bfloat16 else PTD_F32)
+    return AttnShape(B, Hq, Hkv, D, L_cap, _dtype_code(q), od, float(scale))
+
+
+def tree_mask(parent: torch.Tensor, tree_len: Optional[torch.Tensor] = None,
+              dev_status: Optional[torch.Tensor] = None):
+    _need_gpu(parent, tree_len)
+    B, T = parent.shape
+    mask = torch.empty((B, T, (T + 63) // 64), dtype=torch.int64, device=parent.device)
+    depth = torch.empty((B, T), dtype=torch.int32, device=parent.device)
+    ptd_build_tree_mask(parent, tree_len, B, T, mask, depth, dev_status)
+    return mask, depth
+
+
+def tree_attention(q, k_cache, v_cache, kv_len, parent, mask=None, out=None,
+                   out_dtype=None, scale: float = 0.0, workspace=None,
+                   dev_status=None):
+    _need_gpu(q, k_cache, v_cache, kv_len, parent, mask)
+    B, T, Hq, D = q.shape
+    shape = attn_shape(q, k_cache, out_dtype, scale)
+    if out is None:
+        od = torch.bfloat16 if shape.out_dtype == PTD_BF16 else torch.float32
+        out = torch.empty((B, T, Hq, D), dtype=od, device=q.device)
+    nbytes = ptd_tree_attention_workspace_bytes(shape, T)
+    if workspace is None and nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    ptd_tree_attention(q, k_cache, v_cache, kv_len, parent, T, out, shape, mask,
+                       workspace, 0 if workspace is None else workspace.numel(),
+                       dev_status)
+    return out
+
+
+def topk_argmax(logits: torch.Tensor, k: int, with_values: bool = True, workspace=None):
+    """logits [R][V] with unit stride along V (a row stride ld >= V is allowed),
+    or any contiguous [..][V]; returns (argmax [R], idx [R][k], val [R][k])."""
+    if not logits.is_cuda:
+        raise ValueError("expected GPU logits")
+    if logits.dim() != 2:
+        logits = logits.reshape(-1, logits.shape[-1])
+    if logits.stride(1) != 1:
+        raise ValueError("logits need unit stride along the vocabulary")
+    R, V = logits.shape
+    ld = logits.stride(0)
+    dev = logits.device
+    am = torch.empty(R, dtype=torch.int32, device=dev)
+    idx = torch.empty((R, k), dtype=torch.int32, device=dev)
+    val = torch.empty((R, k), dtype=torch.float32, device=dev) if with_values else None
+    nbytes = ptd_topk_workspace_bytes(R, V, k)
+    if workspace is None and nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    ptd_topk_argmax(logits, _dtype_code(logits), R, V, ld, k, am, idx, val, workspace,
+                    0 if workspace is None else workspace.numel())
+    return am, idx, val
+
+
+def verify(argmax, draft_tokens, parent, tree_len=None, dev_status=None):
+    _need_gpu(argmax, draft_tokens, parent, tree_len)
+    B, T = parent.shape
+    dev = parent.device
+    al = torch.empty(B, dtype=torch.int32, device=dev)
+    an = torch.empty((B, T), dtype=torch.int32, device=dev)
+    ot = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+    ptd_verify(argmax, draft_tokens, parent, tree_len, B, T, al, an, ot, dev_status)
+    return al, an, ot
+
+
+def expand(parent, tokens, topk_idx, width_sched: Sequence[int], d_max: int, T_max: int,
+           tree_len=None, dev_status=None):
+    _need_gpu(parent, tokens, topk_idx, tree_len)
+    B, T = parent.shape
+    k = topk_idx.shape[-1]
+    dev = parent.device
+    pn = torch.empty((B, T_max), dtype=torch.int32, device=dev)
+    tn = torch.empty((B, T_max), dtype=torch.int32, device=dev)
+    ln = torch.empty(B, dtype=torch.int32, device=dev)
+    ptd_expand(parent, tokens, tree_len, B, T, topk_idx, k, width_sched, d_max, T_max,
+               pn, tn, ln, dev_status)
+    return pn, tn, ln

@@ -1,0 +1,101 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every symbol include/ptd.h declares, sizes workspaces, and rejects bad
+arguments before launching anything (all calls here fail validation, so no
+kernel is launched and no device pointer is touched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_10661_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "ptd.h")).read()
+    return sorted(set(re.findall(r"^(?:int|size_t|const char\*)\s+(ptd_\w+)\(", src, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert "ptd_tree_attention" in names and len(names) >= 9
+    lib = ctypes.CDLL(P.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+        assert hasattr(P, n), f"binding lacks {n}"
+
+
+def test_status_strings():
+    for code in range(0, 9):
+        assert P.ptd_status_string(code) != "unknown status"
+    assert P.ptd_status_string(99) == "unknown status"
+    assert P.ptd_version() >= 100
+
+
+def _shape(B=1, Hq=32, Hkv=32, D=128, L=2112, dt=P.PTD_BF16, od=P.PTD_BF16):
+    return P.AttnShape(B, Hq, Hkv, D, L, dt, od, 0.0)
+
+
+def test_attention_workspace_sizes():
+    # splits * rows * (D + 2) fp32 partials, plus the masks, each 256-aligned
+    n = P.ptd_tree_attention_workspace_bytes(_shape(), 64)
+    assert n > 0 and n % 256 == 0
+    assert n >= 64 * 32 * 130 * 4  # at least one split's partials
+    assert P.ptd_tree_attention_workspace_bytes(_shape(dt=P.PTD_F32, D=64, Hq=2, Hkv=2, L=144),
+                                                16) == 256  # masks only (no split)
+    assert P.ptd_tree_attention_workspace_bytes(_shape(Hq=30, Hkv=8), 64) == 0  # Hq % Hkv
+    assert P.ptd_tree_attention_workspace_bytes(_shape(D=96), 64) == 0
+    assert P.ptd_tree_attention_workspace_bytes(_shape(), 0) == 0
+    assert P.ptd_tree_attention_workspace_bytes(_shape(), P.PTD_MAX_T + 1) == 0
+    assert P.ptd_tree_attention_workspace_bytes(_shape(L=32), 64) == 0  # L_cap < T
+
+
+def test_topk_workspace_sizes():
+    assert P.ptd_topk_workspace_bytes(65, 32000, 4) > 0
+    assert P.ptd_topk_workspace_bytes(2048, 32000, 4) == 0  # one slice per row
+    assert P.ptd_topk_workspace_bytes(4, 10, 11) == 0       # k > V
+    assert P.ptd_topk_workspace_bytes(4, 100, 17) == 0      # k > PTD_MAX_K
+
+
+FAKE = 1 << 20  # aligned non-null address; every call below fails validation first
+
+
+def _err(fn, *a, **kw):
+    with pytest.raises(P.PTDError) as e:
+        fn(*a, stream=0, **kw)
+    return e.value.status
+
+
+def test_attention_validation():
+    s = _shape()
+    assert _err(P.ptd_tree_attention, None, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 1
+    assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE, s) == 2
+    assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE,
+                _shape(Hq=3, Hkv=2)) == 2
+    bad = _shape()
+    bad.in_dtype = 7
+    assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, bad) == 3
+    assert _err(P.ptd_tree_attention, FAKE + 2, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 4
+    # workspace missing / too small
+    assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 5
+    assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s,
+                workspace=FAKE, workspace_bytes=16) == 5
+
+
+def test_topk_verify_expand_mask_validation():
+    assert _err(P.ptd_topk_argmax, None, P.PTD_BF16, 4, 100, 100, 4, FAKE) == 1
+    assert _err(P.ptd_topk_argmax, FAKE, 5, 4, 100, 100, 4, FAKE) == 3
+    assert _err(P.ptd_topk_argmax, FAKE, P.PTD_BF16, 4, 100, 99, 4, FAKE) == 2   # ld < V
+    assert _err(P.ptd_topk_argmax, FAKE, P.PTD_BF16, 4, 100, 100, 17, FAKE) == 2
+    assert _err(P.ptd_topk_argmax, FAKE + 1, P.PTD_BF16, 4, 100, 100, 4, FAKE) == 4
+    assert _err(P.ptd_topk_argmax, FAKE, P.PTD_BF16, 65, 32000, 32000, 4, FAKE) == 5
+    assert _err(P.ptd_verify, FAKE, FAKE, None, None, 1, 4, FAKE, FAKE, FAKE) == 1
+    assert _err(P.ptd_verify, FAKE, FAKE, FAKE, None, 1, 0, FAKE, FAKE, FAKE) == 2
+    assert _err(P.ptd_verify, FAKE, FAKE, FAKE, None, 1, P.PTD_MAX_T + 1, FAKE, FAKE, FAKE) == 2
+    assert _err(P.ptd_expand, FAKE, FAKE, None, 1, 4, FAKE, 0, [4], 1, 8, FAKE, FAKE, FAKE) == 2
+    assert _err(P.ptd_expand, FAKE, FAKE, None, 1, 4, FAKE, 2, [4] * 65, 65, 8, FAKE, FAKE,
+                FAKE) == 2
+    assert _err(P.ptd_build_tree_mask, FAKE, None, 0, 4, FAKE, FAKE) == 2
+    assert _err(P.ptd_build_tree_mask, None, None, 1, 4, FAKE, FAKE) == 1

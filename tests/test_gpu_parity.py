@@ -1,0 +1,324 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle on
+the same seeded inputs.  Integer results (masks, depths, indices, accepted
+paths, expanded trees) must be bit-exact; attention must be within max-abs
+2e-3 for bf16 inputs and 1e-5 for fp32 inputs (fp32 accumulation)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-3, "f32": 1e-5}
+
+
+@pytest.fixture(scope="module")
+def P():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_10661_amd as lib
+    return lib
+
+
+def cu(a: np.ndarray) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def status_buf():
+    return torch.zeros(1, dtype=torch.int32, device="cuda")
+
+
+# ---------------------------------------------------------------------------
+# ancestor masks
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("T", [1, 2, 63, 64, 65, 130, 1024])
+def test_mask_random_trees(P, T):
+    rng = np.random.default_rng(T)
+    par = np.stack([W.tree_uniform(rng, T)[0], W.tree_chain(T)[0], W.tree_star(T)[0]])
+    tl = np.array([T, max(1, T // 2), T], np.int32)
+    for tree_len in (None, tl):
+        m_ref, d_ref = O.tree_mask(par, tree_len)
+        st = status_buf()
+        m, d = P.tree_mask(cu(par), None if tree_len is None else cu(tree_len), st)
+        torch.cuda.synchronize()
+        assert st.item() == 0
+        assert np.array_equal(m.cpu().numpy().view(np.uint64), m_ref)
+        assert np.array_equal(d.cpu().numpy(), d_ref)
+
+
+def test_mask_reports_bad_tree(P):
+    par = np.array([[-1, 0, 2, 1], [-1, -1, 0, 1]], np.int32)
+    st = status_buf()
+    P.tree_mask(cu(par), None, st)
+    torch.cuda.synchronize()
+    assert st.item() == 7
+
+
+# ---------------------------------------------------------------------------
+# top-k / argmax
+# ---------------------------------------------------------------------------
+def _topk_case(P, arr, k, ld=None):
+    R, V = arr.shape
+    if ld is not None and ld > V:
+        buf = np.zeros((R, ld), arr.dtype)
+        buf[:, :V] = arr
+        t = cu(buf)[:, :V]
+    else:
+        t = cu(arr)
+    am, idx, val = P.topk_argmax(t, k)
+    torch.cuda.synchronize()
+    r_am, r_idx, r_val = O.topk(arr, k)
+    assert np.array_equal(am.cpu().numpy(), r_am)
+    assert np.array_equal(idx.cpu().numpy(), r_idx)
+    v = val.cpu().numpy().astype(np.float64)
+    assert np.array_equal(v, r_val)
+    assert np.array_equal(np.signbit(v), np.signbit(r_val))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("R,V,k", [(1, 1, 1), (3, 7, 5), (17, 1000, 4), (65, 32000, 4),
+                                   (97, 32000, 5), (8, 32003, 16), (5, 128256, 8),
+                                   (1100, 4099, 2)])
+def test_topk_random(P, dtype, R, V, k):
+    rng = np.random.default_rng(R * 7 + V + k)
+    x = rng.standard_normal((R, V), dtype=np.float32) * np.float32(1.41)
+    # injected ties (bf16 makes more on its own) and signed zeros
+    cols = rng.integers(0, V, min(V, 50))
+    x[:, cols] = x[:, cols[:1]]
+    x[::2, rng.integers(0, V, min(V, 9))] = np.float32(-0.0)
+    x[1::2, rng.integers(0, V, min(V, 9))] = np.float32(0.0)
+    arr = W.f32_to_bf16_bits(x) if dtype == "bf16" else x
+    _topk_case(P, arr, k)
+
+
+def test_topk_all_equal_and_strided(P):
+    x = np.full((6, 5000), 0.75, np.float32)
+    x[3, 4999] = 0.8
+    _topk_case(P, W.f32_to_bf16_bits(x), 8)
+    rng = np.random.default_rng(1)
+    x = W.f32_to_bf16_bits(rng.standard_normal((9, 3001), dtype=np.float32))
+    _topk_case(P, x, 6, ld=3008)   # 16-byte aligned rows, vector loads
+    _topk_case(P, x, 6, ld=3005)   # misaligned rows, scalar loads
+
+
+def test_topk_golden(P):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "topk_ties.json")))
+    rows = np.array(g["rows"], np.float32)
+    am, idx, val = P.topk_argmax(cu(rows), g["k"])
+    assert am.cpu().tolist() == g["argmax"]
+    assert idx.cpu().tolist() == g["topk_idx"]
+    assert np.signbit(val.cpu().numpy()[0, 4])
+
+
+# ---------------------------------------------------------------------------
+# verification
+# ---------------------------------------------------------------------------
+def test_verify_random(P):
+    rng = np.random.default_rng(3)
+    for T in (1, 5, 64, 96, 1024):
+        B = 6
+        par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+        tok = rng.integers(0, 3, (B, T)).astype(np.int32)
+        am = rng.integers(0, 3, (B, T + 1)).astype(np.int32)
+        tl = rng.integers(0, T + 1, B).astype(np.int32)
+        for tree_len in (None, tl):
+            ref = O.verify(am, tok, par, tree_len)
+            st = status_buf()
+            got = P.verify(cu(am), cu(tok), cu(par), None if tree_len is None else cu(tree_len), st)
+            torch.cuda.synchronize()
+            assert st.item() == 0
+            for g, r in zip(got, ref):
+                assert np.array_equal(g.cpu().numpy(), r), T
+
+
+def test_verify_golden_and_bad_tree(P):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "verify_example.json")))
+    for c in g["cases"]:
+        al, an, ot = P.verify(cu(np.array([c["argmax"]], np.int32)),
+                              cu(np.array([c["tokens"]], np.int32)),
+                              cu(np.array([c["parent"]], np.int32)))
+        assert al.item() == c["accept_len"]
+        assert an.cpu().tolist()[0] == c["accept_nodes"]
+        assert ot.cpu().tolist()[0] == c["out_tokens"]
+    st = status_buf()
+    P.verify(cu(np.zeros((1, 4), np.int32)), cu(np.zeros((1, 3), np.int32)),
+             cu(np.array([[-1, 1, 0]], np.int32)), None, st)
+    torch.cuda.synchronize()
+    assert st.item() == 7
+
+
+# ---------------------------------------------------------------------------
+# expansion
+# ---------------------------------------------------------------------------
+def test_expand_random(P):
+    rng = np.random.default_rng(4)
+    for trial in range(40):
+        B = 3
+        T = int(rng.choice([1, 7, 33, 64, 200]))
+        k = int(rng.integers(1, 9))
+        d_max = int(rng.integers(1, 8))
+        width = rng.integers(1, 5, d_max).astype(np.int32)
+        T_max = int(rng.choice([1, T, 2 * T, 1024]))
+        par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+        tok = np.stack([W.sibling_distinct_tokens(rng, par[b], 20) for b in range(B)])
+        ti = rng.integers(0, 20, (B, T + 1, k)).astype(np.int32)
+        tl = rng.integers(1, T + 1, B).astype(np.int32) if trial % 2 else None
+        ref = O.expand(par, tok, ti, width, d_max, T_max, tl)
+        got = P.expand(cu(par), cu(tok), cu(ti), width.tolist(), d_max, T_max,
+                       None if tl is None else cu(tl))
+        for g, r in zip(got, ref):
+            assert np.array_equal(g.cpu().numpy(), r), (trial, T, k, d_max, T_max)
+
+
+def test_expand_golden(P):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "expand_example.json")))
+    for c in g["cases"]:
+        pn, tn, ln = P.expand(cu(np.array([g["parent"]], np.int32)),
+                              cu(np.array([g["tokens"]], np.int32)),
+                              cu(np.array([g["topk_idx"]], np.int32)),
+                              g["width_sched"], c["d_max"], c["T_max"])
+        assert pn.cpu().tolist()[0] == c["parent_next"]
+        assert tn.cpu().tolist()[0] == c["tokens_next"]
+        assert ln.item() == c["tree_len_next"]
+
+
+# ---------------------------------------------------------------------------
+# tree attention
+# ---------------------------------------------------------------------------
+def _attn_gpu(P, w, out_dtype=None, with_mask=False):
+    q, kc, vc = cu(w.q), cu(w.k_cache), cu(w.v_cache)
+    kvl, par = cu(w.kv_len), cu(w.parent)
+    mask = P.tree_mask(par)[0] if with_mask else None
+    st = status_buf()
+    out = P.tree_attention(q, kc, vc, kvl, par, mask=mask, out_dtype=out_dtype,
+                           dev_status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    return out.float().cpu().numpy().astype(np.float64)
+
+
+def _spec(**kw):
+    base = dict(B=1, Hq=4, Hkv=4, D=128, kv_len=100, T=16, tree="uniform", V=16,
+                dtype="bf16", plant=None, k=2)
+    base.update(kw)
+    return base
+
+
+SMALL = [
+    _spec(),
+    _spec(D=64, Hq=2, Hkv=2, T=33, kv_len=0),
+    _spec(tree="chain", T=65, kv_len=7),
+    _spec(tree="star", T=64, kv_len=300),
+    _spec(B=3, Hq=8, Hkv=2, T=20, kv_len=[0, 129, 640]),
+    _spec(Hq=32, Hkv=8, T=64, kv_len=1000),          # 256 query rows per KV head
+    _spec(Hq=6, Hkv=1, T=96, kv_len=255),            # 576 rows: several row passes
+    _spec(T=1, kv_len=2047),                         # plain decode
+    _spec(T=130, kv_len=33, Hq=2, Hkv=2),            # three mask words
+    _spec(D=64, Hq=4, Hkv=2, T=9, kv_len=5000, L_pad=40),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_attention_small_full(P, case):
+    w = W.make_workload(SMALL[case], seed=100 + case, logits=False)
+    ref = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    for od in (torch.float32, torch.bfloat16):
+        got = _attn_gpu(P, w, out_dtype=od, with_mask=(case % 2 == 0))
+        tol = TOL["bf16"] if od == torch.float32 else TOL["bf16"] + 2 ** -8 * np.abs(ref).max()
+        err = np.abs(got - ref).max()
+        assert err <= tol, (case, od, err)
+
+
+@pytest.mark.parametrize("spec", [
+    _spec(dtype="f32", D=64, Hq=2, Hkv=2, T=16, kv_len=128),
+    _spec(dtype="f32", D=128, Hq=4, Hkv=2, T=40, kv_len=[77], tree="chain"),
+    _spec(dtype="f32", D=64, Hq=3, Hkv=3, B=2, T=70, kv_len=[0, 200]),
+])
+def test_attention_fp32_full(P, spec):
+    w = W.make_workload(spec, seed=7, logits=False)
+    ref = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    got = _attn_gpu(P, w, out_dtype=torch.float32)
+    assert np.abs(got - ref).max() <= TOL["f32"]
+
+
+def test_attention_tiny_config(P):
+    w = W.make_workload("tiny", logits=False)
+    ref = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    got = _attn_gpu(P, w)
+    assert np.abs(got - ref).max() <= TOL["f32"]
+
+
+def _sample_rows(w, n, seed):
+    rng = np.random.default_rng(seed)
+    rows = {(0, 0, 0), (w.B - 1, w.Hq - 1, w.T - 1), (0, w.Hq // 2, w.T // 2)}
+    while len(rows) < n:
+        rows.add((int(rng.integers(w.B)), int(rng.integers(w.Hq)), int(rng.integers(w.T))))
+    return sorted(rows)
+
+
+@pytest.mark.parametrize("name", ["llama2-7b", "llama2-13b", "llama3-8b-long", "ragged-16"])
+def test_attention_configs_sampled(P, name):
+    w = W.make_workload(name, logits=False)
+    got = _attn_gpu(P, w, with_mask=True)  # bf16 out, as the step runs it
+    got32 = _attn_gpu(P, w, out_dtype=torch.float32, with_mask=True)
+    rows = _sample_rows(w, 40, 1)
+    ref = O.attention_rows(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale, rows)
+    for n, (b, h, i) in enumerate(rows):
+        assert np.abs(got32[b, i, h] - ref[n]).max() <= TOL["bf16"], (b, h, i)
+        assert np.abs(got[b, i, h] - ref[n]).max() <= TOL["bf16"] + 2 ** -8 * np.abs(ref[n]).max()
+    assert np.isfinite(got).all()
+
+
+def test_attention_deterministic(P):
+    w = W.make_workload(_spec(Hq=32, Hkv=8, T=64, kv_len=3000), seed=9, logits=False)
+    a = _attn_gpu(P, w, out_dtype=torch.float32)
+    b = _attn_gpu(P, w, out_dtype=torch.float32)
+    assert np.array_equal(a, b)
+
+
+def test_attention_kv_len_too_long_reports(P):
+    w = W.make_workload(_spec(T=8, kv_len=50), seed=3, logits=False)
+    w.kv_len[0] = w.L_cap  # kv_len + T > L_cap
+    q, kc, vc = cu(w.q), cu(w.k_cache), cu(w.v_cache)
+    st = status_buf()
+    P.tree_attention(q, kc, vc, cu(w.kv_len), cu(w.parent), dev_status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 8
+
+
+# ---------------------------------------------------------------------------
+# one whole step through the C ABI
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny", "llama2-7b"])
+def test_full_step(P, name):
+    w = W.make_workload(name)
+    B, T = w.B, w.T
+    par, tok = cu(w.parent), cu(w.tokens)
+    mask, depth = P.tree_mask(par)
+    out = P.tree_attention(cu(w.q), cu(w.k_cache), cu(w.v_cache), cu(w.kv_len), par, mask=mask)
+    am, idx, val = P.topk_argmax(cu(w.logits), w.k)
+    al, an, ot = P.verify(am.view(B, T + 1), tok, par)
+    pn, tn, ln = P.expand(par, tok, idx.view(B, T + 1, w.k), w.width, w.d_max, w.T_max)
+    torch.cuda.synchronize()
+    r_am, r_idx, _ = O.topk(w.logits, w.k)
+    assert np.array_equal(am.cpu().numpy(), r_am)
+    r_al, r_an, r_ot = O.verify(r_am.reshape(B, -1), w.tokens, w.parent)
+    assert al.cpu().tolist() == r_al.tolist() == w.planted_depth.tolist()
+    assert np.array_equal(an.cpu().numpy(), r_an) and np.array_equal(ot.cpu().numpy(), r_ot)
+    r_pn, r_tn, r_ln = O.expand(w.parent, w.tokens, r_idx.reshape(B, T + 1, w.k), w.width,
+                                w.d_max, w.T_max)
+    assert np.array_equal(pn.cpu().numpy(), r_pn) and np.array_equal(tn.cpu().numpy(), r_tn)
+    assert np.array_equal(ln.cpu().numpy(), r_ln)
+    rows = _sample_rows(w, 12, 2)
+    ref = O.attention_rows(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale, rows)
+    o = out.float().cpu().numpy()
+    for n, (b, h, i) in enumerate(rows):
+        assert np.abs(o[b, i, h] - ref[n]).max() <= TOL[w.dtype] + (
+            2 ** -8 * np.abs(ref[n]).max() if w.dtype == "bf16" else 0)
