@@ -23,6 +23,7 @@
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kTopkLds = 8192;  // top-k rows staged in LDS when (T+1)*k fits
 
 struct WidthArg {
   int32_t w[PTD_MAX_DEPTH];
@@ -111,6 +112,7 @@ k_expand(const int32_t* __restrict__ parent, const int32_t* __restrict__ tokens,
   __shared__ int s_oid[PTD_MAX_T], s_opar[PTD_MAX_T], s_otok[PTD_MAX_T];
   __shared__ int s_part[kThreads / PTD_WAVE];
   __shared__ int s_width[PTD_MAX_DEPTH];
+  __shared__ int s_topk[kTopkLds];
 
   const int b = blockIdx.x, tid = threadIdx.x;
   int n = T;
@@ -122,6 +124,11 @@ k_expand(const int32_t* __restrict__ parent, const int32_t* __restrict__ tokens,
   int32_t* tn = tokens_next + static_cast<size_t>(b) * T_max;
 
   for (int d = tid; d < PTD_MAX_DEPTH; d += kThreads) s_width[d] = ws.w[d];
+  const int32_t* topk_b = topk_idx + static_cast<size_t>(b) * (T + 1) * k;
+  const bool staged = (T + 1) * k <= kTopkLds;
+  if (staged)
+    for (int x = tid; x < (T + 1) * k; x += kThreads) s_topk[x] = topk_b[x];
+  const int32_t* rows = staged ? s_topk : topk_b;
   int bad = 0;
   for (int i = tid; i < n; i += kThreads) {
     const int p = parent[static_cast<size_t>(b) * T + i];
@@ -162,7 +169,7 @@ k_expand(const int32_t* __restrict__ parent, const int32_t* __restrict__ tokens,
   ExpandCtx ctx{s_tok, s_cstart, s_clist, s_ncld, s_dep, nullptr, k, d_max, s_width};
   for (int v = tid; v < n; v += kThreads) {
     ExpandCtx c = ctx;
-    c.row = topk_idx + (static_cast<size_t>(b) * (T + 1) + v + 1) * k;
+    c.row = rows + (v + 1) * k;
     s_nnew[v] = grow(c, v, [](int, int) {});
   }
   // level 1: roots in index order
@@ -200,7 +207,7 @@ k_expand(const int32_t* __restrict__ parent, const int32_t* __restrict__ tokens,
         s_otok[pos] = s_tok[c];
       }
       ExpandCtx c = ctx;
-      c.row = topk_idx + (static_cast<size_t>(b) * (T + 1) + id + 1) * k;
+      c.row = rows + (id + 1) * k;
       const int parent_pos = lo + e;
       grow(c, id, [&](int a, int tok) {
         const int pos = base + nold + a;

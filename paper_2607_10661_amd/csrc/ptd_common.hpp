@@ -26,6 +26,13 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
 }
+// Same rounding by the gfx950 packed converter (v_cvt_pk_bf16_f32, RNE).
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  using bf16x2 = __bf16 __attribute__((ext_vector_type(2)));
+  using f32x2 = float __attribute__((ext_vector_type(2)));
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
 
 // ---------------------------------------------------------------------------
 // device-reported errors: first error wins

@@ -9,11 +9,12 @@
 // a row is distinct.
 //
 // Kernels
-//   k_topk_partial  grid (slices, rows); 256 threads stream one slice of one
-//                   row with 16-byte loads.  Each thread keeps a sorted list of
-//                   its KMAX best keys in registers; the lists are merged per
-//                   wave (KMAX rounds of a 64-lane max) and then per workgroup.
-//   k_topk_merge    one wave per row merges the slice results.
+//   k_topk_partial  one wave per (row, vocabulary slice): each lane keeps a
+//                   sorted list of its KMAX best keys in registers while it
+//                   streams the slice with 16-byte loads (four in flight);
+//                   the 64 lists are then merged by a butterfly of 6 steps,
+//                   each merging two sorted lists with a bitonic network.
+//   k_topk_merge    one wave per row merges the slice results the same way.
 // The selected values are re-read from the logits, so topk_val carries the
 // row's own values (including the sign of a zero).
 #include "ptd_common.hpp"
@@ -46,19 +47,33 @@ __device__ __forceinline__ void insert(uint64_t (&l)[KMAX], uint64_t key) {
   }
 }
 
-// Merge the sorted per-lane lists of a wave; out[r] (r < KMAX) receives the
-// wave's r-th best key (identical in every lane).
+// Top-KMAX of two descending lists, left in `a` (descending): the
+// elementwise max of a and reversed b is a bitonic sequence holding the top
+// KMAX, which a bitonic merge network sorts.
 template <int KMAX>
-__device__ __forceinline__ void wave_merge(uint64_t (&l)[KMAX], uint64_t (&out)[KMAX]) {
+__device__ __forceinline__ void merge_lists(uint64_t (&a)[KMAX], const uint64_t (&b)[KMAX]) {
 #pragma unroll
-  for (int r = 0; r < KMAX; ++r) {
-    const uint64_t m = ptd::wave_max_u64(l[0]);
-    out[r] = m;
-    if (l[0] == m) {
+  for (int i = 0; i < KMAX; ++i) a[i] = a[i] > b[KMAX - 1 - i] ? a[i] : b[KMAX - 1 - i];
 #pragma unroll
-      for (int j = 0; j < KMAX - 1; ++j) l[j] = l[j + 1];
-      l[KMAX - 1] = 0;
-    }
+  for (int j = KMAX / 2; j > 0; j >>= 1)
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i)
+      if ((i & j) == 0 && a[i] < a[i + j]) {
+        const uint64_t t = a[i];
+        a[i] = a[i + j];
+        a[i + j] = t;
+      }
+}
+
+// After the butterfly every lane holds the wave's top KMAX, descending.
+template <int KMAX>
+__device__ __forceinline__ void wave_merge(uint64_t (&l)[KMAX]) {
+#pragma unroll
+  for (int o = 1; o < PTD_WAVE; o <<= 1) {
+    uint64_t other[KMAX];
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) other[i] = ptd::shfl_xor_u64(l[i], o);
+    merge_lists<KMAX>(l, other);
   }
 }
 
@@ -91,12 +106,14 @@ __device__ __forceinline__ void emit(uint64_t key, int lane, int k, int V, const
 
 template <int KMAX, bool BF16, bool VEC>
 __global__ void __launch_bounds__(kThreads)
-k_topk_partial(const void* __restrict__ logits, int V, long long ld, int slice_len, int k,
-               int32_t* __restrict__ argmax, int32_t* __restrict__ topk_idx,
-               float* __restrict__ topk_val, uint64_t* __restrict__ part) {
-  __shared__ uint64_t s_cand[kThreads / PTD_WAVE][KMAX];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int s = blockIdx.x, row = blockIdx.y;
+k_topk_partial(const void* __restrict__ logits, int R, int V, long long ld, int slices,
+               int slice_len, int k, int32_t* __restrict__ argmax,
+               int32_t* __restrict__ topk_idx, float* __restrict__ topk_val,
+               uint64_t* __restrict__ part) {
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * (kThreads / PTD_WAVE) + (threadIdx.x >> 6);
+  if (item >= R * slices) return;  // whole wave
+  const int row = item / slices, s = item % slices;
   const int v0 = s * slice_len;
   const int v1 = min(V, v0 + slice_len);
   const void* rb = BF16 ? static_cast<const void*>(static_cast<const uint16_t*>(logits) + row * ld)
@@ -106,12 +123,28 @@ k_topk_partial(const void* __restrict__ logits, int V, long long ld, int slice_l
   for (int j = 0; j < KMAX; ++j) l[j] = 0;
 
   if constexpr (VEC) {
+    // 16-byte chunks j = lane, lane + 64, ...; U chunks per batch are loaded
+    // (predicated) before any is consumed, so U loads are in flight per lane
     constexpr int E = BF16 ? 8 : 4;  // elements per 16-byte load
-    for (int v = v0 + tid * E; v < v1; v += kThreads * E) {
-      if (v + E <= v1) {
-        const uint4 w = BF16 ? *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(rb) + v)
-                             : *reinterpret_cast<const uint4*>(static_cast<const float*>(rb) + v);
-        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    constexpr int U = 4;
+    const int nfull = (v1 - v0) / E;
+    for (int j0 = 0; j0 < nfull; j0 += U * PTD_WAVE) {
+      uint4 w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + u * PTD_WAVE + lane;
+        if (j < nfull) {
+          const int v = v0 + j * E;
+          w[u] = BF16 ? *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(rb) + v)
+                      : *reinterpret_cast<const uint4*>(static_cast<const float*>(rb) + v);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + u * PTD_WAVE + lane;
+        if (j >= nfull) continue;
+        const int v = v0 + j * E;
+        const uint32_t ws[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           uint32_t bits;
@@ -119,56 +152,44 @@ k_topk_partial(const void* __restrict__ logits, int V, long long ld, int slice_l
           else bits = ws[e];
           insert<KMAX>(l, make_key(bits, static_cast<uint32_t>(v + e)));
         }
-      } else {
-        for (int e = 0; v + e < v1; ++e)
-          insert<KMAX>(l, make_key(elem_bits<BF16>(rb, v + e), static_cast<uint32_t>(v + e)));
       }
     }
+    // the last partial chunk, one element per lane
+    const int vt = v0 + nfull * E + lane;
+    if (vt < v1) insert<KMAX>(l, make_key(elem_bits<BF16>(rb, vt), static_cast<uint32_t>(vt)));
   } else {
-    for (int v = v0 + tid; v < v1; v += kThreads)
+    for (int v = v0 + lane; v < v1; v += PTD_WAVE)
       insert<KMAX>(l, make_key(elem_bits<BF16>(rb, v), static_cast<uint32_t>(v)));
   }
 
-  uint64_t best[KMAX];
-  wave_merge<KMAX>(l, best);
-  if (lane == 0) {
-#pragma unroll
-    for (int r = 0; r < KMAX; ++r) s_cand[wave][r] = best[r];
-  }
-  __syncthreads();
-  if (wave != 0) return;
-  // lane j holds candidate j of the 4 wave lists (4 * KMAX <= 64)
-  uint64_t c[KMAX];
-#pragma unroll
-  for (int j = 0; j < KMAX; ++j) c[j] = 0;
-  if (lane < 4 * KMAX) c[0] = s_cand[lane / KMAX][lane % KMAX];
-  wave_merge<KMAX>(c, best);
+  wave_merge<KMAX>(l);
   uint64_t mine = 0;
 #pragma unroll
-  for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? best[r] : mine;
-  if (gridDim.x == 1) {
+  for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? l[r] : mine;
+  if (slices == 1) {
     emit<BF16>(mine, lane, k, V, rb, row, argmax, topk_idx, topk_val);
   } else if (lane < KMAX) {
-    part[(static_cast<size_t>(row) * gridDim.x + s) * KMAX + lane] = mine;
+    part[static_cast<size_t>(item) * KMAX + lane] = mine;
   }
 }
 
 template <int KMAX, bool BF16>
-__global__ void __launch_bounds__(PTD_WAVE)
-k_topk_merge(const void* __restrict__ logits, int V, long long ld, int slices, int k,
+__global__ void __launch_bounds__(kThreads)
+k_topk_merge(const void* __restrict__ logits, int R, int V, long long ld, int slices, int k,
              const uint64_t* __restrict__ part, int32_t* __restrict__ argmax,
              int32_t* __restrict__ topk_idx, float* __restrict__ topk_val) {
-  const int lane = threadIdx.x, row = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * (kThreads / PTD_WAVE) + (threadIdx.x >> 6);
+  if (row >= R) return;  // whole wave
   uint64_t l[KMAX];
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) l[j] = 0;
   const uint64_t* pr = part + static_cast<size_t>(row) * slices * KMAX;
   for (int j = lane; j < slices * KMAX; j += PTD_WAVE) insert<KMAX>(l, pr[j]);
-  uint64_t best[KMAX];
-  wave_merge<KMAX>(l, best);
+  wave_merge<KMAX>(l);
   uint64_t mine = 0;
 #pragma unroll
-  for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? best[r] : mine;
+  for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? l[r] : mine;
   const void* rb = BF16 ? static_cast<const void*>(static_cast<const uint16_t*>(logits) + row * ld)
                         : static_cast<const void*>(static_cast<const float*>(logits) + row * ld);
   emit<BF16>(mine, lane, k, V, rb, row, argmax, topk_idx, topk_val);
@@ -181,17 +202,14 @@ struct TopkPlan {
 
 bool make_topk_plan(int R, int V, int k, TopkPlan* p) {
   if (R < 1 || V < 1 || k < 1 || k > PTD_MAX_K || k > V) return false;
-  if (R > 65535) return false;
   p->kmax = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : k <= 8 ? 8 : 16;
-  // aim for ~4 workgroups per CU, slices of at least 2048 elements
-  int s = (1024 + R - 1) / R;
-  const int by_len = V / 2048 > 1 ? V / 2048 : 1;
-  if (s > by_len) s = by_len;
-  if (s > 256) s = 256;
+  // one wave per slice of ~4096 elements (eight 16-byte bf16 loads per lane)
+  int s = (V + 4095) / 4096;
   if (s < 1) s = 1;
   int len = (V + s - 1) / s;
   len = (len + 7) & ~7;  // keep slice starts 16-byte aligned
   s = (V + len - 1) / len;
+  if (static_cast<long long>(R) * s > (1LL << 30)) return false;
   p->slices = s;
   p->slice_len = len;
   p->ws_bytes = s > 1 ? static_cast<size_t>(R) * s * p->kmax * sizeof(uint64_t) : 0;
@@ -201,16 +219,17 @@ bool make_topk_plan(int R, int V, int k, TopkPlan* p) {
 template <int KMAX, bool BF16>
 void launch(const TopkPlan& pl, bool vec, const void* logits, int R, int V, long long ld,
             int k, int32_t* am, int32_t* ti, float* tv, uint64_t* part, hipStream_t st) {
-  const dim3 grid(pl.slices, R);
+  constexpr int WPB = kThreads / PTD_WAVE;
+  const dim3 grid((R * pl.slices + WPB - 1) / WPB);
   if (vec)
-    hipLaunchKernelGGL((k_topk_partial<KMAX, BF16, true>), grid, dim3(kThreads), 0, st, logits, V,
-                       ld, pl.slice_len, k, am, ti, tv, part);
+    hipLaunchKernelGGL((k_topk_partial<KMAX, BF16, true>), grid, dim3(kThreads), 0, st, logits, R,
+                       V, ld, pl.slices, pl.slice_len, k, am, ti, tv, part);
   else
     hipLaunchKernelGGL((k_topk_partial<KMAX, BF16, false>), grid, dim3(kThreads), 0, st, logits,
-                       V, ld, pl.slice_len, k, am, ti, tv, part);
+                       R, V, ld, pl.slices, pl.slice_len, k, am, ti, tv, part);
   if (pl.slices > 1)
-    hipLaunchKernelGGL((k_topk_merge<KMAX, BF16>), dim3(R), dim3(PTD_WAVE), 0, st, logits, V, ld,
-                       pl.slices, k, part, am, ti, tv);
+    hipLaunchKernelGGL((k_topk_merge<KMAX, BF16>), dim3((R + WPB - 1) / WPB), dim3(kThreads), 0,
+                       st, logits, R, V, ld, pl.slices, k, part, am, ti, tv);
 }
 
 template <bool BF16>

@@ -8,10 +8,11 @@
 //
 // Kernels
 //   k_attn_mfma    bf16 q/k/v.  One workgroup = (b, g, row pass, KV split);
-//                  8 waves (2 per SIMD), each owning up to 32 query rows and a
-//                  share of every key tile.  K/V tiles of 128 keys are streamed
-//                  HBM -> VGPR -> LDS (double buffered, one barrier per tile)
-//                  and shared by every query row of the GQA group.  Scores are computed
+//                  8 waves (2 per SIMD), each owning up to 32 query rows.  K/V
+//                  stream HBM -> LDS with asynchronous copies into a ring of
+//                  nine 32-key sub-tiles (144 KB in flight), shared by every
+//                  query row of the GQA group; V is read transposed straight
+//                  from its natural layout with ds_read_b64_tr_b16.  Scores are computed
 //                  transposed, S^T = K Q^T, and the output as O^T = V^T P^T,
 //                  so each lane owns one query column in both accumulators and
 //                  the online-softmax rescale is lane-local.  MFMA:
@@ -31,7 +32,6 @@ using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 using u32x2 = uint32_t __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 512;   // 8 waves
-constexpr int kKT = 128;        // keys per LDS tile
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;  // running-max start: finite, below any score
 
@@ -74,34 +74,109 @@ __device__ inline void logical_block(int nblocks, int& id) {
 // ===========================================================================
 // MFMA path
 // ===========================================================================
+// Asynchronous HBM -> LDS copy (gfx950 global_load_lds_dwordx4): every lane
+// copies 16 bytes from its own global address and the wave's 64 x 16 bytes
+// land contiguously at the wave-uniform LDS byte address `lds`.  The copy is
+// issued from inline asm so that the compiler's wait-count insertion does not
+// make later LDS reads wait for every copy in flight; completion is tracked
+// with explicit vmcnt waits (vector-memory operations retire in issue order,
+// so a wait also covers every older load).  M0 is saved and restored inside
+// the asm, and one wait state separates the M0 write from the copy.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(gptr)
+      : "memory");
+}
+
+// Same, 4 bytes per lane (lane l lands at lds + 4*l).
+__device__ __forceinline__ void dma4(const void* gptr, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(gptr)
+      : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait until at most n of this wave's vector-memory operations are pending
+// (n above 24 waits for 24: stricter, never wrong).
+__device__ __forceinline__ void wait_vmcnt_le(int n) {
+  switch (n) {
+#define PTD_W(k) case k: wait_vmcnt<k>(); break;
+    PTD_W(1) PTD_W(2) PTD_W(3) PTD_W(4) PTD_W(5) PTD_W(6) PTD_W(7) PTD_W(8)
+    PTD_W(9) PTD_W(10) PTD_W(11) PTD_W(12) PTD_W(13) PTD_W(14) PTD_W(15) PTD_W(16)
+    PTD_W(17) PTD_W(18) PTD_W(19) PTD_W(20) PTD_W(21) PTD_W(22) PTD_W(23)
+#undef PTD_W
+    case 0: wait_vmcnt<0>(); break;
+    default: wait_vmcnt<24>(); break;
+  }
+}
+
+// Workgroup barrier that also completes this wave's LDS reads; the asm memory
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+#define PTD_LDS __attribute__((address_space(3)))
+using i16x4 = short __attribute__((ext_vector_type(4)));
+
+// LDS byte address of a __shared__ object (address-space casts need C casts)
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const PTD_LDS char*)p));
+}
+__device__ __forceinline__ i16x4 lds_read_tr16(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((PTD_LDS i16x4*)p);
+}
+
+// LDS layout of one 32-key sub-tile: K rows then V rows, each [32][D] bf16,
+// row-major with the 16-byte chunks of row r stored XOR-permuted by (r mod CH)
+// (CH = D/8 chunks per row).  The permutation makes the K-operand reads
+// (16 rows x one chunk per 16 lanes) and the V transpose reads (16 rows x 32
+// bytes) hit distinct banks.
 template <int D>
-struct TileLayout {
-  static constexpr int KS = D + 8;    // K tile row stride (bf16 elements)
-  static constexpr int VS = kKT + 8;  // V^T tile row stride
-  static constexpr int K_ELEMS = kKT * KS;
-  static constexpr int V_ELEMS = D * VS;
-  static constexpr int STAGE_ELEMS = K_ELEMS + V_ELEMS;
-  static constexpr int KCHUNKS = kKT * D / 8;     // 16-byte K chunks per tile
-  static constexpr int VUNITS = (kKT / 4) * (D / 8);  // (4 keys x 8 d) V units per tile
-  static constexpr int KU = (KCHUNKS + kThreads - 1) / kThreads;
-  static constexpr int VU = (VUNITS + kThreads - 1) / kThreads;
+struct Ring {
+  static constexpr int CH = D / 8;                   // 16-byte chunks per row
+  static constexpr int SUB = 32;                     // keys per sub-tile
+  static constexpr int PART = SUB * D * 2;           // bytes of K (or V) per sub-tile
+  static constexpr int SLOT = 2 * PART;              // K + V
+  static constexpr int NS = (144 * 1024) / SLOT;     // sub-tiles in the ring
+  static constexpr int DPS = 2 * SUB * CH / kThreads;  // copies per thread per sub-tile
+  static constexpr int BYTES = NS * SLOT;
+  static_assert(DPS >= 1 && (2 * SUB * CH) % kThreads == 0, "sub-tile split");
+  __device__ static int swz(int row, int chunk) { return chunk ^ (row & (CH - 1)); }
 };
 
 template <int D, int QB, int WR>
 __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
-  using L = TileLayout<D>;
-  constexpr int WK = (kThreads / PTD_WAVE) / WR;  // key groups
-  constexpr int KPW = kKT / WK;         // keys per wave per tile
-  constexpr int SUBS = KPW / 32;        // 32-key MFMA steps per wave per tile
-  constexpr int DB = D / 32;            // 32-wide d blocks (QK^T k-dim)
-  constexpr int DT = D / 16;            // 16-wide d tiles (PV output rows)
-  constexpr int STAGE_BYTES = L::STAGE_ELEMS * 2;
-  constexpr int COMB_BYTES = (WK - 1) * WR * (QB * DT * 64 * 16 + QB * 64 * 8);
-  constexpr int SMEM = (2 * STAGE_BYTES > COMB_BYTES) ? 2 * STAGE_BYTES : COMB_BYTES;
+  using R = Ring<D>;
+  constexpr int WK = (kThreads / PTD_WAVE) / WR;  // key groups: sub-tiles per round
+  constexpr int DB = D / 32;                      // 32-wide d blocks (QK^T k-dim)
+  constexpr int DT = D / 16;                      // 16-wide d tiles (PV output rows)
+  constexpr int COMB_BYTES = 8 * QB * DT * 64 * 16 + 8 * QB * 16 * 8;
+  constexpr int QDED = 16384;  // dedicated query region (blocks of <= 64 rows, D = 128)
+  constexpr int SMEM = (R::BYTES + QDED) > COMB_BYTES ? (R::BYTES + QDED) : COMB_BYTES;
+  static_assert(R::NS >= 2 * WK, "ring must hold two rounds");
   __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int wr = wave % WR;
   const int kg = wave / WR;
@@ -133,28 +208,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   const uint16_t* vbase = static_cast<const uint16_t*>(p.v) +
                           (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D;
   const int rowbase = pass * p.rows_per_pass + wr * 16 * QB;
-  const bool wave_live = rowbase < p.M;  // padding waves only join the barriers
-
-  // ---- query fragments (B operand of S^T = K Q^T): lane holds
-  //      Q[row l16][d = 32*db + 8*l4 .. +8]
-  bf16x8 qf[QB][DB];
-  const uint64_t* mrow[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int r = rowbase + qb * 16 + l16;
-    const bool live = r < p.M;
-    const int i = live ? r / p.G : 0;
-    const int hg = live ? r % p.G : 0;
-    mrow[qb] = p.mask + (static_cast<size_t>(b) * p.T + i) * p.W;
-    const uint16_t* qrow = static_cast<const uint16_t*>(p.q) +
-                           ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (live) v = *reinterpret_cast<const u32x4*>(qrow + db * 32 + l4 * 8);
-      qf[qb][db] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
+  const bool wave_live = rowbase < p.M;  // padding waves only copy and sync
 
   f32x4 o[QB][DT];
   float m[QB], lsum[QB];
@@ -166,181 +220,231 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     for (int dt = 0; dt < DT; ++dt) o[qb][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // ---- tile staging: HBM -> registers -> LDS
-  u32x4 kreg[L::KU];
-  u32x4 vreg[L::VU][4];
-  auto load_tile = [&](int t0) {
+  // ---- sub-tile copies: thread tid moves chunks u*512 + tid of the
+  //      sub-tile's 2*32*CH chunks (K rows, then V rows)
+  const uint32_t ring = lds_addr(smem);
+  // per-thread parts of the copy addresses (the same for every sub-tile)
+  int cp_row[R::DPS], cp_off[R::DPS];
+  const uint16_t* cp_base[R::DPS];
 #pragma unroll
-    for (int u = 0; u < L::KU; ++u) {
-      const int c = tid + kThreads * u;
-      if (L::KCHUNKS % kThreads && c >= L::KCHUNKS) break;
-      const int key = c / (D / 8), dch = c % (D / 8);
-      const int row = min(t0 + key, N - 1);
-      kreg[u] = *reinterpret_cast<const u32x4*>(kbase + static_cast<size_t>(row) * D + dch * 8);
-    }
+  for (int u = 0; u < R::DPS; ++u) {
+    const int c = u * kThreads + tid;
+    const int mat = c / (R::SUB * R::CH);
+    const int local = c % (R::SUB * R::CH);
+    cp_row[u] = local / R::CH;
+    cp_off[u] = R::swz(cp_row[u], local % R::CH) * 8;
+    cp_base[u] = mat ? vbase : kbase;
+  }
+  auto issue = [&](int t) {
+    const uint32_t slot_lds = ring + (t % R::NS) * R::SLOT;
 #pragma unroll
-    for (int u = 0; u < L::VU; ++u) {
-      const int unit = tid + kThreads * u;
-      if (L::VUNITS % kThreads && unit >= L::VUNITS) break;
-      const int kgrp = unit / (D / 8), dch = unit % (D / 8);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int row = min(t0 + 4 * kgrp + e, N - 1);
-        vreg[u][e] = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(row) * D + dch * 8);
-      }
-    }
-  };
-  auto store_tile = [&](int stage) {
-    uint16_t* ks = reinterpret_cast<uint16_t*>(smem) + stage * L::STAGE_ELEMS;
-    uint16_t* vt = ks + L::K_ELEMS;
-#pragma unroll
-    for (int u = 0; u < L::KU; ++u) {
-      const int c = tid + kThreads * u;
-      if (L::KCHUNKS % kThreads && c >= L::KCHUNKS) break;
-      const int key = c / (D / 8), dch = c % (D / 8);
-      *reinterpret_cast<u32x4*>(ks + key * L::KS + dch * 8) = kreg[u];
-    }
-#pragma unroll
-    for (int u = 0; u < L::VU; ++u) {
-      const int unit = tid + kThreads * u;
-      if (L::VUNITS % kThreads && unit >= L::VUNITS) break;
-      const int kgrp = unit / (D / 8), dch = unit % (D / 8);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int w = j >> 1;
-        uint32_t a0 = vreg[u][0][w], a1 = vreg[u][1][w], a2 = vreg[u][2][w], a3 = vreg[u][3][w];
-        u32x2 pk;
-        if (j & 1) {
-          pk[0] = (a0 >> 16) | (a1 & 0xFFFF0000u);
-          pk[1] = (a2 >> 16) | (a3 & 0xFFFF0000u);
-        } else {
-          pk[0] = (a0 & 0xFFFFu) | (a1 << 16);
-          pk[1] = (a2 & 0xFFFFu) | (a3 << 16);
-        }
-        *reinterpret_cast<u32x2*>(vt + (dch * 8 + j) * L::VS + 4 * kgrp) = pk;
-      }
+    for (int u = 0; u < R::DPS; ++u) {
+      const int grow = min(start + t * R::SUB + cp_row[u], N - 1);
+      dma16(cp_base[u] + static_cast<size_t>(grow) * D + cp_off[u],
+            slot_lds + (u * kThreads + wave * PTD_WAVE) * 16);
     }
   };
 
-  const int ntiles = (end - start + kKT - 1) / kKT;
-  load_tile(start);
-  store_tile(0);
-  __syncthreads();
+  const int ntiles = (end - start + R::SUB - 1) / R::SUB;
+  const int nrounds = (ntiles + WK - 1) / WK;
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int t0 = start + t * kKT;
-    const bool more = t + 1 < ntiles;
-    if (more) load_tile(t0 + kKT);
-
-    const uint16_t* ks = reinterpret_cast<const uint16_t*>(smem) + (t & 1) * L::STAGE_ELEMS;
-    const uint16_t* vt = ks + L::K_ELEMS;
+  // ---- ancestor words of the rows' nodes (trees of <= 128 nodes): plain
+  //      loads, first consumed in the tree sub-tiles, which come last
+  const int pr0 = pass * p.rows_per_pass;
+  const bool small_tree = p.W <= 2;
+  const uint64_t* mrow[QB];
+  uint64_t mw0[QB], mw1[QB];
 #pragma unroll
-    for (int sub = 0; sub < SUBS; ++sub) {
-      const int ko = kg * KPW + sub * 32;  // key offset inside the tile
-      const int abs0 = t0 + ko;
-      if (abs0 >= end || !wave_live) break;
+  for (int qb = 0; qb < QB; ++qb) {
+    const int r = min(pr0 + wr * 16 * QB + qb * 16 + l16, p.M - 1);
+    mrow[qb] = p.mask + (static_cast<size_t>(b) * p.T + r / p.G) * p.W;
+    mw0[qb] = small_tree ? mrow[qb][0] : 0ull;
+    mw1[qb] = (small_tree && p.W == 2) ? mrow[qb][1] : 0ull;
+  }
 
-      // ---- S^T (keys x queries) = K Q^T; lane: query l16, keys 4*l4 + e
-      f32x4 s[2][QB];
+  // ---- query rows of this pass go to LDS with the same asynchronous copies:
+  //      into a dedicated region when they fit (all K/V sub-tiles then start
+  //      at once), otherwise into the last ring slots, which turn into K/V
+  //      slots once the fragments are in registers
+  const int qbytes = p.rows_per_pass * D * 2;
+  const bool qded = qbytes <= QDED;
+  const int qslots = qded ? 0 : (qbytes + R::SLOT - 1) / R::SLOT;  // <= 4
+  const int qslot0 = R::NS - qslots;
+  const uint32_t qlds = qded ? ring + R::BYTES : ring + qslot0 * R::SLOT;
+  for (int c0 = wave * PTD_WAVE; c0 < p.rows_per_pass * R::CH; c0 += kThreads) {
+    const int c = c0 + lane;
+    const int rl = c / R::CH, pos = c % R::CH;
+    const int r = min(pr0 + rl, p.M - 1);
+    const int i = r / p.G, hg = r % p.G;
+    const uint16_t* src = static_cast<const uint16_t*>(p.q) +
+                          ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D +
+                          R::swz(rl, pos) * 8;
+    dma16(src, qlds + c0 * 16);
+  }
+  int pending = 0;  // this thread's copies issued after the query rows
+  for (int t = 0; t < min(ntiles, qslot0); ++t) {
+    issue(t);
+    pending += R::DPS;
+  }
+  wait_vmcnt_le(pending);
+  lds_barrier();
+
+  // query fragments (B operand of S^T = K Q^T): lane holds
+  // Q[row l16][d = 32*db + 8*l4 .. +8]
+  bf16x8 qf[QB][DB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int rl = wr * 16 * QB + qb * 16 + l16;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(
+          smem + (qlds - ring) + rl * (D * 2) + R::swz(rl, db * 4 + l4) * 16);
+      qf[qb][db] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  if (!qded) {
+    lds_barrier();  // the query slots become K/V slots
+    for (int t = qslot0; t < min(ntiles, R::NS); ++t) issue(t);
+  }
+
+  // per-lane LDS byte offsets inside a sub-tile (the row's swizzle is the
+  // same for both 16-row halves, which therefore differ by a constant)
+  int koff[DB], voff[DT];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+    koff[db] = l16 * (D * 2) + R::swz(l16, db * 4 + l4) * 16;
+  const int tj = l16 >> 2, tq = l16 & 3;
+  const int key0 = 4 * l4 + tj;  // this lane's source key for the transpose reads
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+    voff[dt] = key0 * (D * 2) + R::swz(key0, 2 * dt + (tq >> 1)) * 16 + (tq & 1) * 8;
+
+  for (int rd = 0; rd < nrounds; ++rd) {
+    const int issued = min(ntiles, R::NS + max(0, rd - 1) * WK);
+    const int needed = min(ntiles, (rd + 1) * WK);
+    wait_vmcnt_le((issued - needed) * R::DPS);
+    lds_barrier();
+    if (rd >= 1) {  // refill the slots the previous round used
+      for (int j = 0; j < WK; ++j) {
+        const int t = R::NS + (rd - 1) * WK + j;
+        if (t < ntiles) issue(t);
+      }
+    }
+    const int t = rd * WK + kg;
+    if (t >= ntiles || !wave_live) continue;
+    const int abs0 = start + t * R::SUB;
+    const unsigned char* ks = smem + (t % R::NS) * R::SLOT;
+    const unsigned char* vs = ks + R::PART;
+
+    // ---- S^T (keys x queries) = K Q^T; lane: query l16, keys 16*kb + 4*l4 + e
+    f32x4 s[2][QB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) s[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(ks + kb * 16 * (D * 2) + koff[db]);
+        const bf16x8 kf = __builtin_bit_cast(bf16x8, kv);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][db], s[kb][qb], 0, 0, 0);
+      }
+    }
+
+    // ---- visibility: past the chunk end, or a tree key that is not an ancestor
+    if (abs0 + R::SUB > n_kv || abs0 + R::SUB > end) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) s[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const u32x4 kv = *reinterpret_cast<const u32x4*>(
-              ks + (ko + kb * 16 + l16) * L::KS + db * 32 + l4 * 8);
-          const bf16x8 kf = __builtin_bit_cast(bf16x8, kv);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][db], s[kb][qb], 0, 0, 0);
-        }
-      }
-
-      // ---- visibility: past the chunk end, or a tree key that is not an ancestor
-      if (abs0 + 32 > n_kv || abs0 + 32 > end) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int key = abs0 + kb * 16 + l4 * 4 + e;
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-              bool vis = key < end;
-              if (vis && key >= n_kv) {
-                const int a = key - n_kv;
-                vis = (mrow[qb][a >> 6] >> (a & 63)) & 1ull;
-              }
-              if (!vis) s[kb][qb][e] = -INFINITY;
-            }
-          }
-      }
-
-      // ---- online softmax (exp2 domain), lane-local per query column
-      bf16x8 pf[QB], pfl[QB];
-      bool rescale = false;
-      float alpha[QB];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        float mx = fmaxf(fmaxf(fmaxf(s[0][qb][0], s[0][qb][1]), fmaxf(s[0][qb][2], s[0][qb][3])),
-                         fmaxf(fmaxf(s[1][qb][0], s[1][qb][1]), fmaxf(s[1][qb][2], s[1][qb][3])));
-        mx = fmaxf(mx, __shfl_xor(mx, 16, PTD_WAVE));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, PTD_WAVE));
-        const float m_new = fmaxf(m[qb], mx);
-        alpha[qb] = __builtin_amdgcn_exp2f((m[qb] - m_new) * p.c);
-        rescale |= m_new != m[qb];
-        m[qb] = m_new;
-        const float mc = m_new * p.c;
-        float pv[8];
-#pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pv[e] = __builtin_amdgcn_exp2f(fmaf(s[0][qb][e], p.c, -mc));
-          pv[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][qb][e], p.c, -mc));
+          const int key = abs0 + kb * 16 + l4 * 4 + e;
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) {
+            bool vis = key < end;
+            if (vis && key >= n_kv) {
+              const int a = key - n_kv;
+              // branchless pick of word a>>6 (0 or 1) for small trees
+              const uint64_t hi_sel = 0ull - static_cast<uint64_t>(a >> 6);
+              const uint64_t word = small_tree ? (mw0[qb] ^ ((mw0[qb] ^ mw1[qb]) & hi_sel))
+                                               : mrow[qb][a >> 6];
+              vis = (word >> (a & 63)) & 1ull;
+            }
+            if (!vis) s[kb][qb][e] = -INFINITY;
+          }
         }
-        // p = hi + lo with hi = bf16(p), lo = bf16(p - hi): the PV product
-        // then sees p to ~2^-17 relative instead of bf16's 2^-9
-        u32x4 ph, pl;
-        float ps = 0.f;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          ph[w] = ptd::pack_bf16x2(pv[2 * w], pv[2 * w + 1]);
-          pl[w] = ptd::pack_bf16x2(pv[2 * w] - ptd::bf16_lo(ph[w]),
-                                   pv[2 * w + 1] - ptd::bf16_hi(ph[w]));
-          ps += pv[2 * w] + pv[2 * w + 1];
-        }
-        lsum[qb] = lsum[qb] * alpha[qb] + ps;
-        pf[qb] = __builtin_bit_cast(bf16x8, ph);
-        pfl[qb] = __builtin_bit_cast(bf16x8, pl);
-      }
-      if (__any(rescale)) {
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[qb][dt] *= alpha[qb];
-      }
-
-      // ---- O^T (d x queries) += V^T P^T; k-slot j of lane group l4 is key
-      //      4*l4 + j (j < 4) or 16 + 4*l4 + (j - 4), matching the S^T layout
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t* vrow = vt + (dt * 16 + l16) * L::VS + ko + l4 * 4;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
-        const u32x4 vv = {lo[0], lo[1], hi[0], hi[1]};
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-          o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[qb][dt], 0, 0, 0);
-          o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl[qb], o[qb][dt], 0, 0, 0);
-        }
-      }
     }
 
-    if (more) store_tile((t + 1) & 1);
-    __syncthreads();
+    // ---- online softmax (exp2 domain), lane-local per query column
+    bf16x8 pf[QB], pfl[QB];
+    bool rescale = false;
+    float alpha[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = fmaxf(fmaxf(fmaxf(s[0][qb][0], s[0][qb][1]), fmaxf(s[0][qb][2], s[0][qb][3])),
+                       fmaxf(fmaxf(s[1][qb][0], s[1][qb][1]), fmaxf(s[1][qb][2], s[1][qb][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, PTD_WAVE));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, PTD_WAVE));
+      // lazy rescale: the reference max only moves when the new scores exceed
+      // it by more than 2^8 in the exp2 domain, so p <= 256 and O/l is unchanged
+      const float m_cand = fmaxf(m[qb], mx);
+      const bool need = (m_cand - m[qb]) * p.c > 8.0f;
+      alpha[qb] = need ? __builtin_amdgcn_exp2f((m[qb] - m_cand) * p.c) : 1.0f;
+      rescale |= need;
+      if (need) m[qb] = m_cand;
+      const float mc = m[qb] * p.c;
+      float pv[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pv[e] = __builtin_amdgcn_exp2f(fmaf(s[0][qb][e], p.c, -mc));
+        pv[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][qb][e], p.c, -mc));
+      }
+      // p = hi + lo with hi = bf16(p), lo = bf16(p - hi): the PV product
+      // then sees p to ~2^-17 relative instead of bf16's 2^-9
+      u32x4 ph, pl;
+      float ps = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        ph[w] = ptd::cvt_pk_bf16(pv[2 * w], pv[2 * w + 1]);
+        pl[w] = ptd::cvt_pk_bf16(pv[2 * w] - ptd::bf16_lo(ph[w]),
+                                 pv[2 * w + 1] - ptd::bf16_hi(ph[w]));
+        ps += pv[2 * w] + pv[2 * w + 1];
+      }
+      lsum[qb] = lsum[qb] * alpha[qb] + ps;
+      pf[qb] = __builtin_bit_cast(bf16x8, ph);
+      pfl[qb] = __builtin_bit_cast(bf16x8, pl);
+    }
+    if (__any(rescale)) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[qb][dt] *= alpha[qb];
+    }
+
+    // ---- O^T (d x queries) += V^T P^T.  K-slot j of lane group l4 is key
+    //      4*l4 + j (j < 4) or 16 + 4*l4 + (j - 4), matching the S^T layout.
+    //      V^T comes from two LDS transpose reads: source lane 4*j + q of a
+    //      16-lane group points at V[key_j][16*dt + 4q], and lane i of the
+    //      group receives V[key_0..3][16*dt + i].
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const i16x4 lo = lds_read_tr16(vs + voff[dt]);
+      const i16x4 hi = lds_read_tr16(vs + 16 * (D * 2) + voff[dt]);
+      const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
+      const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
+      const u32x4 vv = {l2[0], l2[1], h2[0], h2[1]};
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[qb][dt], 0, 0, 0);
+        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl[qb], o[qb][dt], 0, 0, 0);
+      }
+    }
   }
+  wait_vmcnt<0>();
+  lds_barrier();  // every copy landed and every wave is done with the ring
 
   // ---- per-column totals of the softmax denominator
 #pragma unroll
@@ -349,68 +453,61 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     lsum[qb] += __shfl_xor(lsum[qb], 32, PTD_WAVE);
   }
 
-  // ---- merge the key groups of the workgroup (fixed order kg = 1..WK-1)
-  if constexpr (WK > 1) {
-    constexpr int OBYTES = QB * DT * 64 * 16;
-    constexpr int SLOT = OBYTES + QB * 64 * 8;
-    if (kg > 0) {
-      unsigned char* slot = smem + ((kg - 1) * WR + wr) * SLOT;
-      f32x4* so = reinterpret_cast<f32x4*>(slot);
-      float2* sml = reinterpret_cast<float2*>(slot + OBYTES);
+  // ---- epilogue: every wave parks its fragments in LDS (16-byte units of a
+  //      (qb, dt) block permuted by (dt*4 + l4) so that the row-wise reads
+  //      below spread over the banks), then all threads merge the key groups
+  //      (fixed order) and write whole rows with coalesced stores
+  {
+    f32x4* so = reinterpret_cast<f32x4*>(smem);
+    float2* sml = reinterpret_cast<float2*>(smem + 8 * QB * DT * 64 * 16);
+    const int wslot = wr * WK + kg;
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) so[(qb * DT + dt) * 64 + lane] = o[qb][dt];
-        sml[qb * 64 + lane] = make_float2(m[qb], lsum[qb]);
-      }
-    }
-    __syncthreads();
-    if (kg > 0) return;
-#pragma unroll
-    for (int k2 = 1; k2 < WK; ++k2) {
-      const unsigned char* slot = smem + ((k2 - 1) * WR + wr) * SLOT;
-      const f32x4* so = reinterpret_cast<const f32x4*>(slot);
-      const float2* sml = reinterpret_cast<const float2*>(slot + OBYTES);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        const float2 ml = sml[qb * 64 + lane];
-        const float mn = fmaxf(m[qb], ml.x);
-        const float w0 = __builtin_amdgcn_exp2f((m[qb] - mn) * p.c);
-        const float w1 = __builtin_amdgcn_exp2f((ml.x - mn) * p.c);
-        m[qb] = mn;
-        lsum[qb] = lsum[qb] * w0 + ml.y * w1;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[qb][dt] = o[qb][dt] * w0 + so[(qb * DT + dt) * 64 + lane] * w1;
-      }
-    }
-  }
-
-  // ---- write: lane holds O^T[d = 16*dt + 4*l4 + 0..3][query l16]
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int r = rowbase + qb * 16 + l16;
-    if (r >= p.M) continue;
-    if (p.splits == 1) {
-      const int i = r / p.G, hg = r % p.G;
-      const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D;
-      const float inv = 1.0f / lsum[qb];
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int d0 = dt * 16 + l4 * 4;
-        const f32x4 v = o[qb][dt] * inv;
-        if (p.out_bf16) {
-          u32x2 w = {ptd::pack_bf16x2(v[0], v[1]), ptd::pack_bf16x2(v[2], v[3])};
-          *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.out) + off + d0) = w;
-        } else {
-          *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + off + d0) = v;
-        }
-      }
-    } else {
-      const size_t prow = ((static_cast<size_t>(split) * p.B + b) * p.Hkv + g) * p.M + r;
+    for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
-        *reinterpret_cast<f32x4*>(p.part_o + prow * D + dt * 16 + l4 * 4) = o[qb][dt];
-      if (l4 == 0) p.part_ml[prow] = make_float2(m[qb] * p.c, lsum[qb]);
+        so[((wslot * QB + qb) * DT + dt) * 64 + l4 * 16 + (l16 ^ ((dt * 4 + l4) & 15))] = o[qb][dt];
+      if (l4 == 0) sml[(wslot * QB + qb) * 16 + l16] = make_float2(m[qb], lsum[qb]);
+    }
+  }
+  __syncthreads();
+  {
+    const f32x4* so = reinterpret_cast<const f32x4*>(smem);
+    const float2* sml = reinterpret_cast<const float2*>(smem + 8 * QB * DT * 64 * 16);
+    constexpr int D4 = D / 4;
+    const int rows_here = min(p.rows_per_pass, p.M - pr0);
+    for (int e = tid; e < rows_here * D4; e += kThreads) {
+      const int row = e / D4, d4 = e % D4;
+      const int wrr = row / (16 * QB), qb = (row % (16 * QB)) / 16, r16 = row % 16;
+      const int dt = d4 / 4, q4 = d4 % 4;
+      const int pos = q4 * 16 + (r16 ^ ((dt * 4 + q4) & 15));
+      float mm = kNegBig;
+#pragma unroll
+      for (int k2 = 0; k2 < WK; ++k2) mm = fmaxf(mm, sml[((wrr * WK + k2) * QB + qb) * 16 + r16].x);
+      float den = 0.f;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k2 = 0; k2 < WK; ++k2) {
+        const float2 ml = sml[((wrr * WK + k2) * QB + qb) * 16 + r16];
+        const float w = __builtin_amdgcn_exp2f((ml.x - mm) * p.c);
+        den += w * ml.y;
+        acc += so[(((wrr * WK + k2) * QB + qb) * DT + dt) * 64 + pos] * w;
+      }
+      const int r = pr0 + row;
+      if (p.splits == 1) {
+        const int i = r / p.G, hg = r % p.G;
+        const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D + d4 * 4;
+        const f32x4 v = acc * (1.0f / den);
+        if (p.out_bf16) {
+          const u32x2 w2 = {ptd::cvt_pk_bf16(v[0], v[1]), ptd::cvt_pk_bf16(v[2], v[3])};
+          *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.out) + off) = w2;
+        } else {
+          *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + off) = v;
+        }
+      } else {
+        const size_t prow = ((static_cast<size_t>(split) * p.B + b) * p.Hkv + g) * p.M + r;
+        *reinterpret_cast<f32x4*>(p.part_o + prow * D + d4 * 4) = acc;
+        if (d4 == 0) p.part_ml[prow] = make_float2(mm * p.c, den);
+      }
     }
   }
 }
@@ -437,21 +534,26 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnParams p) {
   const int nsp = (N + csz - 1) / csz;  // non-empty splits
   const size_t stride = static_cast<size_t>(p.B) * p.Hkv * p.M;
   const size_t row0 = (static_cast<size_t>(b) * p.Hkv + g) * p.M + r;
-  float mx = kNegBig;
-  for (int s = 0; s < nsp; ++s) mx = fmaxf(mx, p.part_ml[row0 + s * stride].x);
-  float den = 0.f;
+  // one pass, online in the split index; the unrolled body lets the loads of
+  // several splits be in flight together
+  float mrun = kNegBig, den = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
   for (int s = 0; s < nsp; ++s) {
     const float2 ml = p.part_ml[row0 + s * stride];
-    const float w = __builtin_amdgcn_exp2f(ml.x - mx);
-    den += w * ml.y;
-    acc += w * *reinterpret_cast<const f32x4*>(p.part_o + (row0 + s * stride) * D + d4 * 4);
+    const f32x4 ov = *reinterpret_cast<const f32x4*>(p.part_o + (row0 + s * stride) * D + d4 * 4);
+    const float mn = fmaxf(mrun, ml.x);
+    const float a = __builtin_amdgcn_exp2f(mrun - mn);
+    const float w = __builtin_amdgcn_exp2f(ml.x - mn);
+    den = den * a + w * ml.y;
+    acc = acc * a + ov * w;
+    mrun = mn;
   }
   const f32x4 v = acc * (1.0f / den);
   const int i = r / p.G, hg = r % p.G;
   const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D + d4 * 4;
   if (p.out_bf16) {
-    u32x2 w = {ptd::pack_bf16x2(v[0], v[1]), ptd::pack_bf16x2(v[2], v[3])};
+    const u32x2 w = {ptd::cvt_pk_bf16(v[0], v[1]), ptd::cvt_pk_bf16(v[2], v[3])};
     *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.out) + off) = w;
   } else {
     *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + off) = v;

@@ -5,57 +5,63 @@
 // topological order (parent[i] < i), so every walk up the parent chain visits
 // strictly decreasing indices and ends in at most i+1 steps.
 //
-// One thread per node; a thread walks its own chain and assembles the row's
-// 64-bit words from the highest word down, writing every word of the row once.
+// One workgroup per sequence: the parent array is staged in LDS, then every
+// thread walks the chains of its nodes there and assembles each row's 64-bit
+// words from the highest word down, writing every word of the row once.
 #include "ptd_common.hpp"
 #include "ptd_internal.hpp"
 
 namespace {
 
-__global__ void __launch_bounds__(256)
+constexpr int kThreads = 256;
+
+__global__ void __launch_bounds__(kThreads)
 k_tree_mask(const int32_t* __restrict__ parent, const int32_t* __restrict__ tree_len,
             int T, int W, uint64_t* __restrict__ mask, int32_t* __restrict__ depth,
             int32_t* dev_status) {
-  const int b = blockIdx.y;
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= T) return;
+  __shared__ int s_par[PTD_MAX_T];
+  const int b = blockIdx.x;
   int n = T;
   if (tree_len) {
     n = tree_len[b];
     n = n < 0 ? 0 : (n > T ? T : n);
   }
   const int32_t* par = parent + static_cast<size_t>(b) * T;
-  uint64_t* row = mask + (static_cast<size_t>(b) * T + i) * W;
-  if (i >= n) {
-    for (int w = 0; w < W; ++w) row[w] = 0;
-    if (depth) depth[static_cast<size_t>(b) * T + i] = 0;
-    return;
-  }
-  int cur = i >> 6;
-  for (int w = cur + 1; w < W; ++w) row[w] = 0;
-  uint64_t word = 0;
-  int count = 0;
-  int a = i;
-  while (a != -1) {
-    const int p = par[a];
-    if (p < -1 || p >= a) {  // not topological: report and stop the walk
-      ptd::report(dev_status, PTD_ERR_BAD_TREE);
-      break;
+  for (int i = threadIdx.x; i < n; i += kThreads) s_par[i] = par[i];
+  __syncthreads();
+  for (int i = threadIdx.x; i < T; i += kThreads) {
+    uint64_t* row = mask + (static_cast<size_t>(b) * T + i) * W;
+    if (i >= n) {
+      for (int w = 0; w < W; ++w) row[w] = 0;
+      if (depth) depth[static_cast<size_t>(b) * T + i] = 0;
+      continue;
     }
-    const int wa = a >> 6;
-    if (wa != cur) {
-      row[cur] = word;
-      for (int w = wa + 1; w < cur; ++w) row[w] = 0;
-      cur = wa;
-      word = 0;
+    int cur = i >> 6;
+    for (int w = cur + 1; w < W; ++w) row[w] = 0;
+    uint64_t word = 0;
+    int count = 0;
+    int a = i;
+    while (a != -1) {
+      const int p = s_par[a];
+      if (p < -1 || p >= a) {  // not topological: report and stop the walk
+        ptd::report(dev_status, PTD_ERR_BAD_TREE);
+        break;
+      }
+      const int wa = a >> 6;
+      if (wa != cur) {
+        row[cur] = word;
+        for (int w = wa + 1; w < cur; ++w) row[w] = 0;
+        cur = wa;
+        word = 0;
+      }
+      word |= 1ull << (a & 63);
+      ++count;
+      a = p;
     }
-    word |= 1ull << (a & 63);
-    ++count;
-    a = p;
+    row[cur] = word;
+    for (int w = 0; w < cur; ++w) row[w] = 0;
+    if (depth) depth[static_cast<size_t>(b) * T + i] = count;
   }
-  row[cur] = word;
-  for (int w = 0; w < cur; ++w) row[w] = 0;
-  if (depth) depth[static_cast<size_t>(b) * T + i] = count;
 }
 
 }  // namespace
@@ -64,8 +70,7 @@ int ptd_launch_tree_mask(const int32_t* parent, const int32_t* tree_len, int B, 
                          uint64_t* mask, int32_t* depth, int32_t* dev_status,
                          hipStream_t stream) {
   const int W = ptd_cdiv(T, 64);
-  dim3 grid(ptd_cdiv(T, 256), B);
-  hipLaunchKernelGGL(k_tree_mask, grid, dim3(256), 0, stream, parent, tree_len, T, W,
+  hipLaunchKernelGGL(k_tree_mask, dim3(B), dim3(kThreads), 0, stream, parent, tree_len, T, W,
                      mask, depth, dev_status);
   return ptd_launch_status();
 }

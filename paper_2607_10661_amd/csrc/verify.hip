@@ -29,6 +29,7 @@ k_verify(const int32_t* __restrict__ argmax, const int32_t* __restrict__ tokens,
   __shared__ int s_dep[2][PTD_MAX_T];
   __shared__ int s_jmp[2][PTD_MAX_T];
   __shared__ int s_path[PTD_MAX_T];
+  __shared__ int s_am[PTD_MAX_T + 1];
   __shared__ int s_red[kThreads / PTD_WAVE];
 
   const int b = blockIdx.x;
@@ -40,19 +41,14 @@ k_verify(const int32_t* __restrict__ argmax, const int32_t* __restrict__ tokens,
   }
   const int32_t* am = argmax + static_cast<size_t>(b) * (T + 1);
 
+  // stage the tree and the verification tokens (independent loads)
   int bad = 0;
+  for (int i = tid; i <= T; i += kThreads) s_am[i] = am[i];
   for (int i = tid; i < n; i += kThreads) {
     const int p = parent[static_cast<size_t>(b) * T + i];
-    const int t = tokens[static_cast<size_t>(b) * T + i];
     s_par[i] = p;
-    s_tok[i] = t;
-    if (p < -1 || p >= i) {
-      bad = 1;
-      continue;
-    }
-    s_acc[0][i] = (t == am[p + 1]) ? 1 : 0;  // eligibility of the edge into i
-    s_dep[0][i] = 1;
-    s_jmp[0][i] = p;
+    s_tok[i] = tokens[static_cast<size_t>(b) * T + i];
+    bad |= (p < -1 || p >= i);
   }
   if (__syncthreads_or(bad)) {
     if (tid == 0) ptd::report(dev_status, PTD_ERR_BAD_TREE);
@@ -63,6 +59,14 @@ k_verify(const int32_t* __restrict__ argmax, const int32_t* __restrict__ tokens,
     if (tid == 0) accept_len[b] = 0;
     return;
   }
+
+  for (int i = tid; i < n; i += kThreads) {
+    const int p = s_par[i];
+    s_acc[0][i] = (s_tok[i] == s_am[p + 1]) ? 1 : 0;  // eligibility of the edge into i
+    s_dep[0][i] = 1;
+    s_jmp[0][i] = p;
+  }
+  __syncthreads();
 
   // pointer jumping: combine the segment of i with the segment above it
   int cur = 0;
@@ -110,7 +114,7 @@ k_verify(const int32_t* __restrict__ argmax, const int32_t* __restrict__ tokens,
     accept_len[b] = k;
   }
   __syncthreads();
-  const int bonus = am[best + 1];  // row 0 (committed token) when nothing is accepted
+  const int bonus = s_am[best + 1];  // row 0 (committed token) when nothing is accepted
   for (int t = tid; t <= T; t += kThreads) {
     int node = -1, tok = -1;
     if (t < k) {

@@ -54,7 +54,7 @@ def test_attention_workspace_sizes():
 
 def test_topk_workspace_sizes():
     assert P.ptd_topk_workspace_bytes(65, 32000, 4) > 0
-    assert P.ptd_topk_workspace_bytes(2048, 32000, 4) == 0  # one slice per row
+    assert P.ptd_topk_workspace_bytes(2048, 4000, 4) == 0   # one slice per row
     assert P.ptd_topk_workspace_bytes(4, 10, 11) == 0       # k > V
     assert P.ptd_topk_workspace_bytes(4, 100, 17) == 0      # k > PTD_MAX_K
 

@@ -215,7 +215,7 @@ SMALL = [
     _spec(),
     _spec(D=64, Hq=2, Hkv=2, T=33, kv_len=0),
     _spec(tree="chain", T=65, kv_len=7),
-    _spec(tree="star", T=64, kv_len=300),
+    _spec(tree="star", T=64, kv_len=300, V=1000),
     _spec(B=3, Hq=8, Hkv=2, T=20, kv_len=[0, 129, 640]),
     _spec(Hq=32, Hkv=8, T=64, kv_len=1000),          # 256 query rows per KV head
     _spec(Hq=6, Hkv=1, T=96, kv_len=255),            # 576 rows: several row passes
