@@ -3,7 +3,7 @@
 
 A step = the whole hot path over one batch of synthetic inputs, on one stream:
 ptd_build_tree_mask -> ptd_tree_attention (one layer) -> ptd_topk_argmax ->
-ptd_verify -> ptd_expand.  Inputs are seeded synthetic tensors shaped like the
+ptd_verify_expand (verification and expansion in one launch).  Inputs are seeded synthetic tensors shaped like the
 paper's workloads (Llama-2-7B attention shape by default), resident in HBM
 before timing starts; R input sets totalling >= 1 GiB are rotated so the
 256 MB MALL cannot serve the KV cache from one step to the next.
@@ -126,9 +126,8 @@ def main():
             ev[1].record(stream)
         P.ptd_topk_argmax(s["logits"], dt_code, R_rows, w.V, w.V, k, am, tidx, tval,
                           ws_topk, ws_topk.numel(), sp)
-        P.ptd_verify(am, tokens, parent, None, B, T, al, an, ot, status, sp)
-        P.ptd_expand(parent, tokens, None, B, T, tidx, k, w.width, w.d_max, w.T_max,
-                     pn, tn, ln, status, sp)
+        P.ptd_verify_expand(am, tokens, parent, None, B, T, tidx, k, w.width, w.d_max, w.T_max,
+                            al, an, ot, pn, tn, ln, status, sp)
 
     for i in range(args.warmup):
         step(i)

@@ -11,6 +11,7 @@
  *   ptd_topk_argmax      per-row argmax / top-k of the verification logits
  *   ptd_verify           greedy longest accepted path (+ bonus token)
  *   ptd_expand           progressive expansion with top-k children
+ *   ptd_verify_expand    the two above in one launch
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller (stream-ordered;
@@ -152,7 +153,9 @@ size_t ptd_topk_workspace_bytes(int32_t R, int32_t V, int32_t k);
  *   topk_val  float [R][k]         (nullable) the selected entries' own values,
  *                                  widened exactly to fp32
  * Order: value descending; equal values by the lower index; -0.0 equals +0.0.
- * Logits are expected finite (NaN ordering is unspecified).
+ * Logits are expected non-NaN (NaN ordering is unspecified); +-inf are ordered.
+ * A workspace is needed only when V exceeds one workgroup's slice (131072 bf16
+ * or 65536 fp32 values); ptd_topk_workspace_bytes gives 0 otherwise.
  * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_DTYPE, PTD_ERR_WORKSPACE,
  * PTD_ERR_HIP.
  */
@@ -214,6 +217,22 @@ int ptd_expand(const int32_t* parent, const int32_t* tokens,
                int32_t d_max, int32_t T_max, int32_t* parent_next,
                int32_t* tokens_next, int32_t* tree_len_next,
                int32_t* dev_status, void* stream);
+
+/*
+ * ptd_verify_expand -- ptd_verify followed by ptd_expand on the same tree in
+ * one launch (the tree is staged on chip once); outputs are identical to the
+ * two calls in sequence.  Arguments have the meaning given above; both groups
+ * of outputs are written.  Sec. 3.2 and Sec. 3.1 as cited there.
+ * dev_status: PTD_ERR_BAD_TREE.  Errors: PTD_ERR_NULL, PTD_ERR_SHAPE,
+ * PTD_ERR_HIP.
+ */
+int ptd_verify_expand(const int32_t* argmax, const int32_t* draft_tokens,
+                      const int32_t* parent, const int32_t* tree_len, int32_t B,
+                      int32_t T, const int32_t* topk_idx, int32_t k,
+                      const int32_t* width_sched, int32_t d_max, int32_t T_max,
+                      int32_t* accept_len, int32_t* accept_nodes, int32_t* out_tokens,
+                      int32_t* parent_next, int32_t* tokens_next,
+                      int32_t* tree_len_next, int32_t* dev_status, void* stream);
 
 #ifdef __cplusplus
 }

@@ -9,7 +9,8 @@ device memory and the stream.  There is no CPU fallback: without a built
 ``libptd.so`` the import fails.
 
 The lower-case helpers (``tree_mask``, ``tree_attention``, ``topk_argmax``,
-``verify``, ``expand``) allocate outputs with torch and call the entry points.
+``verify``, ``expand``, ``verify_expand``) allocate outputs with torch and call
+the entry points.
 """
 from __future__ import annotations
 
@@ -63,6 +64,8 @@ _SIGS = {
     "ptd_verify": ([_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
     "ptd_expand": ([_vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp,
                     _vp, _vp], ctypes.c_int),
+    "ptd_verify_expand": ([_vp, _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _i32, _vp,
+                           _vp, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -152,6 +155,21 @@ def ptd_expand(parent, tokens, tree_len, B, T, topk_idx, k, width_sched, d_max, 
                            _ptr(tokens_next), _ptr(tree_len_next), _ptr(dev_status),
                            _stream(stream)),
            "ptd_expand")
+
+
+def ptd_verify_expand(argmax, draft_tokens, parent, tree_len, B, T, topk_idx, k, width_sched,
+                      d_max, T_max, accept_len, accept_nodes, out_tokens, parent_next,
+                      tokens_next, tree_len_next, dev_status=None, stream=None):
+    if len(width_sched) < d_max:
+        raise ValueError("width_sched needs d_max entries")
+    ws = (ctypes.c_int32 * max(1, len(width_sched)))(*[int(x) for x in width_sched])
+    _check(_lib.ptd_verify_expand(_ptr(argmax), _ptr(draft_tokens), _ptr(parent),
+                                  _ptr(tree_len), B, T, _ptr(topk_idx), k,
+                                  ctypes.cast(ws, _vp), d_max, T_max, _ptr(accept_len),
+                                  _ptr(accept_nodes), _ptr(out_tokens), _ptr(parent_next),
+                                  _ptr(tokens_next), _ptr(tree_len_next), _ptr(dev_status),
+                                  _stream(stream)),
+           "ptd_verify_expand")
 
 
 # ---------------------------------------------------------------------------
@@ -255,3 +273,22 @@ def expand(parent, tokens, topk_idx, width_sched: Sequence[int], d_max: int, T_m
     ptd_expand(parent, tokens, tree_len, B, T, topk_idx, k, width_sched, d_max, T_max,
                pn, tn, ln, dev_status)
     return pn, tn, ln
+
+
+def verify_expand(argmax, draft_tokens, parent, topk_idx, width_sched: Sequence[int],
+                  d_max: int, T_max: int, tree_len=None, dev_status=None):
+    """Returns (accept_len, accept_nodes, out_tokens, parent_next, tokens_next,
+    tree_len_next)."""
+    _need_gpu(argmax, draft_tokens, parent, topk_idx, tree_len)
+    B, T = parent.shape
+    k = topk_idx.shape[-1]
+    dev = parent.device
+    al = torch.empty(B, dtype=torch.int32, device=dev)
+    an = torch.empty((B, T), dtype=torch.int32, device=dev)
+    ot = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+    pn = torch.empty((B, T_max), dtype=torch.int32, device=dev)
+    tn = torch.empty((B, T_max), dtype=torch.int32, device=dev)
+    ln = torch.empty(B, dtype=torch.int32, device=dev)
+    ptd_verify_expand(argmax, draft_tokens, parent, tree_len, B, T, topk_idx, k, width_sched,
+                      d_max, T_max, al, an, ot, pn, tn, ln, dev_status)
+    return al, an, ot, pn, tn, ln

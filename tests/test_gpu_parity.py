@@ -82,7 +82,7 @@ def _topk_case(P, arr, k, ld=None):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("R,V,k", [(1, 1, 1), (3, 7, 5), (17, 1000, 4), (65, 32000, 4),
                                    (97, 32000, 5), (8, 32003, 16), (5, 128256, 8),
-                                   (1100, 4099, 2)])
+                                   (1100, 4099, 2), (3, 70001, 8), (2, 200003, 16)])
 def test_topk_random(P, dtype, R, V, k):
     rng = np.random.default_rng(R * 7 + V + k)
     x = rng.standard_normal((R, V), dtype=np.float32) * np.float32(1.41)
@@ -103,6 +103,27 @@ def test_topk_all_equal_and_strided(P):
     x = W.f32_to_bf16_bits(rng.standard_normal((9, 3001), dtype=np.float32))
     _topk_case(P, x, 6, ld=3008)   # 16-byte aligned rows, vector loads
     _topk_case(P, x, 6, ld=3005)   # misaligned rows, scalar loads
+    # rows where -inf entries must fill the list (fewer finite values than k)
+    y = np.full((4, 4100), -np.inf, np.float32)
+    y[0, 17] = 1.0
+    y[1, [5, 4099]] = -3.0
+    y[2, 0] = np.float32(-0.0)
+    _topk_case(P, y, 5)
+    _topk_case(P, W.f32_to_bf16_bits(y), 5)
+    big = np.full((2, 200003), -np.inf, np.float32)  # sliced path
+    big[0, 199999] = 2.0
+    _topk_case(P, W.f32_to_bf16_bits(big), 3)
+
+
+@pytest.mark.parametrize("k", [1, 4, 16])
+def test_topk_many_ties_at_the_top(P, k):
+    # more elements tie with the k-th best than the candidate list holds
+    rng = np.random.default_rng(k)
+    x = rng.standard_normal((5, 40000), dtype=np.float32)
+    for r, n in enumerate([1500, 3000, 1025, 1024, 40000]):
+        x[r, rng.choice(40000, n, replace=False)] = np.float32(9.0)
+    _topk_case(P, x, k)
+    _topk_case(P, W.f32_to_bf16_bits(x), k)
 
 
 def test_topk_golden(P):
@@ -174,6 +195,27 @@ def test_expand_random(P):
                        None if tl is None else cu(tl))
         for g, r in zip(got, ref):
             assert np.array_equal(g.cpu().numpy(), r), (trial, T, k, d_max, T_max)
+
+
+def test_verify_expand_fused(P):
+    rng = np.random.default_rng(14)
+    for trial in range(20):
+        B = 4
+        T = int(rng.choice([1, 16, 64, 96, 300]))
+        k = int(rng.integers(1, 9))
+        d_max = int(rng.integers(1, 7))
+        width = rng.integers(1, 5, d_max).astype(np.int32)
+        T_max = int(rng.choice([T, 2 * T, 1024]))
+        par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+        tok = rng.integers(0, 6, (B, T)).astype(np.int32)  # duplicate siblings allowed
+        am = rng.integers(0, 6, (B, T + 1)).astype(np.int32)
+        ti = rng.integers(0, 6, (B, T + 1, k)).astype(np.int32)
+        tl = rng.integers(1, T + 1, B).astype(np.int32) if trial % 2 else None
+        ref = O.verify(am, tok, par, tl) + O.expand(par, tok, ti, width, d_max, T_max, tl)
+        got = P.verify_expand(cu(am), cu(tok), cu(par), cu(ti), width.tolist(), d_max, T_max,
+                              None if tl is None else cu(tl))
+        for g, r in zip(got, ref):
+            assert np.array_equal(g.cpu().numpy(), r), (trial, T, k)
 
 
 def test_expand_golden(P):
