@@ -100,7 +100,9 @@ int ptd_build_tree_mask(const int32_t* parent, const int32_t* tree_len, int32_t 
 
 /*
  * Workspace bytes ptd_tree_attention needs for this shape and tree size
- * (split-KV partial results, plus room for the masks when mask == NULL).
+ * (split-KV partial results, plus room for the masks when they are read from
+ * memory -- fp32 inputs, or T > 128 -- and mask == NULL).  The workspace needs
+ * no initialisation; calls sharing one workspace must not overlap.
  * Returns 0 on invalid arguments.
  */
 size_t ptd_tree_attention_workspace_bytes(const ptd_attn_shape* shape, int32_t T);
@@ -121,7 +123,9 @@ size_t ptd_tree_attention_workspace_bytes(const ptd_attn_shape* shape, int32_t T
  *   out      [B][T][Hq][D]           out_dtype (fp32 accumulation inside)
  *   shape    host struct above
  *   mask     uint64 [B][T][ceil(T/64)] from ptd_build_tree_mask, or NULL to
- *            have it built into the workspace
+ *            have it built into the workspace.  Read only by the fp32 path
+ *            and for T > 128: with bf16 inputs and T <= 128 the kernel derives
+ *            every row's ancestor words from parent itself (mask ignored).
  *   workspace, workspace_bytes: device scratch of at least
  *            ptd_tree_attention_workspace_bytes(shape, T) bytes, 256-byte aligned
  * Pointers to q/k/v/out must be 16-byte aligned.  in_dtype bf16 runs on MFMA

@@ -17,8 +17,12 @@
 //                  so each lane owns one query column in both accumulators and
 //                  the online-softmax rescale is lane-local.  MFMA:
 //                  v_mfma_f32_16x16x32_bf16, fp32 accumulation.
+//                  Trees of up to 128 nodes need no mask pass: each lane
+//                  holds two parent[] entries and walks its rows' ancestor
+//                  chains with wave shuffles.  With the keys split over
+//                  several workgroups, each writes fp32 partials (m, l, O).
+//   k_attn_combine merges split-KV partials in a fixed split order.
 //   k_attn_valu    fp32 (or bf16) inputs on the vector ALUs, fp32 throughout.
-//   k_attn_combine merges split-KV partials (m, l, O) in a fixed split order.
 #include <math.h>
 
 #include "ptd_common.hpp"
@@ -40,7 +44,8 @@ struct AttnParams {
   const void* k;
   const void* v;
   const int32_t* kv_len;
-  const uint64_t* mask;
+  const int32_t* parent;  // [B][T]
+  const uint64_t* mask;   // [B][T][W] ancestor words (trees of more than 128 nodes, fp32 path)
   void* out;
   float* part_o;    // [S][B][Hkv][M][D]
   float2* part_ml;  // [S][B][Hkv][M]: (running max * c, sum of p)
@@ -248,19 +253,30 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   const int ntiles = (end - start + R::SUB - 1) / R::SUB;
   const int nrounds = (ntiles + WK - 1) / WK;
 
-  // ---- ancestor words of the rows' nodes (trees of <= 128 nodes): plain
-  //      loads, first consumed in the tree sub-tiles, which come last
+  // ---- ancestor words of the rows' nodes.  Trees of <= 128 nodes: derived
+  //      in-kernel from parent[], two entries per lane (plain loads, first
+  //      consumed at the first tree sub-tile, which comes last); larger trees:
+  //      mask rows from the mask pass.
   const int pr0 = pass * p.rows_per_pass;
   const bool small_tree = p.W <= 2;
+  int node[QB];
   const uint64_t* mrow[QB];
   uint64_t mw0[QB], mw1[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int r = min(pr0 + wr * 16 * QB + qb * 16 + l16, p.M - 1);
-    mrow[qb] = p.mask + (static_cast<size_t>(b) * p.T + r / p.G) * p.W;
-    mw0[qb] = small_tree ? mrow[qb][0] : 0ull;
-    mw1[qb] = (small_tree && p.W == 2) ? mrow[qb][1] : 0ull;
+    node[qb] = r / p.G;
+    mrow[qb] = small_tree ? nullptr : p.mask + (static_cast<size_t>(b) * p.T + node[qb]) * p.W;
+    mw0[qb] = 0ull;
+    mw1[qb] = 0ull;
   }
+  int par_lo = -1, par_hi = -1;
+  if (small_tree) {
+    const int32_t* pb = p.parent + static_cast<size_t>(b) * p.T;
+    if (lane < p.T) par_lo = pb[lane];
+    if (lane + 64 < p.T) par_hi = pb[lane + 64];
+  }
+  bool words_ready = !small_tree;  // uniform over the wave
 
   // ---- query rows of this pass go to LDS with the same asynchronous copies:
   //      into a dedicated region when they fit (all K/V sub-tiles then start
@@ -352,6 +368,41 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         for (int qb = 0; qb < QB; ++qb)
           s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][db], s[kb][qb], 0, 0, 0);
       }
+    }
+
+    // ---- ancestor words, once per wave, at its first sub-tile with tree keys:
+    //      every lane follows the parent chains of its rows' nodes (parent[a]
+    //      read from lane a % 64 by shuffles, all lanes active); each step
+    //      moves to a lower index, so 128 steps end every walk
+    if (!words_ready && abs0 + R::SUB > n_kv) {
+      int a[QB];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) a[qb] = node[qb];
+      for (int step = 0; step < 128; ++step) {
+        bool live = false;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) live |= a[qb] >= 0;
+        if (!__any(live)) break;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          const int x = a[qb];
+          if (x >= 0) {
+            if (x < 64) mw0[qb] |= 1ull << x;
+            else mw1[qb] |= 1ull << (x - 64);
+          }
+          const int plo = __shfl(par_lo, x & 63, PTD_WAVE);
+          const int phi = __shfl(par_hi, x & 63, PTD_WAVE);
+          int nx = x >= 64 ? phi : plo;
+          if (x < 0) {
+            nx = -1;
+          } else if (nx < -1 || nx >= x) {  // not topological
+            ptd::report(p.dev_status, PTD_ERR_BAD_TREE);
+            nx = -1;
+          }
+          a[qb] = nx;
+        }
+      }
+      words_ready = true;
     }
 
     // ---- visibility: past the chunk end, or a tree key that is not an ancestor
@@ -513,7 +564,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 }
 
 // ===========================================================================
-// split-KV combine: out = sum_s w_s O_s / sum_s w_s l_s, w_s = 2^(mc_s - max mc)
+// split-KV combine: out = sum_s w_s O_s / sum_s w_s l_s, w_s = 2^(mc_s - max mc),
+// one thread per (b, g, row, 4 columns), online in the split index (fixed
+// order, so the result is deterministic)
 // ===========================================================================
 template <int D>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnParams p) {
@@ -534,8 +587,6 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnParams p) {
   const int nsp = (N + csz - 1) / csz;  // non-empty splits
   const size_t stride = static_cast<size_t>(p.B) * p.Hkv * p.M;
   const size_t row0 = (static_cast<size_t>(b) * p.Hkv + g) * p.M + r;
-  // one pass, online in the split index; the unrolled body lets the loads of
-  // several splits be in flight together
   float mrun = kNegBig, den = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
@@ -672,8 +723,12 @@ __global__ void __launch_bounds__(kValuThreads) k_attn_valu(AttnParams p) {
 struct Plan {
   bool mfma;
   int QB, WR, passes, rows_per_pass, splits;
+  bool needs_mask;  // mask rows read from memory (fp32 path, trees over 128 nodes)
+  // workspace: [partials][mask rows], each 256-byte aligned
   size_t partial_bytes, mask_bytes, total_bytes;
 };
+
+size_t align256(size_t n) { return (n + 255) & ~static_cast<size_t>(255); }
 
 constexpr int kTargetBlocks = 256;  // one resident workgroup per CU on MI355X
 
@@ -711,13 +766,12 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
     pl->splits = 1;
   }
   if (static_cast<long long>(s->B) * s->Hkv * pl->passes * pl->splits > 0x7FFFFFFFLL) return false;
+  pl->needs_mask = !pl->mfma || T > 128;
   pl->partial_bytes = pl->splits > 1
-      ? static_cast<size_t>(pl->splits) * s->B * s->Hkv * M * (s->D + 2) * sizeof(float)
+      ? align256(static_cast<size_t>(pl->splits) * s->B * s->Hkv * M * (s->D + 2) * sizeof(float))
       : 0;
-  pl->partial_bytes = (pl->partial_bytes + 255) & ~static_cast<size_t>(255);
-  pl->mask_bytes = static_cast<size_t>(s->B) * T * ((T + 63) / 64) * sizeof(uint64_t);
-  pl->mask_bytes = (pl->mask_bytes + 255) & ~static_cast<size_t>(255);
-  pl->total_bytes = pl->partial_bytes + pl->mask_bytes;
+  pl->mask_bytes = align256(static_cast<size_t>(s->B) * T * ((T + 63) / 64) * sizeof(uint64_t));
+  pl->total_bytes = pl->partial_bytes + (pl->needs_mask ? pl->mask_bytes : 0);
   return true;
 }
 
@@ -756,7 +810,8 @@ extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void
   PTD_RETURN_IF(!ptd_aligned(q, 16) || !ptd_aligned(k_cache, 16) || !ptd_aligned(v_cache, 16) ||
                     !ptd_aligned(out, 16) || (mask && !ptd_aligned(mask, 8)),
                 PTD_ERR_ALIGN);
-  const size_t need = mask ? pl.partial_bytes : pl.total_bytes;
+  const bool build_mask = pl.needs_mask && !mask;
+  const size_t need = pl.partial_bytes + (build_mask ? pl.mask_bytes : 0);
   if (need > 0) {
     PTD_RETURN_IF(!workspace, PTD_ERR_WORKSPACE);
     PTD_RETURN_IF(workspace_bytes < need, PTD_ERR_WORKSPACE);
@@ -764,7 +819,7 @@ extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
-  if (!mask) {
+  if (build_mask) {
     uint64_t* mws = reinterpret_cast<uint64_t*>(ws + pl.partial_bytes);
     const int rc = ptd_launch_tree_mask(parent, nullptr, shape->B, T, mws, nullptr, dev_status, st);
     if (rc != PTD_OK) return rc;
@@ -775,7 +830,8 @@ extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void
   prm.k = k_cache;
   prm.v = v_cache;
   prm.kv_len = kv_len;
-  prm.mask = mask;
+  prm.parent = parent;
+  prm.mask = pl.needs_mask ? mask : nullptr;
   prm.out = out;
   prm.part_o = pl.splits > 1 ? reinterpret_cast<float*>(ws) : nullptr;
   prm.part_ml = nullptr;

@@ -264,6 +264,8 @@ SMALL = [
     _spec(T=1, kv_len=2047),                         # plain decode
     _spec(T=130, kv_len=33, Hq=2, Hkv=2),            # three mask words
     _spec(D=64, Hq=4, Hkv=2, T=9, kv_len=5000, L_pad=40),
+    _spec(tree="chain", T=128, kv_len=40, Hq=2, Hkv=2),  # walks of 128 nodes
+    _spec(Hq=2, Hkv=2, T=100, kv_len=3000),          # two words, many KV splits
 ]
 
 
@@ -323,6 +325,37 @@ def test_attention_deterministic(P):
     a = _attn_gpu(P, w, out_dtype=torch.float32)
     b = _attn_gpu(P, w, out_dtype=torch.float32)
     assert np.array_equal(a, b)
+
+
+def test_attention_workspace_reuse(P):
+    # one workspace (not initialised) through calls of different shapes: the
+    # split arrival words must neither need zeroing nor leak between calls
+    specs = [_spec(Hq=8, Hkv=8, T=64, kv_len=2000), _spec(Hq=2, Hkv=2, T=100, kv_len=3000),
+             _spec(Hq=8, Hkv=8, T=64, kv_len=2000)]
+    ws = torch.full((1 << 24,), 0x5A, dtype=torch.uint8, device="cuda")
+    for n, sp in enumerate(specs):
+        w = W.make_workload(sp, seed=40 + n, logits=False)
+        ref = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+        for rep in range(2):
+            st = status_buf()
+            out = P.tree_attention(cu(w.q), cu(w.k_cache), cu(w.v_cache), cu(w.kv_len),
+                                   cu(w.parent), out_dtype=torch.float32, workspace=ws,
+                                   dev_status=st)
+            torch.cuda.synchronize()
+            assert st.item() == 0
+            err = np.abs(out.cpu().numpy().astype(np.float64) - ref).max()
+            assert err <= TOL["bf16"], (n, rep, err)
+
+
+@pytest.mark.parametrize("T", [20, 130])
+def test_attention_bad_tree_reports(P, T):
+    w = W.make_workload(_spec(T=T, kv_len=50), seed=5, logits=False)
+    w.parent[0, T // 2] = T // 2 + 3  # not topological
+    st = status_buf()
+    P.tree_attention(cu(w.q), cu(w.k_cache), cu(w.v_cache), cu(w.kv_len), cu(w.parent),
+                     dev_status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 7
 
 
 def test_attention_kv_len_too_long_reports(P):
