@@ -38,7 +38,24 @@ def parse():
                     help="total bytes of rotated input sets (cold-cache timing)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle sample (0 disables)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain 512 MiB device copy, 5 times: the reference "
+                         "kernel whose FETCH_SIZE / WRITE_SIZE counters scale the "
+                         "attention kernel's traffic counts")
     return ap.parse_args()
+
+
+def calibrate_copy():
+    import torch
+    n = 512 << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n,
+                      "launches": 5}), flush=True)
 
 
 def kernel_source_hash():
@@ -66,6 +83,9 @@ def load_traffic(workload, per_launch_alg):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
               "multi-GPU path.", file=sys.stderr)
