@@ -210,7 +210,7 @@ __device__ void verify_body(const int* s_par, const int* s_tok, const int* s_am,
 
 __device__ void verify_reject(int b, int T, int32_t* accept_len, int32_t* accept_nodes,
                               int32_t* out_tokens) {
-  for (int i = threadIdx.x; i <= T; i += kThreads) {
+  for (int i = threadIdx.x; i <= T; i += blockDim.x) {
     if (i < T) accept_nodes[static_cast<size_t>(b) * T + i] = -1;
     out_tokens[static_cast<size_t>(b) * (T + 1) + i] = -1;
   }
@@ -343,7 +343,7 @@ __device__ void expand_body(const int* s_par, const int* s_tok, int n, int b, in
 
 __device__ void expand_reject(int b, int T_max, int32_t* parent_next, int32_t* tokens_next,
                               int32_t* tree_len_next) {
-  for (int t = threadIdx.x; t < T_max; t += kThreads) {
+  for (int t = threadIdx.x; t < T_max; t += blockDim.x) {
     parent_next[static_cast<size_t>(b) * T_max + t] = -1;
     tokens_next[static_cast<size_t>(b) * T_max + t] = -1;
   }
@@ -412,6 +412,226 @@ k_verify_expand(const int32_t* __restrict__ argmax, const int32_t* __restrict__ 
               tokens_next, tree_len_next);
 }
 
+// ===========================================================================
+// Trees of up to 64 nodes: one wave per sequence, node i on lane i, no
+// workgroup barriers.  Same results as the workgroup kernels above.
+//   - ancestor sets as 64-bit masks by pointer doubling over wave shuffles
+//     (anc = {i}, jump = parent; anc |= anc[jump], jump = jump[jump] until
+//     every jump is -1); depth = |anc|
+//   - verification: a node is accepted iff anc contains no node whose edge is
+//     ineligible (one ballot), the terminal is the wave maximum of
+//     (depth, -index), and the path is the terminal's ancestor mask
+//   - expansion: children masks by LDS atomic OR; a node's added candidates
+//     as a bit set over its top-k row; breadth-first positions level by
+//     level: the nodes of a level write their child counts at their
+//     positions, one wave scan gives every node its first child's position,
+//     and old children add their rank among their siblings
+// ===========================================================================
+constexpr int kWaveNodes = 64;
+
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+  const uint32_t lo = __shfl(static_cast<uint32_t>(v), src, PTD_WAVE);
+  const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src, PTD_WAVE);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+template <bool VERIFY, bool EXPAND, int KM>
+__global__ void __launch_bounds__(PTD_WAVE)
+k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ tokens,
+            const int32_t* __restrict__ parent, const int32_t* __restrict__ tree_len, int T,
+            const int32_t* __restrict__ topk_idx, int k, WidthArg ws, int d_max, int T_max,
+            int32_t* __restrict__ accept_len, int32_t* __restrict__ accept_nodes,
+            int32_t* __restrict__ out_tokens, int32_t* __restrict__ parent_next,
+            int32_t* __restrict__ tokens_next, int32_t* __restrict__ tree_len_next,
+            int32_t* dev_status) {
+  __shared__ int s_tok[kWaveNodes], s_cnt[kWaveNodes], s_start[kWaveNodes];
+  __shared__ uint64_t s_cm[kWaveNodes];
+  __shared__ int s_width[PTD_MAX_DEPTH];
+  const int lane = threadIdx.x, b = blockIdx.x;
+  const int n = live_nodes(tree_len, b, T);
+  const bool live = lane < n;
+  const uint64_t below = (1ull << lane) - 1ull;
+
+  // every global load first
+  const int par = live ? parent[static_cast<size_t>(b) * T + lane] : -1;
+  const int tok = live ? tokens[static_cast<size_t>(b) * T + lane] : 0;
+  int am_lo = 0, am_hi = 0;  // argmax rows lane and 64
+  if (VERIFY) {
+    const int32_t* am = argmax + static_cast<size_t>(b) * (T + 1);
+    am_lo = lane <= T ? am[lane] : 0;
+    am_hi = T >= kWaveNodes ? am[kWaveNodes] : 0;
+  }
+  int cand[KM];
+  if (EXPAND) {
+    const int32_t* row = topk_idx + (static_cast<size_t>(b) * (T + 1) + lane + 1) * k;
+#pragma unroll
+    for (int r = 0; r < KM; ++r) cand[r] = (live && r < k) ? row[r] : 0;
+    s_width[lane] = ws.w[lane];
+  }
+  s_tok[lane] = tok;
+  s_cm[lane] = 0ull;
+  s_cnt[lane] = 0;
+
+  if (__any(live && (par < -1 || par >= lane))) {  // not topological
+    if (lane == 0) ptd::report(dev_status, PTD_ERR_BAD_TREE);
+    if (VERIFY) verify_reject(b, T, accept_len, accept_nodes, out_tokens);
+    if (EXPAND) expand_reject(b, T_max, parent_next, tokens_next, tree_len_next);
+    return;
+  }
+
+  // ancestor masks and depths
+  uint64_t anc = live ? (1ull << lane) : 0ull;
+  int jump = par;
+  while (__any(jump >= 0)) {
+    const int src = jump >= 0 ? jump : lane;
+    const uint64_t a2 = shfl64(anc, src);
+    const int j2 = __shfl(jump, src, PTD_WAVE);
+    if (jump >= 0) {
+      anc |= a2;
+      jump = j2;
+    }
+  }
+  const int dep = __popcll(anc);
+
+  if (VERIFY) {
+    const int pa = par + 1;  // the parent's argmax row (0 for a root)
+    const int am_par_lo = __shfl(am_lo, pa & 63, PTD_WAVE);
+    const int am_par = pa < kWaveNodes ? am_par_lo : am_hi;
+    const uint64_t elig = __ballot(live && tok == am_par);
+    const bool accepted = live && (anc & ~elig) == 0ull;
+    int key = accepted ? dep * 128 + (127 - lane) : -1;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) key = max(key, __shfl_xor(key, o, PTD_WAVE));
+    const int klen = key < 0 ? 0 : key / 128;
+    const int best = key < 0 ? -1 : 127 - key % 128;
+    const uint64_t path = shfl64(anc, best < 0 ? 0 : best);
+    const int bt = best + 1;  // the terminal's argmax row: the bonus token
+    const int bonus_lo = __shfl(am_lo, bt & 63, PTD_WAVE);
+    const int bonus = bt < kWaveNodes ? bonus_lo : am_hi;
+    int32_t* an = accept_nodes + static_cast<size_t>(b) * T;
+    int32_t* ot = out_tokens + static_cast<size_t>(b) * (T + 1);
+    const bool on_path = best >= 0 && live && ((path >> lane) & 1ull);
+    if (on_path) {
+      an[dep - 1] = lane;
+      ot[dep - 1] = tok;
+    }
+    if (lane < T && lane >= klen) an[lane] = -1;
+    for (int t = lane; t <= T; t += PTD_WAVE) {
+      if (t == klen) ot[t] = bonus;
+      else if (t > klen) ot[t] = -1;
+    }
+    if (lane == 0) accept_len[b] = klen;
+  }
+
+  if (EXPAND) {
+    if (live && par >= 0) atomicOr(reinterpret_cast<unsigned long long*>(&s_cm[par]), 1ull << lane);
+    __syncthreads();
+    const uint64_t cm = s_cm[lane];
+    const int ncld = __popcll(cm);
+    // candidates added under this node (bit r: topk row entry r)
+    uint32_t sel = 0;
+    if (live && dep + 1 <= d_max) {
+      const int cap = s_width[dep];
+      uint32_t dup = 0;
+      for (uint64_t m = cm; m; m &= m - 1ull) {  // existing children's tokens
+        const int t = s_tok[__ffsll(static_cast<long long>(m)) - 1];
+#pragma unroll
+        for (int r = 0; r < KM; ++r) dup |= (cand[r] == t) ? (1u << r) : 0u;
+      }
+      int have = ncld;
+#pragma unroll
+      for (int r = 0; r < KM; ++r) {
+        bool d = (dup >> r) & 1u;
+#pragma unroll
+        for (int r2 = 0; r2 < r; ++r2) d |= cand[r2] == cand[r];
+        if (r < k && have < cap && !d) {
+          sel |= 1u << r;
+          ++have;
+        }
+        if (have >= cap) break;
+      }
+    }
+    const int nnew = __popc(sel);
+
+    int32_t* pn = parent_next + static_cast<size_t>(b) * T_max;
+    int32_t* tn = tokens_next + static_cast<size_t>(b) * T_max;
+    const uint64_t roots = __ballot(live && par < 0);
+    int pos = -1;  // breadth-first position (-1: not placed, or cut at T_max)
+    if (live && par < 0) {
+      const int q = __popcll(roots & below);
+      if (q < T_max) {
+        pos = q;
+        pn[q] = -1;
+        tn[q] = tok;
+      }
+    }
+    int lo = 0, hi = min(__popcll(roots), T_max);
+    for (int level = 1; lo < hi; ++level) {
+      const bool here = pos >= 0 && dep == level;
+      if (here) s_cnt[pos] = ncld + nnew;
+      __syncthreads();
+      const int p = lo + lane;
+      const int c = p < hi ? s_cnt[p] : 0;
+      int x = c;
+#pragma unroll
+      for (int o = 1; o < PTD_WAVE; o <<= 1) {
+        const int y = __shfl_up(x, o, PTD_WAVE);
+        if (lane >= o) x += y;
+      }
+      const int total = __shfl(x, PTD_WAVE - 1, PTD_WAVE);
+      if (p < hi) s_start[p] = hi + x - c;
+      __syncthreads();
+      if (here) {  // added children: after the old ones, in candidate order
+        int q = s_start[pos] + ncld;
+#pragma unroll
+        for (int r = 0; r < KM; ++r) {
+          if ((sel >> r) & 1u) {
+            if (q < T_max) {
+              pn[q] = pos;
+              tn[q] = cand[r];
+            }
+            ++q;
+          }
+        }
+      }
+      const int ppos = __shfl(pos, par >= 0 ? par : lane, PTD_WAVE);
+      if (live && par >= 0 && dep == level + 1 && ppos >= 0) {
+        const int q = s_start[ppos] + __popcll(s_cm[par] & below);
+        if (q < T_max) {
+          pos = q;
+          pn[q] = ppos;
+          tn[q] = tok;
+        }
+      }
+      lo = hi;
+      hi = min(hi + total, T_max);
+    }
+    for (int t = hi + lane; t < T_max; t += PTD_WAVE) {
+      pn[t] = -1;
+      tn[t] = -1;
+    }
+    if (lane == 0) tree_len_next[b] = hi;
+  }
+}
+
+template <bool VERIFY, bool EXPAND>
+void launch_wave(int B, int T, int k, const int32_t* argmax, const int32_t* tokens,
+                 const int32_t* parent, const int32_t* tree_len, const int32_t* topk_idx,
+                 const WidthArg& ws, int d_max, int T_max, int32_t* accept_len,
+                 int32_t* accept_nodes, int32_t* out_tokens, int32_t* parent_next,
+                 int32_t* tokens_next, int32_t* tree_len_next, int32_t* dev_status,
+                 hipStream_t st) {
+#define PTD_WAVE_CASE(km)                                                                      \
+  hipLaunchKernelGGL((k_tree_wave<VERIFY, EXPAND, km>), dim3(B), dim3(PTD_WAVE), 0, st, argmax, \
+                     tokens, parent, tree_len, T, topk_idx, k, ws, d_max, T_max, accept_len,    \
+                     accept_nodes, out_tokens, parent_next, tokens_next, tree_len_next,         \
+                     dev_status)
+  if (!EXPAND || k <= 4) PTD_WAVE_CASE(4);
+  else if (k <= 8) PTD_WAVE_CASE(8);
+  else PTD_WAVE_CASE(16);
+#undef PTD_WAVE_CASE
+}
+
 bool expand_args_ok(int B, int T, int k, int d_max, int T_max) {
   return B >= 1 && T >= 1 && T <= PTD_MAX_T && k >= 1 && k <= PTD_MAX_K && d_max >= 1 &&
          d_max <= PTD_MAX_DEPTH && T_max >= 1 && T_max <= PTD_MAX_T;
@@ -434,9 +654,15 @@ extern "C" int ptd_verify(const int32_t* argmax, const int32_t* draft_tokens,
                 PTD_ERR_NULL);
   PTD_RETURN_IF(B < 1 || T < 1 || T > PTD_MAX_T, PTD_ERR_SHAPE);
   static_assert(PTD_MAX_T <= 2048, "index packing in the best-node key");
-  hipLaunchKernelGGL(k_verify, dim3(B), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
-                     argmax, draft_tokens, parent, tree_len, T, accept_len, accept_nodes,
-                     out_tokens, dev_status);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (T <= kWaveNodes) {
+    launch_wave<true, false>(B, T, 1, argmax, draft_tokens, parent, tree_len, nullptr,
+                             WidthArg{}, 1, 1, accept_len, accept_nodes, out_tokens, nullptr,
+                             nullptr, nullptr, dev_status, st);
+  } else {
+    hipLaunchKernelGGL(k_verify, dim3(B), dim3(kThreads), 0, st, argmax, draft_tokens, parent,
+                       tree_len, T, accept_len, accept_nodes, out_tokens, dev_status);
+  }
   return ptd_launch_status();
 }
 
@@ -450,9 +676,16 @@ extern "C" int ptd_expand(const int32_t* parent, const int32_t* tokens,
                     !tokens_next || !tree_len_next,
                 PTD_ERR_NULL);
   PTD_RETURN_IF(!expand_args_ok(B, T, k, d_max, T_max), PTD_ERR_SHAPE);
-  hipLaunchKernelGGL(k_expand, dim3(B), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
-                     parent, tokens, tree_len, T, topk_idx, k, width_arg(width_sched, d_max),
-                     d_max, T_max, parent_next, tokens_next, tree_len_next, dev_status);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (T <= kWaveNodes && T_max <= kWaveNodes) {
+    launch_wave<false, true>(B, T, k, nullptr, tokens, parent, tree_len, topk_idx,
+                             width_arg(width_sched, d_max), d_max, T_max, nullptr, nullptr,
+                             nullptr, parent_next, tokens_next, tree_len_next, dev_status, st);
+  } else {
+    hipLaunchKernelGGL(k_expand, dim3(B), dim3(kThreads), 0, st, parent, tokens, tree_len, T,
+                       topk_idx, k, width_arg(width_sched, d_max), d_max, T_max, parent_next,
+                       tokens_next, tree_len_next, dev_status);
+  }
   return ptd_launch_status();
 }
 
@@ -469,10 +702,17 @@ extern "C" int ptd_verify_expand(const int32_t* argmax, const int32_t* draft_tok
                     !tokens_next || !tree_len_next,
                 PTD_ERR_NULL);
   PTD_RETURN_IF(!expand_args_ok(B, T, k, d_max, T_max), PTD_ERR_SHAPE);
-  hipLaunchKernelGGL(k_verify_expand, dim3(B), dim3(kThreads), 0,
-                     static_cast<hipStream_t>(stream), argmax, draft_tokens, parent, tree_len, T,
-                     topk_idx, k, width_arg(width_sched, d_max), d_max, T_max, accept_len,
-                     accept_nodes, out_tokens, parent_next, tokens_next, tree_len_next,
-                     dev_status);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (T <= kWaveNodes && T_max <= kWaveNodes) {
+    launch_wave<true, true>(B, T, k, argmax, draft_tokens, parent, tree_len, topk_idx,
+                            width_arg(width_sched, d_max), d_max, T_max, accept_len,
+                            accept_nodes, out_tokens, parent_next, tokens_next, tree_len_next,
+                            dev_status, st);
+  } else {
+    hipLaunchKernelGGL(k_verify_expand, dim3(B), dim3(kThreads), 0, st, argmax, draft_tokens,
+                       parent, tree_len, T, topk_idx, k, width_arg(width_sched, d_max), d_max,
+                       T_max, accept_len, accept_nodes, out_tokens, parent_next, tokens_next,
+                       tree_len_next, dev_status);
+  }
   return ptd_launch_status();
 }

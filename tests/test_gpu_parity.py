@@ -218,6 +218,70 @@ def test_verify_expand_fused(P):
             assert np.array_equal(g.cpu().numpy(), r), (trial, T, k)
 
 
+def _small_tree(rng, T):
+    kind = int(rng.integers(4))
+    if kind == 0:
+        return W.tree_chain(T)[0]
+    if kind == 1:
+        return W.tree_star(T)[0]
+    if kind == 2:
+        br = [int(x) for x in rng.integers(1, 5, 8)]
+        par = W.tree_branching(br, T)[0]
+        if par.shape[0] == T:
+            return par
+    return W.tree_uniform(rng, T)[0]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_verify_expand_small_trees(P, seed):
+    # trees of <= 64 nodes (one wave per sequence): chains, stars, level-built
+    # and uniform trees, k up to 16, deep depth caps, cuts below T
+    rng = np.random.default_rng(200 + seed)
+    for trial in range(25):
+        B = int(rng.integers(1, 5))
+        T = int(rng.choice([1, 2, 5, 31, 63, 64]))
+        k = int(rng.integers(1, 17))
+        d_max = int(rng.integers(1, 65))
+        width = rng.integers(1, 6, d_max).astype(np.int32)
+        T_max = int(rng.integers(1, 65))
+        par = np.stack([_small_tree(rng, T) for _ in range(B)])
+        V = int(rng.choice([3, 8, 1000]))
+        tok = rng.integers(0, V, (B, T)).astype(np.int32)
+        am = rng.integers(0, V, (B, T + 1)).astype(np.int32)
+        if trial % 3 == 0:  # plant accepted chains: every node's token is its parent's argmax
+            for b in range(B):
+                for i in range(T):
+                    tok[b, i] = am[b, par[b, i] + 1]
+        ti = rng.integers(0, V, (B, T + 1, k)).astype(np.int32)
+        tl = rng.integers(0, T + 1, B).astype(np.int32) if trial % 2 else None
+        ref_v = O.verify(am, tok, par, tl)
+        ref_e = O.expand(par, tok, ti, width, d_max, T_max, tl)
+        got = P.verify_expand(cu(am), cu(tok), cu(par), cu(ti), width.tolist(), d_max, T_max,
+                              None if tl is None else cu(tl))
+        for g, r in zip(got, ref_v + ref_e):
+            assert np.array_equal(g.cpu().numpy(), r), (seed, trial, T, k, d_max, T_max)
+        got_v = P.verify(cu(am), cu(tok), cu(par), None if tl is None else cu(tl))
+        got_e = P.expand(cu(par), cu(tok), cu(ti), width.tolist(), d_max, T_max,
+                         None if tl is None else cu(tl))
+        for g, r in zip(tuple(got_v) + tuple(got_e), ref_v + ref_e):
+            assert np.array_equal(g.cpu().numpy(), r), (seed, trial, T, k, d_max, T_max)
+
+
+@pytest.mark.parametrize("T", [9, 64, 100])
+def test_verify_expand_bad_tree_rejects(P, T):
+    par = W.tree_chain(T)[0][None, :].copy()
+    par[0, T // 2] = T // 2  # its own parent
+    st = status_buf()
+    z = np.zeros((1, T + 1), np.int32)
+    got = P.verify_expand(cu(z), cu(z[:, :T]), cu(par), cu(np.zeros((1, T + 1, 2), np.int32)),
+                          [2] * 4, 4, T, None, st)
+    torch.cuda.synchronize()
+    assert st.item() == 7
+    al, an, ot, pn, tn, ln = (g.cpu().numpy() for g in got)
+    assert al[0] == 0 and ln[0] == 0
+    assert (an == -1).all() and (ot == -1).all() and (pn == -1).all() and (tn == -1).all()
+
+
 def test_expand_golden(P):
     import json, os
     g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "expand_example.json")))
