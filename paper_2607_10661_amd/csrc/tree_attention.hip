@@ -100,6 +100,41 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
       : "memory");
 }
 
+// Same copy from a wave-uniform base address (SGPR pair) plus a per-lane
+// 32-bit byte offset: moving to the next tile changes only the scalar base.
+__device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff, uint32_t lds) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(voff), "s"(sbase)
+      : "memory");
+}
+
+// Max / sum of a lane's value and that of lane ^ 32 (or ^ 16), on the VALU
+// (gfx950 v_permlane32_swap / v_permlane16_swap: with both operands holding
+// the value, the two results are the value of the lane and of its partner).
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Same, 4 bytes per lane (lane l lands at lds + 4*l).
 __device__ __forceinline__ void dma4(const void* gptr, uint32_t lds) {
   uint32_t saved;
@@ -174,9 +209,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   constexpr int WK = (kThreads / PTD_WAVE) / WR;  // key groups: sub-tiles per round
   constexpr int DB = D / 32;                      // 32-wide d blocks (QK^T k-dim)
   constexpr int DT = D / 16;                      // 16-wide d tiles (PV output rows)
-  constexpr int COMB_BYTES = 8 * QB * DT * 64 * 16 + 8 * QB * 16 * 8;
+  constexpr int PARK_O = WK > 1 ? WR * WK * QB * DT * 64 * 16 : 0;  // parked fragments
+  constexpr int PARK_BYTES = PARK_O + (WK > 1 ? WR * WK * QB * 64 * 8 : 0);
   constexpr int QDED = 16384;  // dedicated query region (blocks of <= 64 rows, D = 128)
-  constexpr int SMEM = (R::BYTES + QDED) > COMB_BYTES ? (R::BYTES + QDED) : COMB_BYTES;
+  constexpr int SMEM = (R::BYTES + QDED) > PARK_BYTES ? (R::BYTES + QDED) : PARK_BYTES;
   static_assert(R::NS >= 2 * WK, "ring must hold two rounds");
   __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
 
@@ -229,24 +265,36 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   //      sub-tile's 2*32*CH chunks (K rows, then V rows)
   const uint32_t ring = lds_addr(smem);
   // per-thread parts of the copy addresses (the same for every sub-tile)
+  // (chunk u of a thread is K or V for the whole wave: SUB*CH is a multiple
+  //  of 64)
   int cp_row[R::DPS], cp_off[R::DPS];
-  const uint16_t* cp_base[R::DPS];
+  uint32_t cp_voff[R::DPS];
+  bool cp_v[R::DPS];
 #pragma unroll
   for (int u = 0; u < R::DPS; ++u) {
     const int c = u * kThreads + tid;
-    const int mat = c / (R::SUB * R::CH);
+    cp_v[u] = (u * kThreads + wave * PTD_WAVE) / (R::SUB * R::CH) != 0;
     const int local = c % (R::SUB * R::CH);
     cp_row[u] = local / R::CH;
     cp_off[u] = R::swz(cp_row[u], local % R::CH) * 8;
-    cp_base[u] = mat ? vbase : kbase;
+    cp_voff[u] = static_cast<uint32_t>((cp_row[u] * D + cp_off[u]) * 2);
   }
-  auto issue = [&](int t) {
+  auto issue = [&](int t) __attribute__((always_inline)) {
     const uint32_t slot_lds = ring + (t % R::NS) * R::SLOT;
+    const int row0 = start + t * R::SUB;
+    if (row0 + R::SUB <= N) {  // whole sub-tile inside the keys: scalar base
+      const size_t tile = static_cast<size_t>(row0) * D;
 #pragma unroll
-    for (int u = 0; u < R::DPS; ++u) {
-      const int grow = min(start + t * R::SUB + cp_row[u], N - 1);
-      dma16(cp_base[u] + static_cast<size_t>(grow) * D + cp_off[u],
-            slot_lds + (u * kThreads + wave * PTD_WAVE) * 16);
+      for (int u = 0; u < R::DPS; ++u)
+        dma16_s((cp_v[u] ? vbase : kbase) + tile, cp_voff[u],
+                slot_lds + (u * kThreads + wave * PTD_WAVE) * 16);
+    } else {  // last sub-tile: rows past the keys re-read the last key
+#pragma unroll
+      for (int u = 0; u < R::DPS; ++u) {
+        const int grow = min(row0 + cp_row[u], N - 1);
+        dma16((cp_v[u] ? vbase : kbase) + static_cast<size_t>(grow) * D + cp_off[u],
+              slot_lds + (u * kThreads + wave * PTD_WAVE) * 16);
+      }
     }
   };
 
@@ -335,100 +383,55 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   for (int dt = 0; dt < DT; ++dt)
     voff[dt] = key0 * (D * 2) + R::swz(key0, 2 * dt + (tq >> 1)) * 16 + (tq & 1) * 8;
 
-  for (int rd = 0; rd < nrounds; ++rd) {
-    const int issued = min(ntiles, R::NS + max(0, rd - 1) * WK);
-    const int needed = min(ntiles, (rd + 1) * WK);
-    wait_vmcnt_le((issued - needed) * R::DPS);
-    lds_barrier();
-    if (rd >= 1) {  // refill the slots the previous round used
-      for (int j = 0; j < WK; ++j) {
-        const int t = R::NS + (rd - 1) * WK + j;
-        if (t < ntiles) issue(t);
-      }
-    }
-    const int t = rd * WK + kg;
-    if (t >= ntiles || !wave_live) continue;
-    const int abs0 = start + t * R::SUB;
-    const unsigned char* ks = smem + (t % R::NS) * R::SLOT;
-    const unsigned char* vs = ks + R::PART;
-
-    // ---- S^T (keys x queries) = K Q^T; lane: query l16, keys 16*kb + 4*l4 + e
+  // ---- S^T (keys x queries) = K Q^T for sub-tile t; lane: query l16, keys
+  //      16*kb + 4*l4 + e.  Every K fragment is read first (one LDS round trip).
+  struct Tile {
     f32x4 s[2][QB];
+  };
+  auto qk = [&](int t) __attribute__((always_inline)) -> Tile {
+    Tile x;
+    const unsigned char* ks = smem + (t % R::NS) * R::SLOT;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) s[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int qb = 0; qb < QB; ++qb) x.s[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bf16x8 kf[DB][2];
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(ks + kb * 16 * (D * 2) + koff[db]);
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, kv);
+      for (int kb = 0; kb < 2; ++kb)
+        kf[db][kb] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(ks + kb * 16 * (D * 2) + koff[db]));
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][db], s[kb][qb], 0, 0, 0);
-      }
-    }
-
-    // ---- ancestor words, once per wave, at its first sub-tile with tree keys:
-    //      every lane follows the parent chains of its rows' nodes (parent[a]
-    //      read from lane a % 64 by shuffles, all lanes active); each step
-    //      moves to a lower index, so 128 steps end every walk
-    if (!words_ready && abs0 + R::SUB > n_kv) {
-      int a[QB];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) a[qb] = node[qb];
-      for (int step = 0; step < 128; ++step) {
-        bool live = false;
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) live |= a[qb] >= 0;
-        if (!__any(live)) break;
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-          const int x = a[qb];
-          if (x >= 0) {
-            if (x < 64) mw0[qb] |= 1ull << x;
-            else mw1[qb] |= 1ull << (x - 64);
-          }
-          const int plo = __shfl(par_lo, x & 63, PTD_WAVE);
-          const int phi = __shfl(par_hi, x & 63, PTD_WAVE);
-          int nx = x >= 64 ? phi : plo;
-          if (x < 0) {
-            nx = -1;
-          } else if (nx < -1 || nx >= x) {  // not topological
-            ptd::report(p.dev_status, PTD_ERR_BAD_TREE);
-            nx = -1;
-          }
-          a[qb] = nx;
-        }
-      }
-      words_ready = true;
-    }
-
-    // ---- visibility: past the chunk end, or a tree key that is not an ancestor
-    if (abs0 + R::SUB > n_kv || abs0 + R::SUB > end) {
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = abs0 + kb * 16 + l4 * 4 + e;
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) {
-            bool vis = key < end;
-            if (vis && key >= n_kv) {
-              const int a = key - n_kv;
-              // branchless pick of word a>>6 (0 or 1) for small trees
-              const uint64_t hi_sel = 0ull - static_cast<uint64_t>(a >> 6);
-              const uint64_t word = small_tree ? (mw0[qb] ^ ((mw0[qb] ^ mw1[qb]) & hi_sel))
-                                               : mrow[qb][a >> 6];
-              vis = (word >> (a & 63)) & 1ull;
-            }
-            if (!vis) s[kb][qb][e] = -INFINITY;
-          }
-        }
-    }
+        for (int qb = 0; qb < QB; ++qb)
+          x.s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[db][kb], qf[qb][db], x.s[kb][qb], 0, 0, 0);
+    return x;
+  };
 
-    // ---- online softmax (exp2 domain), lane-local per query column
+  // ---- online softmax (exp2 domain, lane-local per query column) and
+  //      O^T (d x queries) += V^T P^T for sub-tile t
+  auto softmax_pv = [&](int t, const Tile& x) __attribute__((always_inline)) {
+    const f32x4 (&s)[2][QB] = x.s;
+    const unsigned char* vs = smem + (t % R::NS) * R::SLOT + R::PART;
+    // V^T fragments do not depend on P: read them first, so that the softmax
+    // covers their latency.  K-slot j of lane group l4 is key 4*l4 + j
+    // (j < 4) or 16 + 4*l4 + (j - 4), matching the S^T layout; source lane
+    // 4*j + q of a 16-lane group points at V[key_j][16*dt + 4q], and lane i of
+    // the group receives V[key_0..3][16*dt + i].
+    bf16x8 vf[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const i16x4 lo = lds_read_tr16(vs + voff[dt]);
+      const i16x4 hi = lds_read_tr16(vs + 16 * (D * 2) + voff[dt]);
+      const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
+      const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
+      const u32x4 vv = {l2[0], l2[1], h2[0], h2[1]};
+      vf[dt] = __builtin_bit_cast(bf16x8, vv);
+    }
     bf16x8 pf[QB], pfl[QB];
     bool rescale = false;
     float alpha[QB];
@@ -436,8 +439,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     for (int qb = 0; qb < QB; ++qb) {
       float mx = fmaxf(fmaxf(fmaxf(s[0][qb][0], s[0][qb][1]), fmaxf(s[0][qb][2], s[0][qb][3])),
                        fmaxf(fmaxf(s[1][qb][0], s[1][qb][1]), fmaxf(s[1][qb][2], s[1][qb][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, PTD_WAVE));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, PTD_WAVE));
+      mx = max_xor32(max_xor16(mx));
       // lazy rescale: the reference max only moves when the new scores exceed
       // it by more than 2^8 in the exp2 domain, so p <= 256 and O/l is unchanged
       const float m_cand = fmaxf(m[qb], mx);
@@ -473,25 +475,110 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[qb][dt] *= alpha[qb];
     }
-
-    // ---- O^T (d x queries) += V^T P^T.  K-slot j of lane group l4 is key
-    //      4*l4 + j (j < 4) or 16 + 4*l4 + (j - 4), matching the S^T layout.
-    //      V^T comes from two LDS transpose reads: source lane 4*j + q of a
-    //      16-lane group points at V[key_j][16*dt + 4q], and lane i of the
-    //      group receives V[key_0..3][16*dt + i].
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const i16x4 lo = lds_read_tr16(vs + voff[dt]);
-      const i16x4 hi = lds_read_tr16(vs + 16 * (D * 2) + voff[dt]);
-      const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
-      const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
-      const u32x4 vv = {l2[0], l2[1], h2[0], h2[1]};
-      const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
-        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb], o[qb][dt], 0, 0, 0);
-        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pfl[qb], o[qb][dt], 0, 0, 0);
+        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf[qb], o[qb][dt], 0, 0, 0);
+        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pfl[qb], o[qb][dt], 0, 0, 0);
       }
+    }
+  };
+
+  // Rounds.  With 3 * WK ring slots or more the rounds are software-
+  // pipelined: round rd issues the QK MFMAs of its new sub-tile and then runs
+  // the softmax and PV of the previous round's sub-tile while they execute; a
+  // slot is then read up to one round after its own and refilled two rounds
+  // after it, and one extra iteration finishes the last sub-tile.  Otherwise
+  // each round finishes its own sub-tile and refills the previous round's.
+  constexpr bool kPipe = 3 * WK <= R::NS;
+  constexpr int kLag = kPipe ? 2 : 1;  // rounds between a slot's use and its refill
+  Tile sc;      // pipelined: masked scores of the sub-tile awaiting its PV
+  int tc = -1;  // that sub-tile, or -1
+  for (int rd = 0; rd < nrounds + (kPipe ? 1 : 0); ++rd) {
+    int t = -1;
+    if (rd < nrounds) {
+      const int issued = min(ntiles, R::NS + max(0, rd - kLag) * WK);
+      const int needed = min(ntiles, (rd + 1) * WK);
+      wait_vmcnt_le((issued - needed) * R::DPS);
+      lds_barrier();
+      if (rd >= kLag) {
+        for (int j = 0; j < WK; ++j) {
+          const int tt = R::NS + (rd - kLag) * WK + j;
+          if (tt < ntiles) issue(tt);
+        }
+      }
+      t = rd * WK + kg;
+      if (t >= ntiles || !wave_live) t = -1;
+    }
+    Tile x;
+    if (t >= 0) {
+      x = qk(t);
+      // ---- scores of keys past the chunk end, or of tree keys that are
+      //      not ancestors, become -inf (inline: the same code in a lambda
+      //      writing the tile was miscompiled)
+      const int abs0 = start + t * R::SUB;
+      // ancestor words, once per wave, at its first sub-tile with tree keys:
+      // every lane follows the parent chains of its rows' nodes (parent[a] read
+      // from lane a % 64 by shuffles, all lanes active); each step moves to a
+      // lower index, so 128 steps end every walk
+      if (!words_ready && abs0 + R::SUB > n_kv) {
+        int a[QB];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) a[qb] = node[qb];
+        for (int step = 0; step < 128; ++step) {
+          bool live = false;
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) live |= a[qb] >= 0;
+          if (!__any(live)) break;
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) {
+            const int x = a[qb];
+            const uint64_t bit = 1ull << (x & 63);  // branchless: no indexed word pair
+            mw0[qb] |= (x >= 0 && x < 64) ? bit : 0ull;
+            mw1[qb] |= (x >= 64) ? bit : 0ull;
+            const int plo = __shfl(par_lo, x & 63, PTD_WAVE);
+            const int phi = __shfl(par_hi, x & 63, PTD_WAVE);
+            int nx = x >= 64 ? phi : plo;
+            if (x < 0) {
+              nx = -1;
+            } else if (nx < -1 || nx >= x) {  // not topological
+              ptd::report(p.dev_status, PTD_ERR_BAD_TREE);
+              nx = -1;
+            }
+            a[qb] = nx;
+          }
+        }
+        words_ready = true;
+      }
+      if (abs0 + R::SUB > n_kv || abs0 + R::SUB > end) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int key = abs0 + kb * 16 + l4 * 4 + e;
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
+              bool vis = key < end;
+              if (vis && key >= n_kv) {
+                const int a = key - n_kv;
+                // branchless pick of word a>>6 (0 or 1) for small trees
+                const uint64_t hi_sel = 0ull - static_cast<uint64_t>(a >> 6);
+                const uint64_t word = small_tree ? (mw0[qb] ^ ((mw0[qb] ^ mw1[qb]) & hi_sel))
+                                                 : mrow[qb][a >> 6];
+                vis = (word >> (a & 63)) & 1ull;
+              }
+              if (!vis) x.s[kb][qb][e] = -INFINITY;
+            }
+          }
+      }
+    }
+    if constexpr (kPipe) {
+      if (tc >= 0) softmax_pv(tc, sc);
+      sc = x;
+      tc = t;
+    } else {
+      if (t >= 0) softmax_pv(t, x);
     }
   }
   wait_vmcnt<0>();
@@ -500,64 +587,76 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   // ---- per-column totals of the softmax denominator
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    lsum[qb] += __shfl_xor(lsum[qb], 16, PTD_WAVE);
-    lsum[qb] += __shfl_xor(lsum[qb], 32, PTD_WAVE);
+    lsum[qb] = sum_xor32(sum_xor16(lsum[qb]));
   }
 
-  // ---- epilogue: every wave parks its fragments in LDS (16-byte units of a
-  //      (qb, dt) block permuted by (dt*4 + l4) so that the row-wise reads
-  //      below spread over the banks), then all threads merge the key groups
-  //      (fixed order) and write whole rows with coalesced stores
-  {
-    f32x4* so = reinterpret_cast<f32x4*>(smem);
-    float2* sml = reinterpret_cast<float2*>(smem + 8 * QB * DT * 64 * 16);
-    const int wslot = wr * WK + kg;
+  // ---- epilogue.  The key groups of a row group hold their fragments in the
+  //      same lane layout (lane: query column l16, d = 16*dt + 4*l4 + 0..3), so
+  //      the merge is lane-local: every wave parks its fragments and (m, l)
+  //      per column in LDS, then wave (wr, kg) merges the key groups (fixed
+  //      order) for d-tiles [kg*DPW, (kg+1)*DPW) of its row group and stores
+  //      them.  With one key group the fragments are stored directly.
+  constexpr int DPW = DT / WK;  // d-tiles merged and stored per wave
+  static_assert(DT % WK == 0, "d-tiles per wave");
+  const bool all_rows = rowbase + 16 * QB <= p.M;  // uniform: the common case
+  auto store_tile = [&](int qb, int dt, f32x4 acc, float mc, float den) {
+    const int r = rowbase + qb * 16 + l16;
+    if (!all_rows && r >= p.M) return;
+    if (p.splits == 1) {
+      const int i = r / p.G, hg = r % p.G;
+      const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D +
+                         16 * dt + 4 * l4;
+      const f32x4 v = acc * (1.0f / den);
+      if (p.out_bf16) {
+        const u32x2 w2 = {ptd::cvt_pk_bf16(v[0], v[1]), ptd::cvt_pk_bf16(v[2], v[3])};
+        *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.out) + off) = w2;
+      } else {
+        *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + off) = v;
+      }
+    } else {
+      const size_t prow = ((static_cast<size_t>(split) * p.B + b) * p.Hkv + g) * p.M + r;
+      *reinterpret_cast<f32x4*>(p.part_o + prow * D + 16 * dt + 4 * l4) = acc;
+      if (dt == 0 && l4 == 0) p.part_ml[prow] = make_float2(mc, den);
+    }
+  };
+  if constexpr (WK == 1) {
+    if (!wave_live) return;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) store_tile(qb, dt, o[qb][dt], m[qb] * p.c, lsum[qb]);
+  } else {
+    f32x4* so = reinterpret_cast<f32x4*>(smem);  // [WR][WK][QB][DT][64]
+    float2* sml = reinterpret_cast<float2*>(smem + PARK_O);  // [WR][WK][QB][64]
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        so[((wslot * QB + qb) * DT + dt) * 64 + l4 * 16 + (l16 ^ ((dt * 4 + l4) & 15))] = o[qb][dt];
-      if (l4 == 0) sml[(wslot * QB + qb) * 16 + l16] = make_float2(m[qb], lsum[qb]);
+      for (int dt = 0; dt < DT; ++dt) so[(((wr * WK + kg) * QB + qb) * DT + dt) * 64 + lane] = o[qb][dt];
+      sml[((wr * WK + kg) * QB + qb) * 64 + lane] = make_float2(m[qb], lsum[qb]);
     }
-  }
-  __syncthreads();
-  {
-    const f32x4* so = reinterpret_cast<const f32x4*>(smem);
-    const float2* sml = reinterpret_cast<const float2*>(smem + 8 * QB * DT * 64 * 16);
-    constexpr int D4 = D / 4;
-    const int rows_here = min(p.rows_per_pass, p.M - pr0);
-    for (int e = tid; e < rows_here * D4; e += kThreads) {
-      const int row = e / D4, d4 = e % D4;
-      const int wrr = row / (16 * QB), qb = (row % (16 * QB)) / 16, r16 = row % 16;
-      const int dt = d4 / 4, q4 = d4 % 4;
-      const int pos = q4 * 16 + (r16 ^ ((dt * 4 + q4) & 15));
-      float mm = kNegBig;
+    lds_barrier();
+    if (!wave_live) return;
 #pragma unroll
-      for (int k2 = 0; k2 < WK; ++k2) mm = fmaxf(mm, sml[((wrr * WK + k2) * QB + qb) * 16 + r16].x);
-      float den = 0.f;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int qb = 0; qb < QB; ++qb) {
+      float mk[WK], w[WK];
+      float mm = kNegBig, den = 0.f;
 #pragma unroll
       for (int k2 = 0; k2 < WK; ++k2) {
-        const float2 ml = sml[((wrr * WK + k2) * QB + qb) * 16 + r16];
-        const float w = __builtin_amdgcn_exp2f((ml.x - mm) * p.c);
-        den += w * ml.y;
-        acc += so[(((wrr * WK + k2) * QB + qb) * DT + dt) * 64 + pos] * w;
+        mk[k2] = sml[((wr * WK + k2) * QB + qb) * 64 + lane].x;
+        mm = fmaxf(mm, mk[k2]);
       }
-      const int r = pr0 + row;
-      if (p.splits == 1) {
-        const int i = r / p.G, hg = r % p.G;
-        const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D + d4 * 4;
-        const f32x4 v = acc * (1.0f / den);
-        if (p.out_bf16) {
-          const u32x2 w2 = {ptd::cvt_pk_bf16(v[0], v[1]), ptd::cvt_pk_bf16(v[2], v[3])};
-          *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.out) + off) = w2;
-        } else {
-          *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + off) = v;
-        }
-      } else {
-        const size_t prow = ((static_cast<size_t>(split) * p.B + b) * p.Hkv + g) * p.M + r;
-        *reinterpret_cast<f32x4*>(p.part_o + prow * D + d4 * 4) = acc;
-        if (d4 == 0) p.part_ml[prow] = make_float2(mm * p.c, den);
+#pragma unroll
+      for (int k2 = 0; k2 < WK; ++k2) {
+        w[k2] = __builtin_amdgcn_exp2f((mk[k2] - mm) * p.c);
+        den += w[k2] * sml[((wr * WK + k2) * QB + qb) * 64 + lane].y;
+      }
+#pragma unroll
+      for (int j = 0; j < DPW; ++j) {
+        const int dt = kg * DPW + j;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k2 = 0; k2 < WK; ++k2) acc += so[(((wr * WK + k2) * QB + qb) * DT + dt) * 64 + lane] * w[k2];
+        store_tile(qb, dt, acc, mm * p.c, den);
       }
     }
   }
