@@ -102,7 +102,13 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
 
 // Same copy from a wave-uniform base address (SGPR pair) plus a per-lane
 // 32-bit byte offset: moving to the next tile changes only the scalar base.
-__device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff, uint32_t lds) {
+// The base must be uniform over the wave; it is moved to SGPRs explicitly.
+__device__ __forceinline__ void dma16_s(const void* base, uint32_t voff, uint32_t lds) {
+  // (readfirstlane returns int: widen through uint32_t, never sign-extend)
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b)));
+  const uint64_t sbase = (static_cast<uint64_t>(hi) << 32) | lo;
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -186,10 +192,13 @@ __device__ __forceinline__ i16x4 lds_read_tr16(const unsigned char* p) {
 }
 
 // LDS layout of one 32-key sub-tile: K rows then V rows, each [32][D] bf16,
-// row-major with the 16-byte chunks of row r stored XOR-permuted by (r mod CH)
-// (CH = D/8 chunks per row).  The permutation makes the K-operand reads
-// (16 rows x one chunk per 16 lanes) and the V transpose reads (16 rows x 32
-// bytes) hit distinct banks.
+// row-major with the 16-byte chunks of row r stored XOR-permuted by f(r)
+// (CH = D/8 chunks per row).  For D = 128, f(r) = ((r mod 8) << 1) | bit 3
+// of r: a bijection on 16 rows, so the K-operand reads (16 rows x one chunk
+// per 16 lanes) hit distinct banks, and f >> 1 is distinct over rows 0..7 and
+// over rows 8..15, so each half-wave of a V transpose read (8 rows x 2
+// adjacent chunks) covers all 16 chunk positions once.  For D = 64,
+// f(r) = r mod 8.
 template <int D>
 struct Ring {
   static constexpr int CH = D / 8;                   // 16-byte chunks per row
@@ -200,7 +209,10 @@ struct Ring {
   static constexpr int DPS = 2 * SUB * CH / kThreads;  // copies per thread per sub-tile
   static constexpr int BYTES = NS * SLOT;
   static_assert(DPS >= 1 && (2 * SUB * CH) % kThreads == 0, "sub-tile split");
-  __device__ static int swz(int row, int chunk) { return chunk ^ (row & (CH - 1)); }
+  __device__ static int swz(int row, int chunk) {
+    if constexpr (CH == 16) return chunk ^ (((row & 7) << 1) | ((row >> 3) & 1));
+    else return chunk ^ (row & (CH - 1));
+  }
 };
 
 template <int D, int QB, int WR>
@@ -432,28 +444,60 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       const u32x4 vv = {l2[0], l2[1], h2[0], h2[1]};
       vf[dt] = __builtin_bit_cast(bf16x8, vv);
     }
-    bf16x8 pf[QB], pfl[QB];
-    bool rescale = false;
-    float alpha[QB];
+    // exponents t = s*c - m*c against the current reference max m.  Lazy
+    // rescale: m only moves when a new score exceeds it by more than 2^8 in
+    // the exp2 domain (so p <= 256 and O/l is unchanged); in the common case
+    // no score of the wave does, and the row maxima are not needed at all.
+    float tv[QB][8];
+    bool over = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      float mx = fmaxf(fmaxf(fmaxf(s[0][qb][0], s[0][qb][1]), fmaxf(s[0][qb][2], s[0][qb][3])),
-                       fmaxf(fmaxf(s[1][qb][0], s[1][qb][1]), fmaxf(s[1][qb][2], s[1][qb][3])));
-      mx = max_xor32(max_xor16(mx));
-      // lazy rescale: the reference max only moves when the new scores exceed
-      // it by more than 2^8 in the exp2 domain, so p <= 256 and O/l is unchanged
-      const float m_cand = fmaxf(m[qb], mx);
-      const bool need = (m_cand - m[qb]) * p.c > 8.0f;
-      alpha[qb] = need ? __builtin_amdgcn_exp2f((m[qb] - m_cand) * p.c) : 1.0f;
-      rescale |= need;
-      if (need) m[qb] = m_cand;
       const float mc = m[qb] * p.c;
-      float pv[8];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        pv[e] = __builtin_amdgcn_exp2f(fmaf(s[0][qb][e], p.c, -mc));
-        pv[4 + e] = __builtin_amdgcn_exp2f(fmaf(s[1][qb][e], p.c, -mc));
+        tv[qb][e] = fmaf(s[0][qb][e], p.c, -mc);
+        tv[qb][4 + e] = fmaf(s[1][qb][e], p.c, -mc);
       }
+      const float tmax = fmaxf(fmaxf(fmaxf(tv[qb][0], tv[qb][1]), fmaxf(tv[qb][2], tv[qb][3])),
+                               fmaxf(fmaxf(tv[qb][4], tv[qb][5]), fmaxf(tv[qb][6], tv[qb][7])));
+      over |= tmax > 8.0f;
+    }
+    if (__any(over)) {  // new reference maxima for the rows whose scores moved past it
+      bool rescale = false;
+      float alpha[QB];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float mx = fmaxf(fmaxf(fmaxf(s[0][qb][0], s[0][qb][1]), fmaxf(s[0][qb][2], s[0][qb][3])),
+                         fmaxf(fmaxf(s[1][qb][0], s[1][qb][1]), fmaxf(s[1][qb][2], s[1][qb][3])));
+        mx = max_xor32(max_xor16(mx));
+        const float m_cand = fmaxf(m[qb], mx);
+        const bool need = (m_cand - m[qb]) * p.c > 8.0f;
+        alpha[qb] = need ? __builtin_amdgcn_exp2f((m[qb] - m_cand) * p.c) : 1.0f;
+        rescale |= need;
+        if (need) {
+          m[qb] = m_cand;
+          const float mc = m_cand * p.c;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            tv[qb][e] = fmaf(s[0][qb][e], p.c, -mc);
+            tv[qb][4 + e] = fmaf(s[1][qb][e], p.c, -mc);
+          }
+          lsum[qb] *= alpha[qb];
+        }
+      }
+      if (__any(rescale)) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[qb][dt] *= alpha[qb];
+      }
+    }
+    bf16x8 pf[QB], pfl[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float pv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(tv[qb][e]);
       // p = hi + lo with hi = bf16(p), lo = bf16(p - hi): the PV product
       // then sees p to ~2^-17 relative instead of bf16's 2^-9
       u32x4 ph, pl;
@@ -465,15 +509,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
                                  pv[2 * w + 1] - ptd::bf16_hi(ph[w]));
         ps += pv[2 * w] + pv[2 * w + 1];
       }
-      lsum[qb] = lsum[qb] * alpha[qb] + ps;
+      lsum[qb] += ps;
       pf[qb] = __builtin_bit_cast(bf16x8, ph);
       pfl[qb] = __builtin_bit_cast(bf16x8, pl);
-    }
-    if (__any(rescale)) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[qb][dt] *= alpha[qb];
     }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
