@@ -10,9 +10,10 @@
 //
 // Kernels
 //   k_topk_row      one workgroup per (row, vocabulary slice), a slice being
-//                   at most 16 loads of 16 bytes per lane (131072 bf16 values):
-//                   a cheap lower bound of the KMAX-th best value leaves a few
-//                   candidates, selected by one wave (details below).
+//                   at most 32768 chunks of 16 bytes (262144 bf16 or 131072
+//                   fp32 values) streamed through LDS: a cheap lower bound of
+//                   the KMAX-th best value leaves a few candidates, selected
+//                   by one wave (details below).
 //   k_topk_scalar   rows that are not 16-byte aligned: one wave per (row,
 //                   slice) with element loads; each lane keeps a sorted list
 //                   of its KMAX best keys in registers.
@@ -20,8 +21,11 @@
 // sorted lists with a bitonic network.
 //   k_topk_merge    one wave per row merges the slice results the same way
 //                   (only when a row spans several slices).
-// The selected values are re-read from the logits, so topk_val carries the
-// row's own values (including the sign of a zero).
+// topk_val carries the row's own values (including the sign of a zero): the
+// candidates keep their bits, and the other paths re-read the logits.
+#include <algorithm>
+
+#include "ptd_async.hpp"
 #include "ptd_common.hpp"
 
 namespace {
@@ -117,30 +121,85 @@ __device__ __forceinline__ void emit(uint64_t key, int lane, int k, int V, const
   }
 }
 
-// One workgroup (16 waves) per (row, slice), a slice being at most kRowLoads
-// 16-byte loads per lane, all issued before any is consumed.
-//   1. Every lane takes the maximum of each of its chunks and of all of them.
-//   2. A lower bound tau of the slice's KMAX-th best value: the lanes of a
-//      wave form KMAX groups; each group's largest lane maximum is a distinct
-//      element, so the least of the KMAX group maxima is at most the KMAX-th
-//      best value.  The bound of the slice is the largest bound of its waves.
-//   3. Elements whose image reaches tau (few, for any spread of values) are
-//      appended to a candidate list in LDS, and one wave selects the KMAX
-//      best of the list.  If the list overflows (many values tied at the
-//      top), every lane instead keeps a sorted list of its best keys among
-//      those elements, re-read from memory, and the lists are merged.
+// One workgroup (16 waves) per (row, slice).  The slice streams through LDS
+// in batches of 4 chunks of 16 bytes per lane (64 KB), copied asynchronously
+// into two buffers so that the next batch lands while one is examined; the
+// loops over batches stay rolled, which keeps the kernel's code small (its
+// instructions are fetched once per CU, cold).  Per batch:
+//   1. Every lane takes the image of each of its chunks (bf16 images are 16
+//      bits wide and computed two at a time with packed 16-bit integer
+//      operations) and their maximum.
+//   2. A lower bound of the KMAX-th best value: the lanes of a wave form KMAX
+//      groups; each group's largest lane maximum is a distinct element, so
+//      the least of the KMAX group maxima is at most the KMAX-th best value.
+//      The running bound tau is the largest bound of any wave and batch so
+//      far: it only rises and never passes the slice's KMAX-th best value.
+//   3. Chunks whose image reaches tau are listed in LDS (the list holds a
+//      whole batch), then the workgroup examines the listed chunks a thread
+//      per element and appends the elements that reach tau to a candidate
+//      list.
+// The slice's last partial chunk (fewer than one chunk of elements) is read
+// with plain loads and checked against the final bound.  Then:
+//   4. The candidates are ranked by counting: the list is cut into parts,
+//      each thread counts the keys of one part above one candidate, and the
+//      counts are summed in LDS.  The candidates of rank below k are the
+//      result.  If the list overflows (many values tied at the top), every
+//      lane keeps a sorted list of its best keys among the elements that reach
+//      the final bound, re-read from memory, and the lists are merged.
 constexpr int kRowThreads = 1024;
-constexpr int kRowLoads = 16;   // 16-byte loads per lane per slice
-constexpr int kCandCap = 1024;  // LDS candidate list
+constexpr int kBatchLoads = 4;                                 // chunks per lane per batch
+constexpr int kBatchChunks = kRowThreads * kBatchLoads;        // 64 KB
+constexpr int kMaxSliceChunks = 8 * kBatchChunks;              // 512 KB per workgroup
+constexpr int kMinSliceChunks = 2048;                          // 32 KB
+constexpr int kTargetBlocks = 256;                             // one per CU
+constexpr int kCandCap = 1024;  // LDS candidate list (= kRowThreads)
 
-template <int KMAX, bool BF16>
-__device__ __forceinline__ void chunk_elems(const uint4& c, float (&x)[BF16 ? 8 : 4]) {
-  const uint32_t ws[4] = {c.x, c.y, c.z, c.w};
-#pragma unroll
-  for (int e = 0; e < (BF16 ? 8 : 4); ++e) {
-    if constexpr (BF16) x[e] = (e & 1) ? ptd::bf16_hi(ws[e >> 1]) : ptd::bf16_lo(ws[e >> 1]);
-    else x[e] = __uint_as_float(ws[e]);
+using s16x2 = short __attribute__((ext_vector_type(2)));
+
+// Images: order-preserving integers, 0 reserved for "no element".
+//   fp32: ord_of (-0 maps like +0).
+//   bf16: 0x8001 + v, v the 16-bit signed-order value (sign-magnitude turned
+//         into two's complement order by flipping the magnitude bits of
+//         negative values).  -0 maps one below +0, so a bound equal to the
+//         image of +0 is lowered to that of -0 before elements are compared.
+constexpr uint32_t kImgPosZeroBf16 = 0x8001u;
+__device__ __forceinline__ s16x2 sorder2(uint32_t d) {
+  const s16x2 v = __builtin_bit_cast(s16x2, d);
+  const s16x2 sg = v >> static_cast<short>(15);
+  return __builtin_bit_cast(s16x2, d ^ (__builtin_bit_cast(uint32_t, sg) & 0x7FFF7FFFu));
+}
+template <bool BF16>
+__device__ __forceinline__ uint32_t elem_img(uint32_t bits32) {  // bits of the fp32 value
+  if constexpr (BF16) {
+    const short h = static_cast<short>(bits32 >> 16);
+    const short o = static_cast<short>(h ^ ((h >> 15) & 0x7FFF));
+    return static_cast<uint32_t>(static_cast<int>(o) + 0x8001);
+  } else {
+    return ord_of(__uint_as_float(bits32));
   }
+}
+template <bool BF16>
+__device__ __forceinline__ uint32_t chunk_img(const uint4& c) {
+  if constexpr (BF16) {
+    const s16x2 m = __builtin_elementwise_max(__builtin_elementwise_max(sorder2(c.x), sorder2(c.y)),
+                                              __builtin_elementwise_max(sorder2(c.z), sorder2(c.w)));
+    return static_cast<uint32_t>(max(static_cast<int>(m.x), static_cast<int>(m.y)) + 0x8001);
+  } else {
+    return ord_of(fmaxf(fmaxf(__uint_as_float(c.x), __uint_as_float(c.y)),
+                        fmaxf(__uint_as_float(c.z), __uint_as_float(c.w))));
+  }
+}
+// fp32 bits of element e of a chunk
+template <bool BF16>
+__device__ __forceinline__ uint32_t chunk_bits(const uint4& c, int e) {
+  const uint32_t ws[4] = {c.x, c.y, c.z, c.w};
+  if constexpr (BF16) return (e & 1) ? (ws[e >> 1] & 0xFFFF0000u) : (ws[e >> 1] << 16);
+  else return ws[e];
+}
+// bound used in comparisons (see the bf16 image above)
+template <bool BF16>
+__device__ __forceinline__ uint32_t cmp_bound(uint32_t tau) {
+  return (BF16 && tau == kImgPosZeroBf16) ? tau - 1 : tau;
 }
 
 template <int KMAX, bool BF16>
@@ -149,117 +208,179 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
            int k, int32_t* __restrict__ argmax, int32_t* __restrict__ topk_idx,
            float* __restrict__ topk_val, uint64_t* __restrict__ part) {
   constexpr int E = BF16 ? 8 : 4;  // elements per 16-byte chunk
+  constexpr int ES = BF16 ? 2 : 4;
   constexpr int NW = kRowThreads / PTD_WAVE;
   constexpr int GL = PTD_WAVE / KMAX;  // lanes per group
+  __shared__ __attribute__((aligned(16))) uint4 s_buf[2][kBatchChunks];
   __shared__ uint64_t s_cand[kCandCap];
-  __shared__ uint32_t s_tau[NW];
+  __shared__ uint32_t s_bits[kCandCap];
+  __shared__ uint32_t s_rank[kCandCap];
+  __shared__ uint16_t s_list[kBatchChunks];
+  __shared__ uint32_t s_tau[2][NW];
+  __shared__ int s_nlist[2];
   __shared__ int s_cnt;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = blockIdx.x / slices, s = blockIdx.x % slices;
   const int v0 = s * slice_len;
   const int v1 = min(V, v0 + slice_len);
-  const void* rb = BF16 ? static_cast<const void*>(static_cast<const uint16_t*>(logits) + row * ld)
-                        : static_cast<const void*>(static_cast<const float*>(logits) + row * ld);
-  const int nfull = (v1 - v0) / E;  // whole chunks; chunk j = tid + u * kRowThreads
-  const int vt = v0 + nfull * E + tid;  // the slice's last partial chunk, one element per lane
+  const char* rb = static_cast<const char*>(logits) + static_cast<size_t>(row) * ld * ES;
+  const char* sb = rb + static_cast<size_t>(v0) * ES;  // the slice, 16-byte aligned
+  const int nfull = (v1 - v0) / E;  // whole chunks of the slice
+  const int nb = (nfull + kBatchChunks - 1) / kBatchChunks;
+  const int vt = v0 + nfull * E + tid;  // the last partial chunk, one element per lane
   const bool tail = vt < v1;
-  if (tid == 0) s_cnt = 0;
-  uint4 w[kRowLoads];
-#pragma unroll
-  for (int u = 0; u < kRowLoads; ++u) {
-    const int j = tid + u * kRowThreads;
-    if (j < nfull) {
-      const int v = v0 + j * E;
-      w[u] = BF16 ? *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(rb) + v)
-                  : *reinterpret_cast<const uint4*>(static_cast<const float*>(rb) + v);
-    }
-  }
-  const float xt = tail ? __uint_as_float(elem_bits<BF16>(rb, vt)) : 0.f;
+  const uint32_t bt = tail ? elem_bits<BF16>(rb, vt) : 0u;  // consumed after every copy
+  const uint32_t buf_lds = ptd::lds_addr(&s_buf[0][0]);
+  static_assert(kCandCap == kRowThreads, "one rank counter per thread");
 
-  // 1. chunk and lane maxima, as images (0 = no element)
-  uint32_t cm[kRowLoads];
-  uint32_t lm = tail ? ord_of(xt) : 0u;
+  // batch b -> buffer b & 1; lane's chunk u of a batch: u * kRowThreads + tid.
+  // Every lane copies (past the end: the slice's last chunk, never examined),
+  // so every wave has the same number of copies in flight per batch.
+  auto issue = [&](int b) {
+    const uint32_t lds = buf_lds + ((b & 1) * kBatchChunks + wave * PTD_WAVE) * 16;
 #pragma unroll
-  for (int u = 0; u < kRowLoads; ++u) {
-    cm[u] = 0;
-    if (tid + u * kRowThreads < nfull) {
-      float x[E];
-      chunk_elems<KMAX, BF16>(w[u], x);
-      float m = x[0];
+    for (int u = 0; u < kBatchLoads; ++u) {
+      const int j = min(b * kBatchChunks + u * kRowThreads + tid, nfull - 1);
+      ptd::dma16_s(sb, static_cast<uint32_t>(j) * 16u, lds + u * kRowThreads * 16);
+    }
+  };
+  s_rank[tid] = 0;
+  if (tid == 0) {
+    s_cnt = 0;
+    s_nlist[0] = 0;
+  }
+  if (nb > 0) issue(0);
+  if (nb > 1) issue(1);
+
+  auto append = [&](uint32_t bits, int v) {
+    const int pos = atomicAdd(&s_cnt, 1);
+    if (pos < kCandCap) {
+      s_cand[pos] = make_key(bits, static_cast<uint32_t>(v));
+      s_bits[pos] = bits;
+    }
+  };
+  uint32_t tau = 0;
+  for (int b = 0; b < nb; ++b) {
+    if (b + 1 < nb) ptd::wait_vmcnt<kBatchLoads>();
+    else ptd::wait_vmcnt<0>();
+    ptd::lds_barrier();  // batch b landed for every wave
+    if (tid == 0) s_nlist[(b + 1) & 1] = 0;  // the next batch's list
+
+    // 1. chunk images and the lane maximum
+    const uint4* buf = s_buf[b & 1];
+    uint32_t cm[kBatchLoads];
+    uint32_t lm = 0;
 #pragma unroll
-      for (int e = 1; e < E; ++e) m = fmaxf(m, x[e]);
-      cm[u] = ord_of(m);
+    for (int u = 0; u < kBatchLoads; ++u) {
+      const int c = u * kRowThreads + tid;
+      cm[u] = b * kBatchChunks + c < nfull ? chunk_img<BF16>(buf[c]) : 0u;
       lm = max(lm, cm[u]);
     }
-  }
-  // 2. the bound: max over the lane groups, then min over the groups
-  uint32_t g = lm;
+    // 2. the bound: max over the lane groups, then min over the groups
+    uint32_t g = lm;
 #pragma unroll
-  for (int o = 1; o < GL; o <<= 1) g = max(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
+    for (int o = 1; o < GL; o <<= 1) g = max(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
 #pragma unroll
-  for (int o = GL; o < PTD_WAVE; o <<= 1) g = min(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
-  if (lane == 0) s_tau[wave] = g;
-  __syncthreads();
-  uint32_t tau = 0;
+    for (int o = GL; o < PTD_WAVE; o <<= 1) g = min(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
+    if (lane == 0) s_tau[b & 1][wave] = g;
+    ptd::lds_barrier();
 #pragma unroll
-  for (int i = 0; i < NW; ++i) tau = max(tau, s_tau[i]);
+    for (int i = 0; i < NW; ++i) tau = max(tau, s_tau[b & 1][i]);
+    const uint32_t tc = cmp_bound<BF16>(tau);
 
-  // 3. collect the elements that reach tau
+    // 3. list the chunks that reach the bound, then examine them
 #pragma unroll
-  for (int u = 0; u < kRowLoads; ++u) {
-    if (cm[u] >= tau && cm[u] != 0) {
-      float x[E];
-      chunk_elems<KMAX, BF16>(w[u], x);
-      const int v = v0 + (tid + u * kRowThreads) * E;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        if (ord_of(x[e]) >= tau) {
-          const int pos = atomicAdd(&s_cnt, 1);
-          if (pos < kCandCap) s_cand[pos] = make_key(__float_as_uint(x[e]), static_cast<uint32_t>(v + e));
-        }
+    for (int u = 0; u < kBatchLoads; ++u) {
+      if (cm[u] != 0 && cm[u] >= tc) {
+        const int pos = atomicAdd(&s_nlist[b & 1], 1);
+        s_list[pos] = static_cast<uint16_t>(u * kRowThreads + tid);
       }
     }
+    ptd::lds_barrier();
+    const int nl = s_nlist[b & 1];
+    for (int i0 = 0; i0 < nl; i0 += kRowThreads / E) {
+      const int i = i0 + tid / E;
+      if (i < nl) {
+        const int c = s_list[i], e = tid & (E - 1);
+        const uint32_t bits = BF16 ? static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(buf + c)[e]) << 16
+                                   : reinterpret_cast<const uint32_t*>(buf + c)[e];
+        if (elem_img<BF16>(bits) >= tc) append(bits, v0 + (b * kBatchChunks + c) * E + e);
+      }
+    }
+    if (b + 2 < nb) {  // uniform
+      ptd::lds_barrier();  // every wave is done with buffer b & 1
+      issue(b + 2);
+    }
   }
-  if (tail && ord_of(xt) >= tau) {
-    const int pos = atomicAdd(&s_cnt, 1);
-    if (pos < kCandCap) s_cand[pos] = make_key(__float_as_uint(xt), static_cast<uint32_t>(vt));
-  }
+  if (nb == 0) __syncthreads();  // s_cnt cleared (no batch barrier passed)
+  const uint32_t tc = cmp_bound<BF16>(tau);
+  if (tail && elem_img<BF16>(bt) >= tc) append(bt, vt);
   __syncthreads();
-  int n = s_cnt;
+  const int n = s_cnt;
+
+  // 4. selection
+  if (n <= kCandCap) {  // uniform over the workgroup
+    int n2 = PTD_WAVE;  // candidates per part-set: a power of two >= n
+    while (n2 < n) n2 <<= 1;
+    const int parts = kRowThreads / n2;
+    const int i = tid & (n2 - 1), p = tid / n2;  // p is uniform over a wave
+    const int len = (n + parts - 1) / parts;
+    const int j0 = p * len, j1 = min(n, j0 + len);
+    const uint64_t mine = i < n ? s_cand[i] : ~0ull;
+    uint32_t above = 0;
+    for (int j = j0; j < j1; ++j) above += s_cand[j] > mine ? 1u : 0u;
+    if (above) atomicAdd(&s_rank[i], above);
+    __syncthreads();
+    if (tid < n) {
+      const uint32_t rank = s_rank[tid];
+      const uint64_t key = s_cand[tid];
+      if (slices == 1) {
+        const int32_t idx = static_cast<int32_t>(key_index(key));
+        if (rank == 0) argmax[row] = idx;
+        if (rank < static_cast<uint32_t>(k)) {
+          if (topk_idx) topk_idx[static_cast<size_t>(row) * k + rank] = idx;
+          if (topk_val) topk_val[static_cast<size_t>(row) * k + rank] = __uint_as_float(s_bits[tid]);
+        }
+      } else if (rank < static_cast<uint32_t>(KMAX)) {
+        part[static_cast<size_t>(blockIdx.x) * KMAX + rank] = key;
+      }
+    } else if (slices > 1 && tid < KMAX) {  // fewer candidates than KMAX: empty slots
+      part[static_cast<size_t>(blockIdx.x) * KMAX + tid] = 0;
+    }
+    return;
+  }
+  // overflow: per-lane sorted lists of the elements that reach the bound
   uint64_t l[KMAX];
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) l[j] = 0;
-  if (n > kCandCap) {  // uniform over the workgroup
-    for (int j = tid; j < nfull; j += kRowThreads) {
-      const int v = v0 + j * E;
-      const uint4 c = BF16 ? *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(rb) + v)
-                           : *reinterpret_cast<const uint4*>(static_cast<const float*>(rb) + v);
-      float x[E];
-      chunk_elems<KMAX, BF16>(c, x);
+  for (int j = tid; j < nfull; j += kRowThreads) {
+    const uint4 c = *reinterpret_cast<const uint4*>(sb + static_cast<size_t>(j) * 16);
+    const int v = v0 + j * E;
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint64_t key = make_key(__float_as_uint(x[e]), static_cast<uint32_t>(v + e));
-        if (ord_of(x[e]) >= tau && key > l[KMAX - 1]) insert<KMAX>(l, key);
-      }
+    for (int e = 0; e < E; ++e) {
+      const uint32_t bits = chunk_bits<BF16>(c, e);
+      const uint64_t key = make_key(bits, static_cast<uint32_t>(v + e));
+      if (elem_img<BF16>(bits) >= tc && key > l[KMAX - 1]) insert<KMAX>(l, key);
     }
-    if (tail) {
-      const uint64_t key = make_key(__float_as_uint(xt), static_cast<uint32_t>(vt));
-      if (key > l[KMAX - 1]) insert<KMAX>(l, key);
-    }
-    wave_merge<KMAX>(l);
-    if (lane < KMAX) {
-      uint64_t mine = 0;
-#pragma unroll
-      for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? l[r] : mine;
-      s_cand[wave * KMAX + lane] = mine;
-    }
-    __syncthreads();
-    n = NW * KMAX;
-#pragma unroll
-    for (int j = 0; j < KMAX; ++j) l[j] = 0;
   }
+  if (tail) {
+    const uint64_t key = make_key(bt, static_cast<uint32_t>(vt));
+    if (key > l[KMAX - 1]) insert<KMAX>(l, key);
+  }
+  wave_merge<KMAX>(l);
+  __syncthreads();  // every wave is done reading the candidate list
+  if (lane < KMAX) {
+    uint64_t mine = 0;
+#pragma unroll
+    for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? l[r] : mine;
+    s_cand[wave * KMAX + lane] = mine;
+  }
+  __syncthreads();
   if (wave != 0) return;
-  for (int i = lane; i < n; i += PTD_WAVE) insert<KMAX>(l, s_cand[i]);
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) l[j] = 0;
+  for (int i = lane; i < NW * KMAX; i += PTD_WAVE) insert<KMAX>(l, s_cand[i]);
   wave_merge<KMAX>(l);
   uint64_t mine = 0;
 #pragma unroll
@@ -336,10 +457,17 @@ bool make_topk_plan(int R, int V, int k, int elem_bytes, bool vec, TopkPlan* p) 
   p->kmax = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : k <= 8 ? 8 : 16;
   p->vec = vec;
   const int E = 16 / elem_bytes;
-  // a slice is at most one batch of loads per lane: a whole row per
-  // workgroup when it fits, so that no merge launch follows
-  const long long max_len = static_cast<long long>(kRowThreads) * kRowLoads * E;
+  // A slice is at most kMaxSliceChunks chunks.  One CU streams at most a few
+  // tens of GB/s, so when there are too few rows to occupy every CU, rows are
+  // split further (into slices of at least kMinSliceChunks chunks, at most
+  // one workgroup per CU in all: each holds most of a CU's LDS) at the cost
+  // of the merge launch.
+  const long long max_len = static_cast<long long>(kMaxSliceChunks) * E;
   int s = static_cast<int>((V + max_len - 1) / max_len);
+  if (vec) {
+    const int want = std::min(kTargetBlocks / R, (V / E) / kMinSliceChunks);
+    s = std::max(s, want);
+  }
   int len = (V + s - 1) / s;
   len = (len + 7) & ~7;  // keep slice starts 16-byte aligned
   s = (V + len - 1) / len;

@@ -53,8 +53,11 @@ def test_attention_workspace_sizes():
 
 
 def test_topk_workspace_sizes():
-    assert P.ptd_topk_workspace_bytes(65, 200000, 4) > 0    # several slices per row
-    assert P.ptd_topk_workspace_bytes(65, 32000, 4) == 0    # one workgroup per row
+    assert P.ptd_topk_workspace_bytes(65, 300000, 4) > 0    # several slices per row
+    assert P.ptd_topk_workspace_bytes(65, 200000, 4) > 0    # several fp32 slices per row
+    assert P.ptd_topk_workspace_bytes(65, 128256, 4) > 0    # few rows: split to fill the CUs
+    assert P.ptd_topk_workspace_bytes(256, 128256, 4) == 0  # enough rows: one workgroup per row
+    assert P.ptd_topk_workspace_bytes(65, 16000, 4) == 0    # too short to split
     assert P.ptd_topk_workspace_bytes(2048, 4000, 4) == 0   # one slice per row
     assert P.ptd_topk_workspace_bytes(4, 10, 11) == 0       # k > V
     assert P.ptd_topk_workspace_bytes(4, 100, 17) == 0      # k > PTD_MAX_K
@@ -92,7 +95,8 @@ def test_topk_verify_expand_mask_validation():
     assert _err(P.ptd_topk_argmax, FAKE, P.PTD_BF16, 4, 100, 100, 17, FAKE) == 2
     assert _err(P.ptd_topk_argmax, FAKE + 1, P.PTD_BF16, 4, 100, 100, 4, FAKE) == 4
     # a row beyond one workgroup's slice is split over slices, which needs a workspace
-    assert _err(P.ptd_topk_argmax, FAKE, P.PTD_BF16, 65, 200000, 200000, 4, FAKE) == 5
+    assert _err(P.ptd_topk_argmax, FAKE, P.PTD_BF16, 65, 300000, 300000, 4, FAKE) == 5
+    assert _err(P.ptd_topk_argmax, FAKE, P.PTD_F32, 65, 200000, 200000, 4, FAKE) == 5
     assert _err(P.ptd_verify, FAKE, FAKE, None, None, 1, 4, FAKE, FAKE, FAKE) == 1
     assert _err(P.ptd_verify, FAKE, FAKE, FAKE, None, 1, 0, FAKE, FAKE, FAKE) == 2
     assert _err(P.ptd_verify, FAKE, FAKE, FAKE, None, 1, P.PTD_MAX_T + 1, FAKE, FAKE, FAKE) == 2

@@ -82,7 +82,8 @@ def _topk_case(P, arr, k, ld=None):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("R,V,k", [(1, 1, 1), (3, 7, 5), (17, 1000, 4), (65, 32000, 4),
                                    (97, 32000, 5), (8, 32003, 16), (5, 128256, 8),
-                                   (1100, 4099, 2), (3, 70001, 8), (2, 200003, 16)])
+                                   (1100, 4099, 2), (3, 70001, 8), (2, 200003, 16),
+                                   (2, 300007, 4)])
 def test_topk_random(P, dtype, R, V, k):
     rng = np.random.default_rng(R * 7 + V + k)
     x = rng.standard_normal((R, V), dtype=np.float32) * np.float32(1.41)
@@ -124,6 +125,31 @@ def test_topk_many_ties_at_the_top(P, k):
         x[r, rng.choice(40000, n, replace=False)] = np.float32(9.0)
     _topk_case(P, x, k)
     _topk_case(P, W.f32_to_bf16_bits(x), k)
+
+
+@pytest.mark.parametrize("V", [32000, 3001])
+def test_topk_signed_zero_ties(P, V):
+    # the best values are zeros of both signs: they tie, lower index first
+    rng = np.random.default_rng(V)
+    x = -np.abs(rng.standard_normal((4, V), dtype=np.float32)) - np.float32(0.5)
+    for r in range(4):
+        pos = rng.choice(V, 12, replace=False)
+        x[r, pos] = np.where(np.arange(12) % 2 == r % 2, np.float32(-0.0), np.float32(0.0))
+    for k in (1, 5, 16):
+        _topk_case(P, x, k)
+        _topk_case(P, W.f32_to_bf16_bits(x), k)
+
+
+@pytest.mark.parametrize("n", [63, 64, 65, 100, 700])
+def test_topk_candidate_counts(P, n):
+    # n values tie at the top: ranked by counting up to 64, merged above
+    rng = np.random.default_rng(n)
+    x = rng.standard_normal((3, 32000), dtype=np.float32)
+    for r in range(3):
+        x[r, rng.choice(32000, n, replace=False)] = np.float32(7.5)
+    for k in (4, 16):
+        _topk_case(P, x, k)
+        _topk_case(P, W.f32_to_bf16_bits(x), k)
 
 
 def test_topk_golden(P):
