@@ -158,11 +158,11 @@ size_t ptd_topk_workspace_bytes(int32_t R, int32_t V, int32_t k);
  *                                  widened exactly to fp32
  * Order: value descending; equal values by the lower index; -0.0 equals +0.0.
  * Logits are expected non-NaN (NaN ordering is unspecified); +-inf are ordered.
- * A workspace is needed when rows are split over several workgroups: when V
- * exceeds one workgroup's slice (262144 bf16 or 131072 fp32 values), and when
- * fewer than 256 rows of at least 32768 bf16 (16384 fp32) values would leave
- * CUs idle.  ptd_topk_workspace_bytes gives its size, 0 when none is needed;
- * it needs no initialisation, and calls sharing one must not overlap.
+ * A workspace is needed when a row is split over several workgroups, that is
+ * when V exceeds one workgroup's slice (32768 bf16 or 16384 fp32 values);
+ * ptd_topk_workspace_bytes gives its size (the larger of the bf16 and fp32
+ * needs), 0 when none is needed.  It needs no initialisation, and calls
+ * sharing one must not overlap.
  * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_DTYPE, PTD_ERR_WORKSPACE,
  * PTD_ERR_HIP.
  */

@@ -10,19 +10,20 @@
 //
 // Kernels
 //   k_topk_row      one workgroup per (row, vocabulary slice), a slice being
-//                   at most 32768 chunks of 16 bytes (262144 bf16 or 131072
-//                   fp32 values) streamed through LDS: a cheap lower bound of
-//                   the KMAX-th best value leaves a few candidates, selected
-//                   by one wave (details below).
+//                   at most 4096 chunks of 16 bytes (32768 bf16 or 16384
+//                   fp32 values) copied into LDS: a cheap lower bound of the
+//                   KMAX-th best value leaves a few candidates, ranked by
+//                   counting (details below).
 //   k_topk_scalar   rows that are not 16-byte aligned: one wave per (row,
 //                   slice) with element loads; each lane keeps a sorted list
 //                   of its KMAX best keys in registers.
 // Sorted lists are merged by a butterfly of 6 steps per wave, each merging two
 // sorted lists with a bitonic network.
-//   k_topk_merge    one wave per row merges the slice results the same way
+//   k_topk_merge    one workgroup per row ranks the slice results by counting
 //                   (only when a row spans several slices).
-// topk_val carries the row's own values (including the sign of a zero): the
-// candidates keep their bits, and the other paths re-read the logits.
+// A slice result is KMAX (key, value bits) pairs in the workspace.  topk_val
+// carries the row's own values (including the sign of a zero): candidates
+// keep their bits; the rare paths that hold only keys re-read the logits.
 #include <algorithm>
 
 #include "ptd_async.hpp"
@@ -121,38 +122,43 @@ __device__ __forceinline__ void emit(uint64_t key, int lane, int k, int V, const
   }
 }
 
-// One workgroup (16 waves) per (row, slice).  The slice streams through LDS
-// in batches of 4 chunks of 16 bytes per lane (64 KB), copied asynchronously
-// into two buffers so that the next batch lands while one is examined; the
-// loops over batches stay rolled, which keeps the kernel's code small (its
-// instructions are fetched once per CU, cold).  Per batch:
+// Slot r of slice result `item` from a key alone (value bits re-read).
+template <bool BF16>
+__device__ __forceinline__ void store_part(uint64_t* part, int item, int kmax, int r, uint64_t key,
+                                           const void* row_base) {
+  uint64_t* q = part + (static_cast<size_t>(item) * kmax + r) * 2;
+  q[0] = key;
+  q[1] = key ? elem_bits<BF16>(row_base, key_index(key)) : 0u;
+}
+
+// One workgroup (16 waves) per (row, slice), a slice being at most one batch
+// of 4 chunks of 16 bytes per lane (64 KB), copied asynchronously into LDS
+// at the start.  The workgroup takes under half of a CU's LDS, so two share a
+// CU and each hides the other's memory latency.
 //   1. Every lane takes the image of each of its chunks (bf16 images are 16
 //      bits wide and computed two at a time with packed 16-bit integer
 //      operations) and their maximum.
-//   2. A lower bound of the KMAX-th best value: the lanes of a wave form KMAX
-//      groups; each group's largest lane maximum is a distinct element, so
-//      the least of the KMAX group maxima is at most the KMAX-th best value.
-//      The running bound tau is the largest bound of any wave and batch so
-//      far: it only rises and never passes the slice's KMAX-th best value.
-//   3. Chunks whose image reaches tau are listed in LDS (the list holds a
-//      whole batch), then the workgroup examines the listed chunks a thread
+//   2. A lower bound tau of the slice's KMAX-th best value: the lanes of a
+//      wave form KMAX groups; each group's largest lane maximum is a distinct
+//      element, so the least of the KMAX group maxima is at most the KMAX-th
+//      best value.  The bound of the slice is the largest bound of its waves.
+//   3. Chunks whose image reaches tau are listed in LDS (the list holds the
+//      whole slice), then the workgroup examines the listed chunks a thread
 //      per element and appends the elements that reach tau to a candidate
-//      list.
-// The slice's last partial chunk (fewer than one chunk of elements) is read
-// with plain loads and checked against the final bound.  Then:
+//      list.  The slice's last partial chunk (fewer than one chunk of
+//      elements) is read with plain loads and checked the same way.
 //   4. The candidates are ranked by counting: the list is cut into parts,
 //      each thread counts the keys of one part above one candidate, and the
 //      counts are summed in LDS.  The candidates of rank below k are the
 //      result.  If the list overflows (many values tied at the top), every
 //      lane keeps a sorted list of its best keys among the elements that reach
-//      the final bound, re-read from memory, and the lists are merged.
+//      tau, re-read from memory, and the lists are merged.
+// The kernel's loops stay rolled, which keeps its code small: its
+// instructions are fetched once per CU, cold.
 constexpr int kRowThreads = 1024;
-constexpr int kBatchLoads = 4;                                 // chunks per lane per batch
-constexpr int kBatchChunks = kRowThreads * kBatchLoads;        // 64 KB
-constexpr int kMaxSliceChunks = 8 * kBatchChunks;              // 512 KB per workgroup
-constexpr int kMinSliceChunks = 2048;                          // 32 KB
-constexpr int kTargetBlocks = 256;                             // one per CU
-constexpr int kCandCap = 1024;  // LDS candidate list (= kRowThreads)
+constexpr int kBatchLoads = 4;                           // chunks per lane
+constexpr int kSliceChunks = kRowThreads * kBatchLoads;  // 64 KB
+constexpr int kCandCap = 256;                            // LDS candidate list
 
 using s16x2 = short __attribute__((ext_vector_type(2)));
 
@@ -211,14 +217,13 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   constexpr int ES = BF16 ? 2 : 4;
   constexpr int NW = kRowThreads / PTD_WAVE;
   constexpr int GL = PTD_WAVE / KMAX;  // lanes per group
-  __shared__ __attribute__((aligned(16))) uint4 s_buf[2][kBatchChunks];
+  __shared__ __attribute__((aligned(16))) uint4 s_buf[kSliceChunks];
   __shared__ uint64_t s_cand[kCandCap];
   __shared__ uint32_t s_bits[kCandCap];
   __shared__ uint32_t s_rank[kCandCap];
-  __shared__ uint16_t s_list[kBatchChunks];
-  __shared__ uint32_t s_tau[2][NW];
-  __shared__ int s_nlist[2];
-  __shared__ int s_cnt;
+  __shared__ uint16_t s_list[kSliceChunks];
+  __shared__ uint32_t s_tau[NW];
+  __shared__ int s_nlist, s_cnt;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = blockIdx.x / slices, s = blockIdx.x % slices;
@@ -226,33 +231,52 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   const int v1 = min(V, v0 + slice_len);
   const char* rb = static_cast<const char*>(logits) + static_cast<size_t>(row) * ld * ES;
   const char* sb = rb + static_cast<size_t>(v0) * ES;  // the slice, 16-byte aligned
-  const int nfull = (v1 - v0) / E;  // whole chunks of the slice
-  const int nb = (nfull + kBatchChunks - 1) / kBatchChunks;
+  const int nfull = (v1 - v0) / E;  // whole chunks of the slice (at most kSliceChunks)
   const int vt = v0 + nfull * E + tid;  // the last partial chunk, one element per lane
   const bool tail = vt < v1;
-  const uint32_t bt = tail ? elem_bits<BF16>(rb, vt) : 0u;  // consumed after every copy
-  const uint32_t buf_lds = ptd::lds_addr(&s_buf[0][0]);
-  static_assert(kCandCap == kRowThreads, "one rank counter per thread");
 
-  // batch b -> buffer b & 1; lane's chunk u of a batch: u * kRowThreads + tid.
-  // Every lane copies (past the end: the slice's last chunk, never examined),
-  // so every wave has the same number of copies in flight per batch.
-  auto issue = [&](int b) {
-    const uint32_t lds = buf_lds + ((b & 1) * kBatchChunks + wave * PTD_WAVE) * 16;
+  // Every lane copies its kBatchLoads chunks (past the end: the slice's last
+  // chunk, never examined); chunk u of a lane is u * kRowThreads + tid.
+  if (nfull > 0) {
+    const uint32_t lds = ptd::lds_addr(s_buf) + wave * PTD_WAVE * 16;
 #pragma unroll
     for (int u = 0; u < kBatchLoads; ++u) {
-      const int j = min(b * kBatchChunks + u * kRowThreads + tid, nfull - 1);
+      const int j = min(u * kRowThreads + tid, nfull - 1);
       ptd::dma16_s(sb, static_cast<uint32_t>(j) * 16u, lds + u * kRowThreads * 16);
     }
-  };
-  s_rank[tid] = 0;
+  }
+  const uint32_t bt = tail ? elem_bits<BF16>(rb, vt) : 0u;
+  if (tid < kCandCap) s_rank[tid] = 0;
   if (tid == 0) {
     s_cnt = 0;
-    s_nlist[0] = 0;
+    s_nlist = 0;
   }
-  if (nb > 0) issue(0);
-  if (nb > 1) issue(1);
+  ptd::wait_vmcnt<0>();
+  ptd::lds_barrier();  // the slice landed for every wave
 
+  // 1. chunk images and the lane maximum
+  uint32_t cm[kBatchLoads];
+  uint32_t lm = tail ? elem_img<BF16>(bt) : 0u;
+#pragma unroll
+  for (int u = 0; u < kBatchLoads; ++u) {
+    const int c = u * kRowThreads + tid;
+    cm[u] = c < nfull ? chunk_img<BF16>(s_buf[c]) : 0u;
+    lm = max(lm, cm[u]);
+  }
+  // 2. the bound: max over the lane groups, then min over the groups
+  uint32_t g = lm;
+#pragma unroll
+  for (int o = 1; o < GL; o <<= 1) g = max(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
+#pragma unroll
+  for (int o = GL; o < PTD_WAVE; o <<= 1) g = min(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
+  if (lane == 0) s_tau[wave] = g;
+  ptd::lds_barrier();
+  uint32_t tau = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) tau = max(tau, s_tau[i]);
+  const uint32_t tc = cmp_bound<BF16>(tau);
+
+  // 3. list the chunks that reach the bound, then examine them
   auto append = [&](uint32_t bits, int v) {
     const int pos = atomicAdd(&s_cnt, 1);
     if (pos < kCandCap) {
@@ -260,62 +284,25 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
       s_bits[pos] = bits;
     }
   };
-  uint32_t tau = 0;
-  for (int b = 0; b < nb; ++b) {
-    if (b + 1 < nb) ptd::wait_vmcnt<kBatchLoads>();
-    else ptd::wait_vmcnt<0>();
-    ptd::lds_barrier();  // batch b landed for every wave
-    if (tid == 0) s_nlist[(b + 1) & 1] = 0;  // the next batch's list
-
-    // 1. chunk images and the lane maximum
-    const uint4* buf = s_buf[b & 1];
-    uint32_t cm[kBatchLoads];
-    uint32_t lm = 0;
 #pragma unroll
-    for (int u = 0; u < kBatchLoads; ++u) {
-      const int c = u * kRowThreads + tid;
-      cm[u] = b * kBatchChunks + c < nfull ? chunk_img<BF16>(buf[c]) : 0u;
-      lm = max(lm, cm[u]);
-    }
-    // 2. the bound: max over the lane groups, then min over the groups
-    uint32_t g = lm;
-#pragma unroll
-    for (int o = 1; o < GL; o <<= 1) g = max(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
-#pragma unroll
-    for (int o = GL; o < PTD_WAVE; o <<= 1) g = min(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
-    if (lane == 0) s_tau[b & 1][wave] = g;
-    ptd::lds_barrier();
-#pragma unroll
-    for (int i = 0; i < NW; ++i) tau = max(tau, s_tau[b & 1][i]);
-    const uint32_t tc = cmp_bound<BF16>(tau);
-
-    // 3. list the chunks that reach the bound, then examine them
-#pragma unroll
-    for (int u = 0; u < kBatchLoads; ++u) {
-      if (cm[u] != 0 && cm[u] >= tc) {
-        const int pos = atomicAdd(&s_nlist[b & 1], 1);
-        s_list[pos] = static_cast<uint16_t>(u * kRowThreads + tid);
-      }
-    }
-    ptd::lds_barrier();
-    const int nl = s_nlist[b & 1];
-    for (int i0 = 0; i0 < nl; i0 += kRowThreads / E) {
-      const int i = i0 + tid / E;
-      if (i < nl) {
-        const int c = s_list[i], e = tid & (E - 1);
-        const uint32_t bits = BF16 ? static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(buf + c)[e]) << 16
-                                   : reinterpret_cast<const uint32_t*>(buf + c)[e];
-        if (elem_img<BF16>(bits) >= tc) append(bits, v0 + (b * kBatchChunks + c) * E + e);
-      }
-    }
-    if (b + 2 < nb) {  // uniform
-      ptd::lds_barrier();  // every wave is done with buffer b & 1
-      issue(b + 2);
+  for (int u = 0; u < kBatchLoads; ++u) {
+    if (cm[u] != 0 && cm[u] >= tc) {
+      const int pos = atomicAdd(&s_nlist, 1);
+      s_list[pos] = static_cast<uint16_t>(u * kRowThreads + tid);
     }
   }
-  if (nb == 0) __syncthreads();  // s_cnt cleared (no batch barrier passed)
-  const uint32_t tc = cmp_bound<BF16>(tau);
   if (tail && elem_img<BF16>(bt) >= tc) append(bt, vt);
+  ptd::lds_barrier();
+  const int nl = s_nlist;
+  for (int i0 = 0; i0 < nl; i0 += kRowThreads / E) {
+    const int i = i0 + tid / E;
+    if (i < nl) {
+      const int c = s_list[i], e = tid & (E - 1);
+      const uint32_t bits = BF16 ? static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(s_buf + c)[e]) << 16
+                                 : reinterpret_cast<const uint32_t*>(s_buf + c)[e];
+      if (elem_img<BF16>(bits) >= tc) append(bits, v0 + c * E + e);
+    }
+  }
   __syncthreads();
   const int n = s_cnt;
 
@@ -343,23 +330,28 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
           if (topk_val) topk_val[static_cast<size_t>(row) * k + rank] = __uint_as_float(s_bits[tid]);
         }
       } else if (rank < static_cast<uint32_t>(KMAX)) {
-        part[static_cast<size_t>(blockIdx.x) * KMAX + rank] = key;
+        uint64_t* q = part + (static_cast<size_t>(blockIdx.x) * KMAX + rank) * 2;
+        q[0] = key;
+        q[1] = s_bits[tid];
       }
     } else if (slices > 1 && tid < KMAX) {  // fewer candidates than KMAX: empty slots
-      part[static_cast<size_t>(blockIdx.x) * KMAX + tid] = 0;
+      uint64_t* q = part + (static_cast<size_t>(blockIdx.x) * KMAX + tid) * 2;
+      q[0] = 0;
+      q[1] = 0;
     }
     return;
   }
-  // overflow: per-lane sorted lists of the elements that reach the bound
+
+  // overflow: per-lane sorted lists of the slice's elements that reach tau
   uint64_t l[KMAX];
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) l[j] = 0;
-  for (int j = tid; j < nfull; j += kRowThreads) {
-    const uint4 c = *reinterpret_cast<const uint4*>(sb + static_cast<size_t>(j) * 16);
-    const int v = v0 + j * E;
+  for (int c = tid; c < nfull; c += kRowThreads) {
+    const uint4 w = s_buf[c];
+    const int v = v0 + c * E;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const uint32_t bits = chunk_bits<BF16>(c, e);
+      const uint32_t bits = chunk_bits<BF16>(w, e);
       const uint64_t key = make_key(bits, static_cast<uint32_t>(v + e));
       if (elem_img<BF16>(bits) >= tc && key > l[KMAX - 1]) insert<KMAX>(l, key);
     }
@@ -369,12 +361,11 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
     if (key > l[KMAX - 1]) insert<KMAX>(l, key);
   }
   wave_merge<KMAX>(l);
-  __syncthreads();  // every wave is done reading the candidate list
   if (lane < KMAX) {
     uint64_t mine = 0;
 #pragma unroll
     for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? l[r] : mine;
-    s_cand[wave * KMAX + lane] = mine;
+    s_cand[wave * KMAX + lane] = mine;  // every wave is past its reads of s_cand
   }
   __syncthreads();
   if (wave != 0) return;
@@ -385,11 +376,8 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   uint64_t mine = 0;
 #pragma unroll
   for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? l[r] : mine;
-  if (slices == 1) {
-    emit<BF16>(mine, lane, k, V, rb, row, argmax, topk_idx, topk_val);
-  } else if (lane < KMAX) {
-    part[static_cast<size_t>(blockIdx.x) * KMAX + lane] = mine;
-  }
+  if (slices == 1) emit<BF16>(mine, lane, k, V, rb, row, argmax, topk_idx, topk_val);
+  else if (lane < KMAX) store_part<BF16>(part, blockIdx.x, KMAX, lane, mine, rb);
 }
 
 // Rows that are not 16-byte aligned: one wave per (row, slice), element loads.
@@ -417,26 +405,61 @@ k_topk_scalar(const void* __restrict__ logits, int R, int V, long long ld, int s
   uint64_t mine = 0;
 #pragma unroll
   for (int r = 0; r < KMAX; ++r) mine = (lane == r) ? l[r] : mine;
-  if (slices == 1) {
-    emit<BF16>(mine, lane, k, V, rb, row, argmax, topk_idx, topk_val);
-  } else if (lane < KMAX) {
-    part[static_cast<size_t>(item) * KMAX + lane] = mine;
-  }
+  if (slices == 1) emit<BF16>(mine, lane, k, V, rb, row, argmax, topk_idx, topk_val);
+  else if (lane < KMAX) store_part<BF16>(part, item, KMAX, lane, mine, rb);
 }
 
+// One workgroup per row: the row's slices * KMAX (key, bits) pairs are ranked
+// by counting like the candidates of k_topk_row (empty slots hold key 0,
+// below every element, so they never reach a rank below k <= V).  Beyond
+// kThreads pairs, wave 0 merges sorted lists instead.
 template <int KMAX, bool BF16>
 __global__ void __launch_bounds__(kThreads)
-k_topk_merge(const void* __restrict__ logits, int R, int V, long long ld, int slices, int k,
+k_topk_merge(const void* __restrict__ logits, int V, long long ld, int slices, int k,
              const uint64_t* __restrict__ part, int32_t* __restrict__ argmax,
              int32_t* __restrict__ topk_idx, float* __restrict__ topk_val) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * (kThreads / PTD_WAVE) + (threadIdx.x >> 6);
-  if (row >= R) return;  // whole wave
+  __shared__ uint64_t s_key[kThreads];
+  __shared__ uint32_t s_rank[kThreads];
+  const int tid = threadIdx.x, lane = tid & 63, row = blockIdx.x;
+  const int n = slices * KMAX;
+  const uint64_t* pr = part + static_cast<size_t>(row) * n * 2;
+  if (n <= kThreads) {  // uniform
+    uint64_t key = 0;
+    uint32_t bits = 0;
+    if (tid < n) {
+      key = pr[2 * tid];
+      bits = static_cast<uint32_t>(pr[2 * tid + 1]);
+      s_key[tid] = key;
+    }
+    s_rank[tid] = 0;
+    __syncthreads();
+    int n2 = PTD_WAVE;
+    while (n2 < n) n2 <<= 1;
+    const int parts = kThreads / n2;
+    const int i = tid & (n2 - 1), p = tid / n2;
+    const int len = (n + parts - 1) / parts;
+    const int j0 = p * len, j1 = min(n, j0 + len);
+    const uint64_t mine = i < n ? s_key[i] : ~0ull;
+    uint32_t above = 0;
+    for (int j = j0; j < j1; ++j) above += s_key[j] > mine ? 1u : 0u;
+    if (above) atomicAdd(&s_rank[i], above);
+    __syncthreads();
+    if (tid < n) {
+      const uint32_t rank = s_rank[tid];
+      if (rank < static_cast<uint32_t>(k)) {
+        const int32_t idx = static_cast<int32_t>(key_index(key));
+        if (rank == 0) argmax[row] = idx;
+        if (topk_idx) topk_idx[static_cast<size_t>(row) * k + rank] = idx;
+        if (topk_val) topk_val[static_cast<size_t>(row) * k + rank] = __uint_as_float(bits);
+      }
+    }
+    return;
+  }
+  if (tid >= PTD_WAVE) return;
   uint64_t l[KMAX];
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) l[j] = 0;
-  const uint64_t* pr = part + static_cast<size_t>(row) * slices * KMAX;
-  for (int j = lane; j < slices * KMAX; j += PTD_WAVE) insert<KMAX>(l, pr[j]);
+  for (int j = lane; j < n; j += PTD_WAVE) insert<KMAX>(l, pr[2 * j]);
   wave_merge<KMAX>(l);
   uint64_t mine = 0;
 #pragma unroll
@@ -457,24 +480,17 @@ bool make_topk_plan(int R, int V, int k, int elem_bytes, bool vec, TopkPlan* p) 
   p->kmax = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : k <= 8 ? 8 : 16;
   p->vec = vec;
   const int E = 16 / elem_bytes;
-  // A slice is at most kMaxSliceChunks chunks.  One CU streams at most a few
-  // tens of GB/s, so when there are too few rows to occupy every CU, rows are
-  // split further (into slices of at least kMinSliceChunks chunks, at most
-  // one workgroup per CU in all: each holds most of a CU's LDS) at the cost
-  // of the merge launch.
-  const long long max_len = static_cast<long long>(kMaxSliceChunks) * E;
+  // A slice is at most kSliceChunks whole chunks (plus, for the last, a
+  // partial chunk): rows longer than that are split and merged afterwards.
+  const long long max_len = static_cast<long long>(kSliceChunks) * E;
   int s = static_cast<int>((V + max_len - 1) / max_len);
-  if (vec) {
-    const int want = std::min(kTargetBlocks / R, (V / E) / kMinSliceChunks);
-    s = std::max(s, want);
-  }
   int len = (V + s - 1) / s;
   len = (len + 7) & ~7;  // keep slice starts 16-byte aligned
   s = (V + len - 1) / len;
   if (static_cast<long long>(R) * s > (1LL << 30)) return false;
   p->slices = s;
   p->slice_len = len;
-  p->ws_bytes = s > 1 ? static_cast<size_t>(R) * s * p->kmax * sizeof(uint64_t) : 0;
+  p->ws_bytes = s > 1 ? static_cast<size_t>(R) * s * p->kmax * 2 * sizeof(uint64_t) : 0;
   return true;
 }
 
@@ -490,8 +506,8 @@ void launch(const TopkPlan& pl, const void* logits, int R, int V, long long ld, 
                        dim3(kThreads), 0, st, logits, R, V, ld, pl.slices, pl.slice_len, k, am,
                        ti, tv, part);
   if (pl.slices > 1)
-    hipLaunchKernelGGL((k_topk_merge<KMAX, BF16>), dim3((R + WPB - 1) / WPB), dim3(kThreads), 0,
-                       st, logits, R, V, ld, pl.slices, k, part, am, ti, tv);
+    hipLaunchKernelGGL((k_topk_merge<KMAX, BF16>), dim3(R), dim3(kThreads), 0, st, logits, V, ld,
+                       pl.slices, k, part, am, ti, tv);
 }
 
 template <bool BF16>

@@ -54,10 +54,9 @@ def test_attention_workspace_sizes():
 
 def test_topk_workspace_sizes():
     assert P.ptd_topk_workspace_bytes(65, 300000, 4) > 0    # several slices per row
-    assert P.ptd_topk_workspace_bytes(65, 200000, 4) > 0    # several fp32 slices per row
-    assert P.ptd_topk_workspace_bytes(65, 128256, 4) > 0    # few rows: split to fill the CUs
-    assert P.ptd_topk_workspace_bytes(256, 128256, 4) == 0  # enough rows: one workgroup per row
-    assert P.ptd_topk_workspace_bytes(65, 16000, 4) == 0    # too short to split
+    assert P.ptd_topk_workspace_bytes(65, 128256, 4) == 65 * 8 * 4 * 16   # 8 fp32 slices (bf16: 4)
+    assert P.ptd_topk_workspace_bytes(65, 32768, 4) == 65 * 2 * 4 * 16    # 2 fp32 slices
+    assert P.ptd_topk_workspace_bytes(65, 16384, 4) == 0    # one slice per row
     assert P.ptd_topk_workspace_bytes(2048, 4000, 4) == 0   # one slice per row
     assert P.ptd_topk_workspace_bytes(4, 10, 11) == 0       # k > V
     assert P.ptd_topk_workspace_bytes(4, 100, 17) == 0      # k > PTD_MAX_K
