@@ -424,8 +424,11 @@ k_verify_expand(const int32_t* __restrict__ argmax, const int32_t* __restrict__ 
 //   - expansion: children masks by LDS atomic OR; a node's added candidates
 //     as a bit set over its top-k row; breadth-first positions level by
 //     level: the nodes of a level write their child counts at their
-//     positions, one wave scan gives every node its first child's position,
-//     and old children add their rank among their siblings
+//     positions, a scan over the wave (7 ballots: counts stay below 128)
+//     gives every node its first child's position, and old children add
+//     their rank among their siblings to their parent's
+// Wave reductions use DPP and the gfx950 lane swaps (VALU only); gathers
+// from other lanes are the remaining LDS-latency steps.
 // ===========================================================================
 constexpr int kWaveNodes = 64;
 
@@ -433,6 +436,37 @@ __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
   const uint32_t lo = __shfl(static_cast<uint32_t>(v), src, PTD_WAVE);
   const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src, PTD_WAVE);
   return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Maximum over the wave: within quads (quad permutes), half-rows and rows
+// (mirrors), then across rows by v_permlane16_swap / v_permlane32_swap (with
+// both operands holding the value, the two results are the lane's value and
+// that of lane ^ 16, resp. lane ^ 32).
+__device__ __forceinline__ int wave_max_i32(int x) {
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));  // row_mirror
+  const auto r16 = __builtin_amdgcn_permlane16_swap(static_cast<uint32_t>(x), static_cast<uint32_t>(x), false, false);
+  x = max(static_cast<int>(r16[0]), static_cast<int>(r16[1]));
+  const auto r32 = __builtin_amdgcn_permlane32_swap(static_cast<uint32_t>(x), static_cast<uint32_t>(x), false, false);
+  return max(static_cast<int>(r32[0]), static_cast<int>(r32[1]));
+}
+
+// Exclusive prefix sum over the lanes of c in [0, 128), and the total: one
+// ballot per bit, counted below the lane with mbcnt.
+__device__ __forceinline__ int wave_excl_scan7(int c, int* total) {
+  int x = 0, t = 0;
+#pragma unroll
+  for (int bit = 0; bit < 7; ++bit) {
+    const uint64_t m = __ballot((c >> bit) & 1);
+    const int below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
+                                                __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0));
+    x += below << bit;
+    t += __popcll(m) << bit;
+  }
+  *total = t;
+  return x;
 }
 
 template <bool VERIFY, bool EXPAND, int KM>
@@ -444,7 +478,7 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
             int32_t* __restrict__ out_tokens, int32_t* __restrict__ parent_next,
             int32_t* __restrict__ tokens_next, int32_t* __restrict__ tree_len_next,
             int32_t* dev_status) {
-  __shared__ int s_tok[kWaveNodes], s_cnt[kWaveNodes], s_start[kWaveNodes];
+  __shared__ int s_tok[kWaveNodes], s_cnt[kWaveNodes];
   __shared__ uint64_t s_cm[kWaveNodes];
   __shared__ int s_width[PTD_MAX_DEPTH];
   const int lane = threadIdx.x, b = blockIdx.x;
@@ -452,9 +486,9 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
   const bool live = lane < n;
   const uint64_t below = (1ull << lane) - 1ull;
 
-  // every global load first
-  const int par = live ? parent[static_cast<size_t>(b) * T + lane] : -1;
-  const int tok = live ? tokens[static_cast<size_t>(b) * T + lane] : 0;
+  // every global load first, none waiting for tree_len
+  const int par_in = lane < T ? parent[static_cast<size_t>(b) * T + lane] : -1;
+  const int tok_in = lane < T ? tokens[static_cast<size_t>(b) * T + lane] : 0;
   int am_lo = 0, am_hi = 0;  // argmax rows lane and 64
   if (VERIFY) {
     const int32_t* am = argmax + static_cast<size_t>(b) * (T + 1);
@@ -465,9 +499,11 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
   if (EXPAND) {
     const int32_t* row = topk_idx + (static_cast<size_t>(b) * (T + 1) + lane + 1) * k;
 #pragma unroll
-    for (int r = 0; r < KM; ++r) cand[r] = (live && r < k) ? row[r] : 0;
+    for (int r = 0; r < KM; ++r) cand[r] = (lane < T && r < k) ? row[r] : 0;
     s_width[lane] = ws.w[lane];
   }
+  const int par = live ? par_in : -1;
+  const int tok = live ? tok_in : 0;
   s_tok[lane] = tok;
   s_cm[lane] = 0ull;
   s_cnt[lane] = 0;
@@ -499,9 +535,7 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
     const int am_par = pa < kWaveNodes ? am_par_lo : am_hi;
     const uint64_t elig = __ballot(live && tok == am_par);
     const bool accepted = live && (anc & ~elig) == 0ull;
-    int key = accepted ? dep * 128 + (127 - lane) : -1;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) key = max(key, __shfl_xor(key, o, PTD_WAVE));
+    const int key = wave_max_i32(accepted ? dep * 128 + (127 - lane) : -1);
     const int klen = key < 0 ? 0 : key / 128;
     const int best = key < 0 ? -1 : 127 - key % 128;
     const uint64_t path = shfl64(anc, best < 0 ? 0 : best);
@@ -565,24 +599,20 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
         tn[q] = tok;
       }
     }
+    // an old child's rank among its siblings (children masks are complete)
+    const int srank = live && par >= 0 ? __popcll(s_cm[par] & below) : 0;
     int lo = 0, hi = min(__popcll(roots), T_max);
     for (int level = 1; lo < hi; ++level) {
+      // positions [lo, hi) hold this level; lane p of the scan is position lo + p
       const bool here = pos >= 0 && dep == level;
       if (here) s_cnt[pos] = ncld + nnew;
       __syncthreads();
       const int p = lo + lane;
-      const int c = p < hi ? s_cnt[p] : 0;
-      int x = c;
-#pragma unroll
-      for (int o = 1; o < PTD_WAVE; o <<= 1) {
-        const int y = __shfl_up(x, o, PTD_WAVE);
-        if (lane >= o) x += y;
-      }
-      const int total = __shfl(x, PTD_WAVE - 1, PTD_WAVE);
-      if (p < hi) s_start[p] = hi + x - c;
-      __syncthreads();
+      int total;
+      const int first = hi + wave_excl_scan7(p < hi ? s_cnt[p] : 0, &total);
+      const int start = __shfl(first, here ? pos - lo : 0, PTD_WAVE);  // valid where here
       if (here) {  // added children: after the old ones, in candidate order
-        int q = s_start[pos] + ncld;
+        int q = start + ncld;
 #pragma unroll
         for (int r = 0; r < KM; ++r) {
           if ((sel >> r) & 1u) {
@@ -594,9 +624,11 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
           }
         }
       }
-      const int ppos = __shfl(pos, par >= 0 ? par : lane, PTD_WAVE);
-      if (live && par >= 0 && dep == level + 1 && ppos >= 0) {
-        const int q = s_start[ppos] + __popcll(s_cm[par] & below);
+      const int src = par >= 0 ? par : lane;
+      const int pstart = __shfl(start, src, PTD_WAVE);
+      const int ppos = __shfl(pos, src, PTD_WAVE);
+      if (live && par >= 0 && dep == level + 1 && ppos >= 0) {  // the parent is on this level
+        const int q = pstart + srank;
         if (q < T_max) {
           pos = q;
           pn[q] = ppos;
