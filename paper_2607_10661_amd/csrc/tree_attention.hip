@@ -25,6 +25,8 @@
 //   k_attn_valu    fp32 (or bf16) inputs on the vector ALUs, fp32 throughout.
 #include <math.h>
 
+#include <type_traits>
+
 #include "ptd_async.hpp"
 #include "ptd_common.hpp"
 #include "ptd_internal.hpp"
@@ -44,9 +46,12 @@ using f32x4 = float __attribute__((ext_vector_type(4)));
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 using u32x2 = uint32_t __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 512;   // 8 waves
+constexpr int kThreads = 512;   // 8 waves: two per SIMD
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;  // running-max start: finite, below any score
+// Sequences with at least this many keys carry the softmax weights p as
+// bf16 into the PV product; shorter ones as bf16 hi + lo (see k_attn_mfma).
+constexpr int kPlainKeys = 512;
 
 struct AttnParams {
   const void* q;
@@ -128,15 +133,27 @@ struct Ring {
   static constexpr int SUB = 32;                     // keys per sub-tile
   static constexpr int PART = SUB * D * 2;           // bytes of K (or V) per sub-tile
   static constexpr int SLOT = 2 * PART;              // K + V
-  static constexpr int NS = (144 * 1024) / SLOT;     // sub-tiles in the ring
+  static constexpr int NS = (160 * 1024) / SLOT;     // sub-tiles in the ring (all of LDS)
   static constexpr int DPS = 2 * SUB * CH / kThreads;  // copies per thread per sub-tile
   static constexpr int BYTES = NS * SLOT;
-  static_assert(DPS >= 1 && (2 * SUB * CH) % kThreads == 0, "sub-tile split");
+  static_assert((DPS == 1 || DPS % 2 == 0) && (2 * SUB * CH) % kThreads == 0, "sub-tile split");
   __device__ static int swz(int row, int chunk) {
     if constexpr (CH == 16) return chunk ^ (((row & 7) << 1) | ((row >> 3) & 1));
     else return chunk ^ (row & (CH - 1));
   }
 };
+
+// 16-byte global load into VGPRs, issued from inline asm like the copies, so
+// that the compiler does not track it: the caller waits with an explicit
+// vmcnt and then fences the registers (vector-memory operations retire in
+// issue order, so the loads issued before the copies complete first).
+__device__ __forceinline__ u32x4 gload16(const void* p) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+// Orders every later use of v after the preceding (volatile) wait.
+__device__ __forceinline__ void reg_fence(u32x4& v) { asm volatile("" : "+v"(v)); }
 
 template <int D, int QB, int WR>
 __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
@@ -146,9 +163,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   constexpr int DT = D / 16;                      // 16-wide d tiles (PV output rows)
   constexpr int PARK_O = WK > 1 ? WR * WK * QB * DT * 64 * 16 : 0;  // parked fragments
   constexpr int PARK_BYTES = PARK_O + (WK > 1 ? WR * WK * QB * 64 * 8 : 0);
-  constexpr int QDED = 16384;  // dedicated query region (blocks of <= 64 rows, D = 128)
-  constexpr int SMEM = (R::BYTES + QDED) > PARK_BYTES ? (R::BYTES + QDED) : PARK_BYTES;
+  constexpr int SMEM = R::BYTES > PARK_BYTES ? R::BYTES : PARK_BYTES;
   static_assert(R::NS >= 2 * WK, "ring must hold two rounds");
+  static_assert(QB * DB + 2 + R::NS * R::DPS <= 63, "vector-memory counter range");
   __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
 
   const int tid = threadIdx.x;
@@ -183,27 +200,29 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
                           (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D;
   const uint16_t* vbase = static_cast<const uint16_t*>(p.v) +
                           (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D;
-  const int rowbase = pass * p.rows_per_pass + wr * 16 * QB;
+  const int pr0 = pass * p.rows_per_pass;
+  const int rowbase = pr0 + wr * 16 * QB;
   const bool wave_live = rowbase < p.M;  // padding waves only copy and sync
 
-  f32x4 o[QB][DT];
-  float m[QB], lsum[QB];
+  // ---- query fragments straight to VGPRs (B operand of S^T = K Q^T): lane
+  //      holds Q[row l16][d = 32*db + 8*l4 .. +8]; issued before every copy
+  u32x4 qraw[QB][DB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    m[qb] = kNegBig;
-    lsum[qb] = 0.f;
+    const int r = min(rowbase + qb * 16 + l16, p.M - 1);
+    const int i = r / p.G, hg = r % p.G;
+    const uint16_t* src = static_cast<const uint16_t*>(p.q) +
+                          ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D + 8 * l4;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[qb][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int db = 0; db < DB; ++db) qraw[qb][db] = gload16(src + 32 * db);
   }
 
   // ---- sub-tile copies: thread tid moves chunks u*512 + tid of the
-  //      sub-tile's 2*32*CH chunks (K rows, then V rows)
+  //      sub-tile's 2*32*CH chunks (K rows, then V rows); chunk u of a thread
+  //      is K or V for the whole wave (SUB*CH is a multiple of 64)
   const uint32_t ring = lds_addr(smem);
-  // per-thread parts of the copy addresses (the same for every sub-tile)
-  // (chunk u of a thread is K or V for the whole wave: SUB*CH is a multiple
-  //  of 64)
+  uint32_t cp_voff[R::DPS], cp_lds[R::DPS];
   int cp_row[R::DPS], cp_off[R::DPS];
-  uint32_t cp_voff[R::DPS];
   bool cp_v[R::DPS];
 #pragma unroll
   for (int u = 0; u < R::DPS; ++u) {
@@ -213,98 +232,49 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     cp_row[u] = local / R::CH;
     cp_off[u] = R::swz(cp_row[u], local % R::CH) * 8;
     cp_voff[u] = static_cast<uint32_t>((cp_row[u] * D + cp_off[u]) * 2);
+    cp_lds[u] = static_cast<uint32_t>((u * kThreads + wave * PTD_WAVE) * 16);
   }
-  auto issue = [&](int t) __attribute__((always_inline)) {
-    const uint32_t slot_lds = ring + (t % R::NS) * R::SLOT;
+  // copy sub-tile t (keys start + 32t ..) into ring slot `slot`
+  auto issue = [&](int t, int slot) __attribute__((always_inline)) {
+    const uint32_t slot_lds = ring + slot * R::SLOT;
     const int row0 = start + t * R::SUB;
     if (row0 + R::SUB <= N) {  // whole sub-tile inside the keys: scalar base
       const size_t tile = static_cast<size_t>(row0) * D;
+      if constexpr (R::DPS == 1) {
+        dma16_s((cp_v[0] ? vbase : kbase) + tile, cp_voff[0], slot_lds + cp_lds[0]);
+      } else {
 #pragma unroll
-      for (int u = 0; u < R::DPS; ++u)
-        dma16_s((cp_v[u] ? vbase : kbase) + tile, cp_voff[u],
-                slot_lds + (u * kThreads + wave * PTD_WAVE) * 16);
+        for (int u = 0; u < R::DPS; u += 2)
+          ptd::dma16_s2((cp_v[u] ? vbase : kbase) + tile, cp_voff[u], slot_lds + cp_lds[u],
+                        (cp_v[u + 1] ? vbase : kbase) + tile, cp_voff[u + 1], slot_lds + cp_lds[u + 1]);
+      }
     } else {  // last sub-tile: rows past the keys re-read the last key
 #pragma unroll
       for (int u = 0; u < R::DPS; ++u) {
         const int grow = min(row0 + cp_row[u], N - 1);
         dma16((cp_v[u] ? vbase : kbase) + static_cast<size_t>(grow) * D + cp_off[u],
-              slot_lds + (u * kThreads + wave * PTD_WAVE) * 16);
+              slot_lds + cp_lds[u]);
       }
     }
   };
 
   const int ntiles = (end - start + R::SUB - 1) / R::SUB;
   const int nrounds = (ntiles + WK - 1) / WK;
+  const int ninit = min(ntiles, R::NS);
 
-  // ---- ancestor words of the rows' nodes.  Trees of <= 128 nodes: derived
-  //      in-kernel from parent[], two entries per lane (plain loads, first
-  //      consumed at the first tree sub-tile, which comes last); larger trees:
-  //      mask rows from the mask pass.
-  const int pr0 = pass * p.rows_per_pass;
+  // ---- parent[] entries for deriving ancestor words in-kernel (trees of
+  //      <= 128 nodes: two per lane), loaded untracked like the query rows
+  //      and, like them, before any copy
   const bool small_tree = p.W <= 2;
-  int node[QB];
-  const uint64_t* mrow[QB];
-  uint64_t mw0[QB], mw1[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int r = min(pr0 + wr * 16 * QB + qb * 16 + l16, p.M - 1);
-    node[qb] = r / p.G;
-    mrow[qb] = small_tree ? nullptr : p.mask + (static_cast<size_t>(b) * p.T + node[qb]) * p.W;
-    mw0[qb] = 0ull;
-    mw1[qb] = 0ull;
-  }
-  int par_lo = -1, par_hi = -1;
+  u32x4 par_raw = {0xFFFFFFFFu, 0xFFFFFFFFu, 0u, 0u};  // (parent[lane], parent[lane + 64])
   if (small_tree) {
     const int32_t* pb = p.parent + static_cast<size_t>(b) * p.T;
-    if (lane < p.T) par_lo = pb[lane];
-    if (lane + 64 < p.T) par_hi = pb[lane + 64];
+    // 4-byte untracked loads; lanes past T keep -1
+    if (lane < p.T) par_raw[0] = ptd::gload4(pb + lane);
+    if (lane + 64 < p.T) par_raw[1] = ptd::gload4(pb + lane + 64);
   }
-  bool words_ready = !small_tree;  // uniform over the wave
-
-  // ---- query rows of this pass go to LDS with the same asynchronous copies:
-  //      into a dedicated region when they fit (all K/V sub-tiles then start
-  //      at once), otherwise into the last ring slots, which turn into K/V
-  //      slots once the fragments are in registers
-  const int qbytes = p.rows_per_pass * D * 2;
-  const bool qded = qbytes <= QDED;
-  const int qslots = qded ? 0 : (qbytes + R::SLOT - 1) / R::SLOT;  // <= 4
-  const int qslot0 = R::NS - qslots;
-  const uint32_t qlds = qded ? ring + R::BYTES : ring + qslot0 * R::SLOT;
-  for (int c0 = wave * PTD_WAVE; c0 < p.rows_per_pass * R::CH; c0 += kThreads) {
-    const int c = c0 + lane;
-    const int rl = c / R::CH, pos = c % R::CH;
-    const int r = min(pr0 + rl, p.M - 1);
-    const int i = r / p.G, hg = r % p.G;
-    const uint16_t* src = static_cast<const uint16_t*>(p.q) +
-                          ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D +
-                          R::swz(rl, pos) * 8;
-    dma16(src, qlds + c0 * 16);
-  }
-  int pending = 0;  // this thread's copies issued after the query rows
-  for (int t = 0; t < min(ntiles, qslot0); ++t) {
-    issue(t);
-    pending += R::DPS;
-  }
-  wait_vmcnt_le(pending);
-  lds_barrier();
-
-  // query fragments (B operand of S^T = K Q^T): lane holds
-  // Q[row l16][d = 32*db + 8*l4 .. +8]
-  bf16x8 qf[QB][DB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int rl = wr * 16 * QB + qb * 16 + l16;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(
-          smem + (qlds - ring) + rl * (D * 2) + R::swz(rl, db * 4 + l4) * 16);
-      qf[qb][db] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
-  if (!qded) {
-    lds_barrier();  // the query slots become K/V slots
-    for (int t = qslot0; t < min(ntiles, R::NS); ++t) issue(t);
-  }
+  int par_lo = -1, par_hi = -1;
+  bf16x8 qf[QB][DB];  // set from qraw once the first wait has covered the loads
 
   // per-lane LDS byte offsets inside a sub-tile (the row's swizzle is the
   // same for both 16-row halves, which therefore differ by a constant)
@@ -318,46 +288,50 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   for (int dt = 0; dt < DT; ++dt)
     voff[dt] = key0 * (D * 2) + R::swz(key0, 2 * dt + (tq >> 1)) * 16 + (tq & 1) * 8;
 
-  // ---- S^T (keys x queries) = K Q^T for sub-tile t; lane: query l16, keys
-  //      16*kb + 4*l4 + e.  Every K fragment is read first (one LDS round trip).
   struct Tile {
     f32x4 s[2][QB];
   };
-  auto qk = [&](int t) __attribute__((always_inline)) -> Tile {
-    Tile x;
-    const unsigned char* ks = smem + (t % R::NS) * R::SLOT;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) x.s[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bf16x8 kf[DB][2];
+  struct KFrag {
+    bf16x8 k[DB][2];
+  };
+  // K fragments of the sub-tile in `slot` (A operand: 16 keys x 32 d)
+  auto read_k = [&](int slot) __attribute__((always_inline)) -> KFrag {
+    KFrag f;
+    const unsigned char* ks = smem + slot * R::SLOT;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        kf[db][kb] = __builtin_bit_cast(
+        f.k[db][kb] = __builtin_bit_cast(
             bf16x8, *reinterpret_cast<const u32x4*>(ks + kb * 16 * (D * 2) + koff[db]));
+    return f;
+  };
+  // S^T (keys x queries) = K Q^T; lane: query l16, keys 16*kb + 4*l4 + e
+  auto qk = [&](const KFrag& f) __attribute__((always_inline)) -> Tile {
+    Tile x;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) x.s[kb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
-          x.s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[db][kb], qf[qb][db], x.s[kb][qb], 0, 0, 0);
+          x.s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[db][kb], qf[qb][db], x.s[kb][qb], 0, 0, 0);
     return x;
   };
-
-  // ---- online softmax (exp2 domain, lane-local per query column) and
-  //      O^T (d x queries) += V^T P^T for sub-tile t
-  auto softmax_pv = [&](int t, const Tile& x) __attribute__((always_inline)) {
-    const f32x4 (&s)[2][QB] = x.s;
-    const unsigned char* vs = smem + (t % R::NS) * R::SLOT + R::PART;
-    // V^T fragments do not depend on P: read them first, so that the softmax
-    // covers their latency.  K-slot j of lane group l4 is key 4*l4 + j
-    // (j < 4) or 16 + 4*l4 + (j - 4), matching the S^T layout; source lane
-    // 4*j + q of a 16-lane group points at V[key_j][16*dt + 4q], and lane i of
-    // the group receives V[key_0..3][16*dt + i].
-    bf16x8 vf[DT];
+  // V^T fragments (A operand of O^T += V^T P^T).  K-slot j of lane group l4
+  // is key 4*l4 + j (j < 4) or 16 + 4*l4 + (j - 4), matching the S^T layout;
+  // source lane 4*j + q of a 16-lane group points at V[key_j][16*dt + 4q],
+  // and lane i of the group receives V[key_0..3][16*dt + i].
+  struct VFrag {
+    bf16x8 v[DT];
+  };
+  auto read_v = [&](int slot) __attribute__((always_inline)) -> VFrag {
+    VFrag f;
+    const unsigned char* vs = smem + slot * R::SLOT + R::PART;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       const i16x4 lo = lds_read_tr16(vs + voff[dt]);
@@ -365,185 +339,280 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
       const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
       const u32x4 vv = {l2[0], l2[1], h2[0], h2[1]};
-      vf[dt] = __builtin_bit_cast(bf16x8, vv);
+      f.v[dt] = __builtin_bit_cast(bf16x8, vv);
     }
-    // exponents t = s*c - m*c against the current reference max m.  Lazy
-    // rescale: m only moves when a new score exceeds it by more than 2^8 in
-    // the exp2 domain (so p <= 256 and O/l is unchanged); in the common case
-    // no score of the wave does, and the row maxima are not needed at all.
-    float tv[QB][8];
+    return f;
+  };
+
+  // ---- scores of keys past the chunk end, or of tree keys that are not
+  //      ancestors, become -inf.  For trees of <= 128 nodes the ancestor words
+  //      of the rows' nodes are derived here, at each sub-tile with tree keys
+  //      (only the last few of a sequence): every lane follows the parent
+  //      chains of its rows' nodes (parent[a] read from lane a % 64 by
+  //      shuffles, all lanes active); each step moves to a lower index, so
+  //      128 steps end every walk.  Larger trees read the mask pass's rows.
+  auto mask_tile = [&](Tile& x, int t) __attribute__((always_inline)) {
+    const int abs0 = start + t * R::SUB;
+    if (abs0 + R::SUB <= n_kv && abs0 + R::SUB <= end) return;
+    int node[QB];
+    uint64_t mw0[QB], mw1[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      node[qb] = min(rowbase + qb * 16 + l16, p.M - 1) / p.G;
+      mw0[qb] = 0ull;
+      mw1[qb] = 0ull;
+    }
+    if (small_tree && abs0 + R::SUB > n_kv) {
+      int a[QB];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) a[qb] = node[qb];
+      for (int step = 0; step < 128; ++step) {
+        bool live = false;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) live |= a[qb] >= 0;
+        if (!__any(live)) break;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          const int xa = a[qb];
+          const uint64_t bit = 1ull << (xa & 63);  // branchless: no indexed word pair
+          mw0[qb] |= (xa >= 0 && xa < 64) ? bit : 0ull;
+          mw1[qb] |= (xa >= 64) ? bit : 0ull;
+          const int plo = __shfl(par_lo, xa & 63, PTD_WAVE);
+          const int phi = __shfl(par_hi, xa & 63, PTD_WAVE);
+          int nx = xa >= 64 ? phi : plo;
+          if (xa < 0) {
+            nx = -1;
+          } else if (nx < -1 || nx >= xa) {  // not topological
+            ptd::report(p.dev_status, PTD_ERR_BAD_TREE);
+            nx = -1;
+          }
+          a[qb] = nx;
+        }
+      }
+    }
+    // visibility as selects only: per-element branches writing the tile
+    // through this lambda's reference were miscompiled
+    if (small_tree) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = abs0 + kb * 16 + l4 * 4 + e;
+          const int a = key - n_kv;
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) {
+            const uint64_t word = a >= 64 ? mw1[qb] : mw0[qb];
+            const bool anc = ((word >> (a & 63)) & 1ull) != 0;
+            const bool vis = key < end && (key < n_kv || anc);
+            x.s[kb][qb][e] = vis ? x.s[kb][qb][e] : -INFINITY;
+          }
+        }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = abs0 + kb * 16 + l4 * 4 + e;
+          const int a = min(max(key - n_kv, 0), p.T - 1);  // in-range row word for any key
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) {
+            const uint64_t word = p.mask[(static_cast<size_t>(b) * p.T + node[qb]) * p.W + (a >> 6)];
+            const bool anc = ((word >> (a & 63)) & 1ull) != 0;
+            const bool vis = key < end && (key < n_kv || anc);
+            x.s[kb][qb][e] = vis ? x.s[kb][qb][e] : -INFINITY;
+          }
+        }
+    }
+  };
+
+  // ---- online softmax state.  Scores become p = 2^(s*c - m*c) against a
+  //      reference maximum m per query row that moves lazily: the first
+  //      sub-tile in which a row sees a key sets it (O is still zero then),
+  //      and later it moves only when a score exceeds it by more than 16 in
+  //      the exp2 domain (thr = m + 16/c), so p <= 2^16 and O, l stay far
+  //      inside the fp32 range.  In the common case no score of the wave
+  //      passes thr and the row maxima are never formed.
+  f32x4 o[QB][DT];
+  float m[QB], nmc[QB], thr[QB], lsum[QB];
+  const float c = p.c;
+  const float span = 16.0f / c;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m[qb] = kNegBig;
+    nmc[qb] = -kNegBig * c;
+    thr[qb] = kNegBig;
+    lsum[qb] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[qb][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  auto check_scores = [&](const Tile& x) __attribute__((always_inline)) {
     bool over = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      const float mc = m[qb] * p.c;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        tv[qb][e] = fmaf(s[0][qb][e], p.c, -mc);
-        tv[qb][4 + e] = fmaf(s[1][qb][e], p.c, -mc);
-      }
-      const float tmax = fmaxf(fmaxf(fmaxf(tv[qb][0], tv[qb][1]), fmaxf(tv[qb][2], tv[qb][3])),
-                               fmaxf(fmaxf(tv[qb][4], tv[qb][5]), fmaxf(tv[qb][6], tv[qb][7])));
-      over |= tmax > 8.0f;
+      const float a = fmaxf(fmaxf(x.s[0][qb][0], x.s[0][qb][1]), x.s[0][qb][2]);
+      const float bb = fmaxf(fmaxf(x.s[0][qb][3], x.s[1][qb][0]), x.s[1][qb][1]);
+      const float cc = fmaxf(fmaxf(x.s[1][qb][2], x.s[1][qb][3]), a);
+      over |= fmaxf(bb, cc) > thr[qb];
     }
-    if (__any(over)) {  // new reference maxima for the rows whose scores moved past it
-      bool rescale = false;
-      float alpha[QB];
+    if (!__any(over)) return;
+    // rare: move the reference of the rows whose maximum passed thr
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        float mx = fmaxf(fmaxf(fmaxf(s[0][qb][0], s[0][qb][1]), fmaxf(s[0][qb][2], s[0][qb][3])),
-                         fmaxf(fmaxf(s[1][qb][0], s[1][qb][1]), fmaxf(s[1][qb][2], s[1][qb][3])));
-        mx = max_xor32(max_xor16(mx));
-        const float m_cand = fmaxf(m[qb], mx);
-        const bool need = (m_cand - m[qb]) * p.c > 8.0f;
-        alpha[qb] = need ? __builtin_amdgcn_exp2f((m[qb] - m_cand) * p.c) : 1.0f;
-        rescale |= need;
-        if (need) {
-          m[qb] = m_cand;
-          const float mc = m_cand * p.c;
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = fmaxf(fmaxf(fmaxf(x.s[0][qb][0], x.s[0][qb][1]), fmaxf(x.s[0][qb][2], x.s[0][qb][3])),
+                       fmaxf(fmaxf(x.s[1][qb][0], x.s[1][qb][1]), fmaxf(x.s[1][qb][2], x.s[1][qb][3])));
+      mx = max_xor32(max_xor16(mx));
+      if (mx > thr[qb]) {  // uniform over the row's four lanes
+        const float alpha = __builtin_amdgcn_exp2f((m[qb] - mx) * c);  // 0 for the first keys
+        m[qb] = mx;
+        nmc[qb] = -mx * c;
+        thr[qb] = mx + span;
+        lsum[qb] *= alpha;
+        // in-place scaling of the accumulators (asm keeps the compiler from
+        // duplicating them around this rarely taken path)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            tv[qb][e] = fmaf(s[0][qb][e], p.c, -mc);
-            tv[qb][4 + e] = fmaf(s[1][qb][e], p.c, -mc);
+            float v = o[qb][dt][e];
+            asm volatile("v_mul_f32 %0, %0, %1" : "+v"(v) : "v"(alpha));
+            o[qb][dt][e] = v;
           }
-          lsum[qb] *= alpha[qb];
-        }
-      }
-      if (__any(rescale)) {
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[qb][dt] *= alpha[qb];
       }
     }
-    bf16x8 pf[QB], pfl[QB];
+  };
+  // p of a tile as bf16 MFMA operands (B of O^T += V^T P^T: lane holds its
+  // query column's 8 keys); with PRECISE also the rounding residue p - bf16(p)
+  struct PFrag {
+    bf16x8 hi[QB], lo[QB];
+  };
+  auto softmax = [&](const Tile& x, bool precise) __attribute__((always_inline)) -> PFrag {
+    PFrag f;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float pv[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(tv[qb][e]);
-      // p = hi + lo with hi = bf16(p), lo = bf16(p - hi): the PV product
-      // then sees p to ~2^-17 relative instead of bf16's 2^-9
+      for (int e = 0; e < 4; ++e) {
+        pv[e] = __builtin_amdgcn_exp2f(fmaf(x.s[0][qb][e], c, nmc[qb]));
+        pv[4 + e] = __builtin_amdgcn_exp2f(fmaf(x.s[1][qb][e], c, nmc[qb]));
+      }
       u32x4 ph, pl;
-      float ps = 0.f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        ph[w] = ptd::cvt_pk_bf16(pv[2 * w], pv[2 * w + 1]);
-        pl[w] = ptd::cvt_pk_bf16(pv[2 * w] - ptd::bf16_lo(ph[w]),
-                                 pv[2 * w + 1] - ptd::bf16_hi(ph[w]));
-        ps += pv[2 * w] + pv[2 * w + 1];
+      for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[2 * w], pv[2 * w + 1]);
+      if (precise) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          pl[w] = ptd::cvt_pk_bf16(pv[2 * w] - ptd::bf16_lo(ph[w]),
+                                   pv[2 * w + 1] - ptd::bf16_hi(ph[w]));
+        f.lo[qb] = __builtin_bit_cast(bf16x8, pl);
       }
-      lsum[qb] += ps;
-      pf[qb] = __builtin_bit_cast(bf16x8, ph);
-      pfl[qb] = __builtin_bit_cast(bf16x8, pl);
+      lsum[qb] += ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
+      f.hi[qb] = __builtin_bit_cast(bf16x8, ph);
     }
+    return f;
+  };
+  auto pv_acc = [&](const VFrag& v, const PFrag& f, bool precise) __attribute__((always_inline)) {
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
+    for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf[qb], o[qb][dt], 0, 0, 0);
-        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pfl[qb], o[qb][dt], 0, 0, 0);
-      }
+      for (int qb = 0; qb < QB; ++qb)
+        o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v.v[dt], f.hi[qb], o[qb][dt], 0, 0, 0);
+    if (precise) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v.v[dt], f.lo[qb], o[qb][dt], 0, 0, 0);
     }
   };
 
-  // Rounds.  With 3 * WK ring slots or more the rounds are software-
-  // pipelined: round rd issues the QK MFMAs of its new sub-tile and then runs
-  // the softmax and PV of the previous round's sub-tile while they execute; a
-  // slot is then read up to one round after its own and refilled two rounds
-  // after it, and one extra iteration finishes the last sub-tile.  Otherwise
-  // each round finishes its own sub-tile and refills the previous round's.
-  constexpr bool kPipe = 3 * WK <= R::NS;
-  constexpr int kLag = kPipe ? 2 : 1;  // rounds between a slot's use and its refill
-  Tile sc;      // pipelined: masked scores of the sub-tile awaiting its PV
-  int tc = -1;  // that sub-tile, or -1
-  for (int rd = 0; rd < nrounds + (kPipe ? 1 : 0); ++rd) {
-    int t = -1;
-    if (rd < nrounds) {
-      const int issued = min(ntiles, R::NS + max(0, rd - kLag) * WK);
+  // ---- rounds.  Round rd holds sub-tiles rd*WK .. rd*WK + WK - 1 (wave kg
+  //      takes rd*WK + kg).  The two waves that share a SIMD (waves w and
+  //      w + 4) run a round in opposite orders, so that one issues MFMAs while
+  //      the other does the softmax on the vector ALUs:
+  //        phase A:  QK^T(rd) -> softmax(rd) -> PV(rd)
+  //        phase B:  softmax(rd - 1) -> PV(rd - 1) -> QK^T(rd)
+  //      (phase B carries its scores across the barrier).  A slot is read in
+  //      its own round and, by phase B, in the next one, so the slots of round
+  //      rd - 2 are refilled at the barrier of round rd; the data of round rd
+  //      is then issued by round rd - 1, which needs 3*WK ring slots.  With
+  //      more key groups every wave runs phase A and slots are refilled one
+  //      round after their use.
+  //      P is carried as bf16 when the sequence has at least kPlainKeys keys
+  //      (the softmax weight is then spread over many keys and bf16 rounding
+  //      of p moves the output by well under 1e-3); shorter sequences, where
+  //      a few keys can hold all the weight, carry p as bf16 hi + lo.
+  const bool precise = N < kPlainKeys;  // uniform over the workgroup
+  constexpr bool kPingPong = 3 * WK <= R::NS;
+  constexpr int LAG = kPingPong ? 2 : 1;  // rounds between a slot's use and its refill
+  static_assert((LAG + 1) * WK <= R::NS, "round data issued one round ahead");
+  const bool phase_b = kPingPong && ((wave >> 2) & 1) != 0;
+  auto finish = [&](const Tile& x, int slot) __attribute__((always_inline)) {
+    const VFrag vf = read_v(slot);
+    check_scores(x);
+    const PFrag pf = softmax(x, precise);
+    pv_acc(vf, pf, precise);
+  };
+  for (int t = 0; t < ninit; ++t) issue(t, t);
+  wait_vmcnt_le((ninit - min(ntiles, WK)) * R::DPS);  // round 0 (query rows, parents) landed
+  lds_barrier();
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      reg_fence(qraw[qb][db]);
+      qf[qb][db] = __builtin_bit_cast(bf16x8, qraw[qb][db]);
+    }
+  reg_fence(par_raw);
+  par_lo = static_cast<int>(par_raw[0]);
+  par_hi = static_cast<int>(par_raw[1]);
+
+  int cs = kg;       // ring slot of this wave's sub-tile of the current round
+  int rs = 0;        // slot refilled next (round rd - LAG's slots, in order)
+  Tile sc;           // phase B: scores waiting for their softmax + PV
+  int sc_slot = -1;  // phase B: their slot, or -1
+  for (int rd = 0; rd < nrounds; ++rd) {
+    if (rd > 0) {
+      const int issued = min(ntiles, R::NS + max(0, rd - LAG) * WK);
       const int needed = min(ntiles, (rd + 1) * WK);
       wait_vmcnt_le((issued - needed) * R::DPS);
       lds_barrier();
-      if (rd >= kLag) {
-        for (int j = 0; j < WK; ++j) {
-          const int tt = R::NS + (rd - kLag) * WK + j;
-          if (tt < ntiles) issue(tt);
+      if (rd >= LAG) {
+#pragma unroll
+        for (int w = 0; w < WK; ++w) {
+          const int tt = R::NS + (rd - LAG) * WK + w;
+          if (tt < ntiles) issue(tt, rs);
+          rs = rs + 1 == R::NS ? 0 : rs + 1;
         }
       }
-      t = rd * WK + kg;
-      if (t >= ntiles || !wave_live) t = -1;
     }
-    Tile x;
-    if (t >= 0) {
-      x = qk(t);
-      // ---- scores of keys past the chunk end, or of tree keys that are
-      //      not ancestors, become -inf (inline: the same code in a lambda
-      //      writing the tile was miscompiled)
-      const int abs0 = start + t * R::SUB;
-      // ancestor words, once per wave, at its first sub-tile with tree keys:
-      // every lane follows the parent chains of its rows' nodes (parent[a] read
-      // from lane a % 64 by shuffles, all lanes active); each step moves to a
-      // lower index, so 128 steps end every walk
-      if (!words_ready && abs0 + R::SUB > n_kv) {
-        int a[QB];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) a[qb] = node[qb];
-        for (int step = 0; step < 128; ++step) {
-          bool live = false;
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) live |= a[qb] >= 0;
-          if (!__any(live)) break;
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) {
-            const int x = a[qb];
-            const uint64_t bit = 1ull << (x & 63);  // branchless: no indexed word pair
-            mw0[qb] |= (x >= 0 && x < 64) ? bit : 0ull;
-            mw1[qb] |= (x >= 64) ? bit : 0ull;
-            const int plo = __shfl(par_lo, x & 63, PTD_WAVE);
-            const int phi = __shfl(par_hi, x & 63, PTD_WAVE);
-            int nx = x >= 64 ? phi : plo;
-            if (x < 0) {
-              nx = -1;
-            } else if (nx < -1 || nx >= x) {  // not topological
-              ptd::report(p.dev_status, PTD_ERR_BAD_TREE);
-              nx = -1;
-            }
-            a[qb] = nx;
-          }
-        }
-        words_ready = true;
+    const int j = rd * WK + kg;
+    if (wave_live) {
+      // one copy of each step: phase A fills sc before the softmax + PV,
+      // phase B after it
+      if (!phase_b && j < ntiles) {
+        sc = qk(read_k(cs));
+        mask_tile(sc, j);
+        sc_slot = cs;
       }
-      if (abs0 + R::SUB > n_kv || abs0 + R::SUB > end) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int key = abs0 + kb * 16 + l4 * 4 + e;
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) {
-              bool vis = key < end;
-              if (vis && key >= n_kv) {
-                const int a = key - n_kv;
-                // branchless pick of word a>>6 (0 or 1) for small trees
-                const uint64_t hi_sel = 0ull - static_cast<uint64_t>(a >> 6);
-                const uint64_t word = small_tree ? (mw0[qb] ^ ((mw0[qb] ^ mw1[qb]) & hi_sel))
-                                                 : mrow[qb][a >> 6];
-                vis = (word >> (a & 63)) & 1ull;
-              }
-              if (!vis) x.s[kb][qb][e] = -INFINITY;
-            }
-          }
+      __builtin_amdgcn_sched_barrier(0);
+      if (sc_slot >= 0) {
+        finish(sc, sc_slot);
+        sc_slot = -1;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (phase_b && j < ntiles) {
+        sc = qk(read_k(cs));
+        mask_tile(sc, j);
+        sc_slot = cs;
       }
     }
-    if constexpr (kPipe) {
-      if (tc >= 0) softmax_pv(tc, sc);
-      sc = x;
-      tc = t;
-    } else {
-      if (t >= 0) softmax_pv(t, x);
-    }
+    cs += WK;
+    if (cs >= R::NS) cs -= R::NS;
   }
+  if (sc_slot >= 0) finish(sc, sc_slot);  // phase B: the last sub-tile
   wait_vmcnt<0>();
   lds_barrier();  // every copy landed and every wave is done with the ring
+
 
   // ---- per-column totals of the softmax denominator
 #pragma unroll
@@ -805,8 +874,7 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
   if (pl->mfma) {
     const int mp = static_cast<int>(M < 256 ? M : 256);
     const int nblk = (mp + 15) / 16;
-    // 8 waves: WR row groups of 16*QB rows (QB <= 2) x (8/WR) key groups,
-    // each key group at least 32 keys of the 128-key tile
+    // 8 waves: WR row groups of 16*QB rows (QB <= 2) x (8/WR) key groups
     if (nblk <= 4) { pl->WR = 2; pl->QB = (nblk + 1) / 2; }
     else if (nblk <= 8) { pl->WR = 4; pl->QB = (nblk + 3) / 4; }
     else { pl->WR = 8; pl->QB = (nblk + 7) / 8; }
