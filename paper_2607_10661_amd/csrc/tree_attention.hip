@@ -351,9 +351,11 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   //      chains of its rows' nodes (parent[a] read from lane a % 64 by
   //      shuffles, all lanes active); each step moves to a lower index, so
   //      128 steps end every walk.  Larger trees read the mask pass's rows.
+  // first sub-tile reaching past the committed keys or the chunk end
+  const int t_mask0 = max(0, (min(n_kv, end) - start) / R::SUB);
   auto mask_tile = [&](Tile& x, int t) __attribute__((always_inline)) {
+    if (t < t_mask0) return;
     const int abs0 = start + t * R::SUB;
-    if (abs0 + R::SUB <= n_kv && abs0 + R::SUB <= end) return;
     int node[QB];
     uint64_t mw0[QB], mw1[QB];
 #pragma unroll
@@ -426,46 +428,48 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   };
 
   // ---- online softmax state.  Scores become p = 2^(s*c - m*c) against a
-  //      reference maximum m per query row that moves lazily: the first
-  //      sub-tile in which a row sees a key sets it (O is still zero then),
-  //      and later it moves only when a score exceeds it by more than 16 in
-  //      the exp2 domain (thr = m + 16/c), so p <= 2^16 and O, l stay far
-  //      inside the fp32 range.  In the common case no score of the wave
-  //      passes thr and the row maxima are never formed.
+  //      reference maximum m per query row that moves lazily.  The partial
+  //      row sums of p, needed anyway, serve as the test: while no lane's sum
+  //      over a sub-tile exceeds 2^16, no p does, and O, l stay far inside the
+  //      fp32 range with m unchanged.  Otherwise (the first keys a row sees,
+  //      m still at its start value, or a score well above m) the rows'
+  //      maxima are formed, m moves up to them, O and l are rescaled and the
+  //      sub-tile's p are recomputed.
   f32x4 o[QB][DT];
-  float m[QB], nmc[QB], thr[QB], lsum[QB];
+  float m[QB], nmc[QB], lsum[QB];
   const float c = p.c;
-  const float span = 16.0f / c;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     m[qb] = kNegBig;
     nmc[qb] = -kNegBig * c;
-    thr[qb] = kNegBig;
     lsum[qb] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[qb][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  auto check_scores = [&](const Tile& x) __attribute__((always_inline)) {
-    bool over = false;
+  auto exp_tile = [&](const Tile& x, float (&pv)[QB][8], float (&ps)[QB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      const float a = fmaxf(fmaxf(x.s[0][qb][0], x.s[0][qb][1]), x.s[0][qb][2]);
-      const float bb = fmaxf(fmaxf(x.s[0][qb][3], x.s[1][qb][0]), x.s[1][qb][1]);
-      const float cc = fmaxf(fmaxf(x.s[1][qb][2], x.s[1][qb][3]), a);
-      over |= fmaxf(bb, cc) > thr[qb];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pv[qb][e] = __builtin_amdgcn_exp2f(fmaf(x.s[0][qb][e], c, nmc[qb]));
+        pv[qb][4 + e] = __builtin_amdgcn_exp2f(fmaf(x.s[1][qb][e], c, nmc[qb]));
+      }
+      ps[qb] = ((pv[qb][0] + pv[qb][1]) + (pv[qb][2] + pv[qb][3])) +
+               ((pv[qb][4] + pv[qb][5]) + (pv[qb][6] + pv[qb][7]));
     }
-    if (!__any(over)) return;
-    // rare: move the reference of the rows whose maximum passed thr
+  };
+  // rare: move the reference of rows whose maximum passed it (uniform over
+  // the row's four lanes)
+  auto move_ref = [&](const Tile& x) __attribute__((always_inline)) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float mx = fmaxf(fmaxf(fmaxf(x.s[0][qb][0], x.s[0][qb][1]), fmaxf(x.s[0][qb][2], x.s[0][qb][3])),
                        fmaxf(fmaxf(x.s[1][qb][0], x.s[1][qb][1]), fmaxf(x.s[1][qb][2], x.s[1][qb][3])));
       mx = max_xor32(max_xor16(mx));
-      if (mx > thr[qb]) {  // uniform over the row's four lanes
+      if (mx > m[qb]) {
         const float alpha = __builtin_amdgcn_exp2f((m[qb] - mx) * c);  // 0 for the first keys
         m[qb] = mx;
         nmc[qb] = -mx * c;
-        thr[qb] = mx + span;
         lsum[qb] *= alpha;
         // in-place scaling of the accumulators (asm keeps the compiler from
         // duplicating them around this rarely taken path)
@@ -481,31 +485,34 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     }
   };
   // p of a tile as bf16 MFMA operands (B of O^T += V^T P^T: lane holds its
-  // query column's 8 keys); with PRECISE also the rounding residue p - bf16(p)
+  // query column's 8 keys); with `precise` also the rounding residue p - bf16(p)
   struct PFrag {
     bf16x8 hi[QB], lo[QB];
   };
   auto softmax = [&](const Tile& x, bool precise) __attribute__((always_inline)) -> PFrag {
+    float pv[QB][8], ps[QB];
+    exp_tile(x, pv, ps);
+    bool over = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) over |= !(ps[qb] <= 65536.0f);
+    if (__any(over)) {
+      move_ref(x);
+      exp_tile(x, pv, ps);
+    }
     PFrag f;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      float pv[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        pv[e] = __builtin_amdgcn_exp2f(fmaf(x.s[0][qb][e], c, nmc[qb]));
-        pv[4 + e] = __builtin_amdgcn_exp2f(fmaf(x.s[1][qb][e], c, nmc[qb]));
-      }
       u32x4 ph, pl;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[2 * w], pv[2 * w + 1]);
+      for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[qb][2 * w], pv[qb][2 * w + 1]);
       if (precise) {
 #pragma unroll
         for (int w = 0; w < 4; ++w)
-          pl[w] = ptd::cvt_pk_bf16(pv[2 * w] - ptd::bf16_lo(ph[w]),
-                                   pv[2 * w + 1] - ptd::bf16_hi(ph[w]));
+          pl[w] = ptd::cvt_pk_bf16(pv[qb][2 * w] - ptd::bf16_lo(ph[w]),
+                                   pv[qb][2 * w + 1] - ptd::bf16_hi(ph[w]));
         f.lo[qb] = __builtin_bit_cast(bf16x8, pl);
       }
-      lsum[qb] += ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
+      lsum[qb] += ps[qb];
       f.hi[qb] = __builtin_bit_cast(bf16x8, ph);
     }
     return f;
@@ -526,32 +533,51 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   };
 
   // ---- rounds.  Round rd holds sub-tiles rd*WK .. rd*WK + WK - 1 (wave kg
-  //      takes rd*WK + kg).  The two waves that share a SIMD (waves w and
-  //      w + 4) run a round in opposite orders, so that one issues MFMAs while
-  //      the other does the softmax on the vector ALUs:
-  //        phase A:  QK^T(rd) -> softmax(rd) -> PV(rd)
-  //        phase B:  softmax(rd - 1) -> PV(rd - 1) -> QK^T(rd)
-  //      (phase B carries its scores across the barrier).  A slot is read in
-  //      its own round and, by phase B, in the next one, so the slots of round
-  //      rd - 2 are refilled at the barrier of round rd; the data of round rd
-  //      is then issued by round rd - 1, which needs 3*WK ring slots.  With
-  //      more key groups every wave runs phase A and slots are refilled one
-  //      round after their use.
+  //      takes rd*WK + kg).  Software pipeline (PIPE): during round rd a wave
+  //      issues the QK^T MFMAs of its round rd + 1 sub-tile interleaved with
+  //      the softmax of its round rd sub-tile (scores kept in registers from
+  //      the round before), then the PV MFMAs of round rd.  Round rd thus
+  //      reads K of round rd + 1 and V of round rd, the data of round rd + 1
+  //      is waited for at the barrier of round rd, and the slots of round
+  //      rd - 1 are free there and refilled right away.  Round rd + 1's data
+  //      is then issued by round rd - 1, which needs 3*WK ring slots; with
+  //      more key groups a round computes its own sub-tile start to end.
   //      P is carried as bf16 when the sequence has at least kPlainKeys keys
   //      (the softmax weight is then spread over many keys and bf16 rounding
   //      of p moves the output by well under 1e-3); shorter sequences, where
   //      a few keys can hold all the weight, carry p as bf16 hi + lo.
+  constexpr bool PIPE = 3 * WK <= R::NS;
+  static_assert((2 + (PIPE ? 1 : 0)) * WK <= R::NS, "round data issued one round ahead");
   const bool precise = N < kPlainKeys;  // uniform over the workgroup
-  constexpr bool kPingPong = 3 * WK <= R::NS;
-  constexpr int LAG = kPingPong ? 2 : 1;  // rounds between a slot's use and its refill
-  static_assert((LAG + 1) * WK <= R::NS, "round data issued one round ahead");
-  const bool phase_b = kPingPong && ((wave >> 2) & 1) != 0;
-  auto finish = [&](const Tile& x, int slot) __attribute__((always_inline)) {
-    const VFrag vf = read_v(slot);
-    check_scores(x);
-    const PFrag pf = softmax(x, precise);
-    pv_acc(vf, pf, precise);
+  // bf16 p of scores x (exponentials pv and their lane sums ps computed)
+  auto to_p = [&](const Tile& x, float (&pv)[QB][8], float (&ps)[QB]) __attribute__((always_inline))
+      -> PFrag {
+    bool over = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) over |= !(ps[qb] <= 65536.0f);
+    if (__any(over)) {
+      move_ref(x);
+      exp_tile(x, pv, ps);
+    }
+    PFrag f;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      u32x4 ph, pl;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[qb][2 * w], pv[qb][2 * w + 1]);
+      if (precise) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          pl[w] = ptd::cvt_pk_bf16(pv[qb][2 * w] - ptd::bf16_lo(ph[w]),
+                                   pv[qb][2 * w + 1] - ptd::bf16_hi(ph[w]));
+        f.lo[qb] = __builtin_bit_cast(bf16x8, pl);
+      }
+      lsum[qb] += ps[qb];
+      f.hi[qb] = __builtin_bit_cast(bf16x8, ph);
+    }
+    return f;
   };
+
   for (int t = 0; t < ninit; ++t) issue(t, t);
   wait_vmcnt_le((ninit - min(ntiles, WK)) * R::DPS);  // round 0 (query rows, parents) landed
   lds_barrier();
@@ -566,50 +592,67 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   par_lo = static_cast<int>(par_raw[0]);
   par_hi = static_cast<int>(par_raw[1]);
 
-  int cs = kg;       // ring slot of this wave's sub-tile of the current round
-  int rs = 0;        // slot refilled next (round rd - LAG's slots, in order)
-  Tile sc;           // phase B: scores waiting for their softmax + PV
-  int sc_slot = -1;  // phase B: their slot, or -1
+  // rounds whose wait count is the steady-state constant: every refill so far
+  // issued in full (R::NS + (rd - 1) * WK <= ntiles)
+  const int steady_end = ntiles >= R::NS ? (ntiles - R::NS) / WK + 1 : -1;
+  int cs = kg;  // ring slot of this wave's sub-tile of the current round
+  int rs = 0;   // slot refilled next (round rd - 1's slots, in order)
+  Tile sc;      // PIPE: scores of the current round's sub-tile
+  if (PIPE && wave_live && kg < ntiles) {
+    sc = qk(read_k(cs));
+    mask_tile(sc, kg);
+  }
   for (int rd = 0; rd < nrounds; ++rd) {
-    if (rd > 0) {
-      const int issued = min(ntiles, R::NS + max(0, rd - LAG) * WK);
-      const int needed = min(ntiles, (rd + 1) * WK);
-      wait_vmcnt_le((issued - needed) * R::DPS);
+    const bool do_wait = PIPE ? rd + 1 < nrounds : rd >= 1;
+    if (do_wait) {
+      if (rd >= 1 && rd <= steady_end) {
+        wait_vmcnt<(R::NS - (2 + (PIPE ? 1 : 0)) * WK) * R::DPS>();
+      } else {
+        const int issued = min(ntiles, R::NS + max(0, rd - 1) * WK);
+        const int needed = min(ntiles, (rd + 1 + (PIPE ? 1 : 0)) * WK);
+        wait_vmcnt_le((issued - needed) * R::DPS);
+      }
       lds_barrier();
-      if (rd >= LAG) {
+      if (rd >= 1) {
 #pragma unroll
         for (int w = 0; w < WK; ++w) {
-          const int tt = R::NS + (rd - LAG) * WK + w;
+          const int tt = R::NS + (rd - 1) * WK + w;
           if (tt < ntiles) issue(tt, rs);
           rs = rs + 1 == R::NS ? 0 : rs + 1;
         }
       }
     }
+    int ns = cs + WK;
+    if (ns >= R::NS) ns -= R::NS;
     const int j = rd * WK + kg;
-    if (wave_live) {
-      // one copy of each step: phase A fills sc before the softmax + PV,
-      // phase B after it
-      if (!phase_b && j < ntiles) {
+    if (wave_live && j < ntiles) {
+      float pv[QB][8], ps[QB];
+      if constexpr (PIPE) {
+        // next K reads in flight while this sub-tile's exponentials run (they
+        // overlap the previous round's PV MFMAs, still executing); then the
+        // next QK^T and this PV back to back on the matrix cores.  After the
+        // wave's last sub-tile the next-tile QK^T works on whatever the slot
+        // holds and its result is dropped: one code path keeps the register
+        // allocation of this loop within the two-waves-per-SIMD budget.
+        const KFrag kf = read_k(ns);
+        exp_tile(sc, pv, ps);
+        const PFrag pf = to_p(sc, pv, ps);
+        Tile sn = qk(kf);
+        const VFrag vf = read_v(cs);
+        pv_acc(vf, pf, precise);
+        if (j + WK < ntiles) mask_tile(sn, j + WK);
+        sc = sn;
+      } else {
         sc = qk(read_k(cs));
         mask_tile(sc, j);
-        sc_slot = cs;
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (sc_slot >= 0) {
-        finish(sc, sc_slot);
-        sc_slot = -1;
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (phase_b && j < ntiles) {
-        sc = qk(read_k(cs));
-        mask_tile(sc, j);
-        sc_slot = cs;
+        const VFrag vf = read_v(cs);
+        exp_tile(sc, pv, ps);
+        const PFrag pf = to_p(sc, pv, ps);
+        pv_acc(vf, pf, precise);
       }
     }
-    cs += WK;
-    if (cs >= R::NS) cs -= R::NS;
+    cs = ns;
   }
-  if (sc_slot >= 0) finish(sc, sc_slot);  // phase B: the last sub-tile
   wait_vmcnt<0>();
   lds_barrier();  // every copy landed and every wave is done with the ring
 
