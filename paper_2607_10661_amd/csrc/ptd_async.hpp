@@ -14,7 +14,12 @@ namespace ptd {
 // with explicit vmcnt waits (vector-memory operations retire in issue order,
 // so a wait also covers every older load).  M0 is saved and restored inside
 // the asm, and one wait state separates the M0 write from the copy.
+__device__ __forceinline__ uint32_t uniform_u32(uint32_t x) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(x)));
+}
+
 __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds) {
+  lds = uniform_u32(lds);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -36,6 +41,7 @@ __device__ __forceinline__ void dma16_s(const void* base, uint32_t voff, uint32_
   const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)));
   const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b)));
   const uint64_t sbase = (static_cast<uint64_t>(hi) << 32) | lo;
+  lds = uniform_u32(lds);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -57,6 +63,8 @@ __device__ __forceinline__ void dma16_s2(const void* base0, uint32_t voff0, uint
                       static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b0)));
   const uint64_t s1 = (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b1 >> 32)))) << 32) |
                       static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b1)));
+  lds0 = uniform_u32(lds0);
+  lds1 = uniform_u32(lds1);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -74,6 +82,7 @@ __device__ __forceinline__ void dma16_s2(const void* base0, uint32_t voff0, uint
 
 // Same, 4 bytes per lane (lane l lands at lds + 4*l).
 __device__ __forceinline__ void dma4(const void* gptr, uint32_t lds) {
+  lds = uniform_u32(lds);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
