@@ -41,8 +41,12 @@ def _load():
     lib.oracle_topk.argtypes = [vp, i, i, i, ctypes.c_longlong, i, vp, vp, vp]
     lib.oracle_verify.argtypes = [vp, vp, vp, vp, i, i, vp, vp, vp]
     lib.oracle_expand.argtypes = [vp, vp, vp, i, i, vp, i, vp, i, i, vp, vp, vp]
+    lib.oracle_tree_rope.argtypes = [vp, vp, i, vp, vp, i, i, i, i, i, i, vp, i, vp, vp,
+                                     vp]
+    lib.oracle_kv_commit.argtypes = [vp, vp, i, vp, vp, vp, i, i, i, i, i, vp]
     for f in ("oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
-              "oracle_topk", "oracle_verify", "oracle_expand"):
+              "oracle_topk", "oracle_verify", "oracle_expand", "oracle_tree_rope",
+              "oracle_kv_commit"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -62,7 +66,8 @@ def _c(a, dt):
 
 def _check(st: int):
     if st != 0:
-        raise OracleError({2: "bad sizes", 7: "malformed tree"}.get(st, st))
+        raise OracleError({2: "bad sizes", 7: "malformed tree", 8: "kv_len out of range",
+                           9: "malformed accepted path"}.get(st, st))
 
 
 def _dtype_code(arr: np.ndarray) -> int:
@@ -172,3 +177,58 @@ def expand(parent, tokens, topk_idx, width_sched, d_max: int, T_max: int,
     _check(_load().oracle_expand(_p(parent), _p(tokens), _p(tl), B, T, _p(ti), k,
                                  _p(ws), d_max, T_max, _p(pn), _p(tn), _p(ln)))
     return pn, tn, ln
+
+
+def rope_inv_freq(D: int, theta: float) -> np.ndarray:
+    """Rotary frequencies of RoFormer (Su et al., 2021): pair p of a head of
+    D dimensions turns by theta^(-2p/D) radians per position, p < D/2."""
+    p = np.arange(D // 2, dtype=np.float64)
+    return np.power(float(theta), -2.0 * p / D)
+
+
+def tree_rope(q, k_cache, kv_len, parent, theta: float = 10000.0, inv_freq=None,
+              pairing: int = 0):
+    """Positions kv_len + |pi(i)| - 1 of the tree nodes and the rotary
+    embedding of their queries and keys (the tree rows kv_len + i of k_cache).
+    pairing 0: pair p = (p, p + D/2); 1: pair p = (2p, 2p + 1).
+    -> (q_out float64 [B][T][Hq][D], k_out float64 [B][Hkv][T][D],
+        pos int32 [B][T])."""
+    q = np.ascontiguousarray(q)
+    k_cache = np.ascontiguousarray(k_cache)
+    dt = _dtype_code(q)
+    if _dtype_code(k_cache) != dt:
+        raise TypeError("q/k dtypes differ")
+    B, T, Hq, D = q.shape
+    _, Hkv, L_cap, _ = k_cache.shape
+    f = rope_inv_freq(D, theta) if inv_freq is None else _c(inv_freq, np.float64)
+    if f.shape != (D // 2,):
+        raise ValueError("inv_freq needs D/2 entries")
+    qo = np.zeros((B, T, Hq, D), np.float64)
+    ko = np.zeros((B, Hkv, T, D), np.float64)
+    pos = np.zeros((B, T), np.int32)
+    kvl = _c(kv_len, np.int32)
+    par = _c(parent, np.int32)
+    _check(_load().oracle_tree_rope(_p(q), _p(k_cache), dt, _p(kvl), _p(par), B, T, Hq, Hkv,
+                                    D, L_cap, _p(f), int(pairing), _p(qo), _p(ko),
+                                    _p(pos)))
+    return qo, ko, pos
+
+
+def kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes):
+    """Commit of the accepted path on copies of the caches
+    ([B][Hkv][L_cap][D], bf16 bits or float32).
+    -> (k_cache_new, v_cache_new, kv_len_next int32 [B])."""
+    kc = np.array(k_cache, copy=True, order="C")
+    vc = np.array(v_cache, copy=True, order="C")
+    dt = _dtype_code(kc)
+    if _dtype_code(vc) != dt:
+        raise TypeError("k/v dtypes differ")
+    B, Hkv, L_cap, D = kc.shape
+    an = _c(accept_nodes, np.int32)
+    T = an.shape[-1]
+    an = an.reshape(B, T)
+    nxt = np.zeros(B, np.int32)
+    _check(_load().oracle_kv_commit(_p(kc), _p(vc), dt, _p(_c(kv_len, np.int32)),
+                                    _p(_c(accept_len, np.int32)), _p(an), B, T, Hkv, D,
+                                    L_cap, _p(nxt)))
+    return kc, vc, nxt

@@ -20,9 +20,15 @@
  *                          Alg. 1 step 5-6.
  *   oracle_expand          Sec. 3.1 "Progressive Expansion" (V^t, E^t) with the
  *                          width limit of "Overhead Constraints", top-k children.
+ *   oracle_tree_rope       Sec. 3.1 position |pi(v)| of a tree node, continuing
+ *                          the committed positions; rotary embedding of its
+ *                          query and key at that position (RoFormer rotation).
+ *   oracle_kv_commit       Sec. 3.2 accepted sequence X': the accepted nodes'
+ *                          keys and values become the next committed rows.
  *
  * Error returns: 0 = ok, 7 = malformed tree (parent[i] outside [-1, i)),
- * 2 = bad sizes.
+ * 2 = bad sizes, 8 = kv_len outside [0, L_cap - T], 9 = accepted path not
+ * strictly increasing node ids in [0, T) (or its length outside [0, T]).
  */
 #include <math.h>
 #include <stdint.h>
@@ -32,6 +38,8 @@
 #define ORC_OK 0
 #define ORC_BAD_SIZE 2
 #define ORC_BAD_TREE 7
+#define ORC_BAD_KV_LEN 8
+#define ORC_BAD_PATH 9
 
 /* element widening: dtype 0 = fp32, 1 = bf16 (upper half of an fp32) */
 static double load_elem(const void* base, int dtype, size_t idx) {
@@ -353,5 +361,130 @@ int oracle_expand(const int32_t* parent, const int32_t* tokens,
     tree_len_next[b] = keep;
   }
   free(gpar); free(gtok); free(gdep); free(newid); free(order);
+  return status;
+}
+
+/* ---------------------------------------------------------------------------
+ * Positions and rotary embedding of the tree rows.
+ * Sec. 3.1 "Tree Construction": the position of node v is given by |pi(v)|.
+ * A root's parent is the last committed token, at position kv_len[b] - 1, so
+ * node i of sequence b sits at
+ *     pos(i) = kv_len[b] + |pi(i)| - 1,
+ * which is where a chain of accepted nodes lands once committed.
+ * The model turns queries and keys by their positions with the rotary
+ * embedding of Su et al. (RoFormer, 2021): dimension pair p (0 <= p < D/2)
+ * is rotated by the angle a = pos * inv_freq[p],
+ *     (x_a, x_b) -> (x_a cos a - x_b sin a,  x_a sin a + x_b cos a),
+ * where pair p is (x[p], x[p + D/2]) for pairing 0 ("half" layout) or
+ * (x[2p], x[2p + 1]) for pairing 1 ("interleaved" layout).
+ * In:  q [B][T][Hq][D]; keys are rows kv_len[b] + i of k_cache
+ *      [B][Hkv][L_cap][D]; inv_freq [D/2].
+ * Out (fp64): q_out [B][T][Hq][D], k_out [B][Hkv][T][D] (the tree rows),
+ *      pos [B][T].  A sequence with a malformed tree or kv_len outside
+ *      [0, L_cap - T] is skipped (outputs zero) and reported.
+ * ------------------------------------------------------------------------- */
+static void rope_vector(const void* src, int dtype, size_t base, int D, double pos,
+                        const double* inv_freq, int pairing, double* dst) {
+  for (int p = 0; p < D / 2; ++p) {
+    const int ia = pairing == 0 ? p : 2 * p;
+    const int ib = pairing == 0 ? p + D / 2 : 2 * p + 1;
+    const double xa = load_elem(src, dtype, base + (size_t)ia);
+    const double xb = load_elem(src, dtype, base + (size_t)ib);
+    const double a = pos * inv_freq[p];
+    dst[ia] = xa * cos(a) - xb * sin(a);
+    dst[ib] = xa * sin(a) + xb * cos(a);
+  }
+}
+
+int oracle_tree_rope(const void* q, const void* k_cache, int dtype, const int32_t* kv_len,
+                     const int32_t* parent, int B, int T, int Hq, int Hkv, int D, int L_cap,
+                     const double* inv_freq, int pairing, double* q_out, double* k_out,
+                     int32_t* pos) {
+  if (B < 0 || T < 1 || Hq < 1 || Hkv < 1 || D < 2 || D % 2 != 0 || L_cap < 1 ||
+      (pairing != 0 && pairing != 1))
+    return ORC_BAD_SIZE;
+  int status = ORC_OK;
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    memset(q_out + (size_t)b * T * Hq * D, 0, sizeof(double) * (size_t)T * Hq * D);
+    memset(k_out + (size_t)b * Hkv * T * D, 0, sizeof(double) * (size_t)Hkv * T * D);
+    memset(pos + (size_t)b * T, 0, sizeof(int32_t) * (size_t)T);
+    if (!tree_is_valid(par, T)) { status = ORC_BAD_TREE; continue; }
+    if (kv_len[b] < 0 || (long long)kv_len[b] + T > L_cap) {
+      if (status == ORC_OK) status = ORC_BAD_KV_LEN;
+      continue;
+    }
+    for (int i = 0; i < T; ++i) {
+      int size = 0;                                 /* |pi(i)| */
+      for (int a = i; a != -1; a = par[a]) ++size;
+      const int p_i = kv_len[b] + size - 1;
+      pos[(size_t)b * T + i] = p_i;
+      for (int h = 0; h < Hq; ++h) {
+        const size_t off = (((size_t)b * T + i) * Hq + h) * D;
+        rope_vector(q, dtype, off, D, (double)p_i, inv_freq, pairing, q_out + off);
+      }
+      for (int g = 0; g < Hkv; ++g) {
+        const size_t src = (((size_t)b * Hkv + g) * L_cap + kv_len[b] + i) * D;
+        const size_t dst = (((size_t)b * Hkv + g) * T + i) * D;
+        rope_vector(k_cache, dtype, src, D, (double)p_i, inv_freq, pairing, k_out + dst);
+      }
+    }
+  }
+  return status;
+}
+
+/* ---------------------------------------------------------------------------
+ * Commit of the accepted path (Sec. 3.2).  The step accepts
+ * X' = (n_0, n_1, ..., n_k, V_{n_k}): n_0 is the last committed token, and
+ * n_1 .. n_k (accept_nodes[b][0 .. k-1], k = accept_len[b], shallowest
+ * first) are draft nodes whose keys and values the forward pass wrote at
+ * cache rows kv_len[b] + n_j.  They become committed tokens: node n_j
+ * (j = 1 .. k) is copied to row kv_len[b] + j - 1 in every KV head, and the
+ * committed length becomes kv_len[b] + k.  Every other row keeps its content.
+ * The bonus token V_{n_k} is the next step's input; it has no key or value yet.
+ * The k source rows are read before any destination row is written, so a
+ * destination that is also an earlier node's source is copied correctly.
+ * Caches [B][Hkv][L_cap][D] (dtype 0 fp32, 1 bf16) are updated in place.
+ * A sequence with kv_len outside [0, L_cap - T], or a path that is not
+ * strictly increasing node ids in [0, T) with 0 <= k <= T, is left unchanged
+ * (kv_len_next = kv_len) and reported.
+ * ------------------------------------------------------------------------- */
+int oracle_kv_commit(void* k_cache, void* v_cache, int dtype, const int32_t* kv_len,
+                     const int32_t* accept_len, const int32_t* accept_nodes, int B, int T,
+                     int Hkv, int D, int L_cap, int32_t* kv_len_next) {
+  if (B < 0 || T < 1 || Hkv < 1 || D < 1 || L_cap < 1) return ORC_BAD_SIZE;
+  const size_t es = dtype == 1 ? 2 : 4;
+  const size_t row = es * (size_t)D;
+  unsigned char* tmp = (unsigned char*)malloc(row * (size_t)T);
+  if (!tmp) return ORC_BAD_SIZE;
+  int status = ORC_OK;
+  for (int b = 0; b < B; ++b) {
+    const int32_t* nodes = accept_nodes + (size_t)b * T;
+    const int k = accept_len[b];
+    kv_len_next[b] = kv_len[b];
+    if (kv_len[b] < 0 || (long long)kv_len[b] + T > L_cap) {
+      if (status == ORC_OK) status = ORC_BAD_KV_LEN;
+      continue;
+    }
+    int path_ok = k >= 0 && k <= T;
+    for (int j = 0; path_ok && j < k; ++j)
+      if (nodes[j] < 0 || nodes[j] >= T || (j > 0 && nodes[j] <= nodes[j - 1])) path_ok = 0;
+    if (!path_ok) {
+      if (status == ORC_OK) status = ORC_BAD_PATH;
+      continue;
+    }
+    for (int c = 0; c < 2; ++c) {
+      unsigned char* cache = (unsigned char*)(c == 0 ? k_cache : v_cache);
+      for (int g = 0; g < Hkv; ++g) {
+        unsigned char* head = cache + ((size_t)b * Hkv + g) * (size_t)L_cap * row;
+        for (int j = 0; j < k; ++j)              /* read every source row ... */
+          memcpy(tmp + (size_t)j * row, head + (size_t)(kv_len[b] + nodes[j]) * row, row);
+        for (int j = 0; j < k; ++j)              /* ... then write the destinations */
+          memcpy(head + (size_t)(kv_len[b] + j) * row, tmp + (size_t)j * row, row);
+      }
+    }
+    kv_len_next[b] = kv_len[b] + k;
+  }
+  free(tmp);
   return status;
 }

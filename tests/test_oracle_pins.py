@@ -461,3 +461,211 @@ def test_bf16_rounding_is_rne():
     assert abs(back[4] - 3.0e-3) <= 3.0e-3 * 2 ** -8
     assert np.array_equal(W.f32_to_bf16_bits(
         torch.from_numpy(x).to(torch.bfloat16).float().numpy()), b)
+
+
+# ---------------------------------------------------------------------------
+# positions and rotary embedding of the tree rows
+# ---------------------------------------------------------------------------
+def _rope_inputs(rng, B, T, Hq, Hkv, D, L_cap):
+    q = rng.standard_normal((B, T, Hq, D)).astype(np.float32)
+    k = rng.standard_normal((B, Hkv, L_cap, D)).astype(np.float32)
+    return q, k
+
+
+def test_rope_inv_freq_closed_form():
+    # RoFormer: theta_p = base^(-2p/D)
+    assert np.array_equal(O.rope_inv_freq(4, 10000.0), [1.0, 0.01])
+    assert np.allclose(O.rope_inv_freq(8, 256.0), [1.0, 0.25, 1 / 16, 1 / 64], rtol=0, atol=1e-15)
+
+
+def test_rope_positions_closed_forms():
+    rng = np.random.default_rng(11)
+    T = 15
+    chain, _ = W.tree_chain(T)
+    star, _ = W.tree_star(T)
+    heap = np.array([-1] + [(i - 1) // 2 for i in range(1, T)], np.int32)
+    parent = np.stack([chain, star, heap])
+    kv_len = np.array([0, 7, 40], np.int32)
+    q, k = _rope_inputs(rng, 3, T, 1, 1, 4, 64)
+    _, _, pos = O.tree_rope(q, k, kv_len, parent)
+    i = np.arange(T)
+    assert (pos[0] == kv_len[0] + i).all()                            # chain: depth i + 1
+    assert (pos[1] == kv_len[1]).all()                                # star: every node a root
+    assert (pos[2] == kv_len[2] + np.floor(np.log2(i + 1))).all()     # heap: depth bit_length(i+1)
+
+
+def test_rope_position_zero_is_identity():
+    rng = np.random.default_rng(12)
+    T, D = 6, 16
+    star, _ = W.tree_star(T)
+    q, k = _rope_inputs(rng, 1, T, 3, 2, D, T)
+    for pairing in (0, 1):
+        qo, ko, pos = O.tree_rope(q, k, np.array([0], np.int32), star[None], pairing=pairing)
+        assert (pos == 0).all()
+        assert np.array_equal(qo, q.astype(np.float64))
+        assert np.array_equal(ko, k[:, :, :T].astype(np.float64))
+
+
+def test_rope_turns_e1_counterclockwise():
+    # D = 2, one pair with frequency 1: e1 at position a becomes (cos a, sin a),
+    # e2 becomes (-sin a, cos a) (the textbook plane rotation by a).
+    T = 4
+    chain, _ = W.tree_chain(T)
+    q = np.zeros((1, T, 2, 2), np.float32)
+    q[0, :, 0] = [1.0, 0.0]
+    q[0, :, 1] = [0.0, 1.0]
+    k = np.zeros((1, 1, T + 1, 2), np.float32)
+    qo, _, pos = O.tree_rope(q, k, np.array([1], np.int32), chain[None],
+                             inv_freq=np.array([1.0]))
+    for i in range(T):
+        a = float(pos[0, i])
+        assert a == 1 + i
+        assert np.allclose(qo[0, i, 0], [np.cos(a), np.sin(a)], rtol=0, atol=1e-15)
+        assert np.allclose(qo[0, i, 1], [-np.sin(a), np.cos(a)], rtol=0, atol=1e-15)
+
+
+def test_rope_preserves_pair_norms():
+    rng = np.random.default_rng(13)
+    B, T, Hq, Hkv, D, L = 2, 9, 2, 1, 32, 40
+    parent = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    q, k = _rope_inputs(rng, B, T, Hq, Hkv, D, L)
+    kv_len = np.array([3, 31], np.int32)
+    for pairing in (0, 1):
+        qo, ko, _ = O.tree_rope(q, k, kv_len, parent, theta=500000.0, pairing=pairing)
+        p = np.arange(D // 2)
+        a, b2 = (p, p + D // 2) if pairing == 0 else (2 * p, 2 * p + 1)
+        n_in = q[..., a].astype(np.float64) ** 2 + q[..., b2].astype(np.float64) ** 2
+        n_out = qo[..., a] ** 2 + qo[..., b2] ** 2
+        assert np.allclose(n_out, n_in, rtol=1e-12, atol=0)
+        kin = np.stack([k[b, :, kv_len[b]:kv_len[b] + T] for b in range(B)]).astype(np.float64)
+        assert np.allclose(ko[..., a] ** 2 + ko[..., b2] ** 2, kin[..., a] ** 2 + kin[..., b2] ** 2,
+                           rtol=1e-12, atol=0)
+
+
+def test_rope_scores_depend_on_relative_position_only():
+    # the same query and key vectors at every node of a chain: the rotated
+    # score of node i against node j is a function of i - j alone
+    rng = np.random.default_rng(14)
+    T, D, kv = 10, 16, 5
+    chain, _ = W.tree_chain(T)
+    q0 = rng.standard_normal(D).astype(np.float32)
+    k0 = rng.standard_normal(D).astype(np.float32)
+    q = np.broadcast_to(q0, (1, T, 1, D)).copy()
+    k = np.zeros((1, 1, kv + T, D), np.float32)
+    k[0, 0, kv:] = k0
+    for pairing in (0, 1):
+        qo, ko, _ = O.tree_rope(q, k, np.array([kv], np.int32), chain[None], theta=100.0,
+                                pairing=pairing)
+        s = qo[0, :, 0] @ ko[0, 0].T               # [i][j]
+        for d in range(-T + 1, T):
+            diag = np.diagonal(s, offset=-d)       # entries with i - j = d
+            assert np.allclose(diag, diag[0], rtol=0, atol=1e-12)
+        assert np.ptp([np.diagonal(s, -d)[0] for d in range(T)]) > 1e-3
+
+
+def test_rope_interleaved_is_half_on_permuted_dims():
+    rng = np.random.default_rng(15)
+    B, T, Hq, Hkv, D, L = 1, 7, 2, 2, 16, 20
+    parent = W.tree_uniform(rng, T)[0][None]
+    q, k = _rope_inputs(rng, B, T, Hq, Hkv, D, L)
+    perm = np.concatenate([np.arange(0, D, 2), np.arange(1, D, 2)])   # half slot -> x index
+    kv_len = np.array([9], np.int32)
+    qi, ki, _ = O.tree_rope(q, k, kv_len, parent, pairing=1)
+    qh, kh, _ = O.tree_rope(q[..., perm], k[..., perm], kv_len, parent, pairing=0)
+    inv = np.argsort(perm)
+    assert np.allclose(qi, qh[..., inv], rtol=0, atol=1e-14)
+    assert np.allclose(ki, kh[..., inv], rtol=0, atol=1e-14)
+
+
+def test_rope_rejects_bad_tree_and_kv_len():
+    rng = np.random.default_rng(16)
+    q, k = _rope_inputs(rng, 1, 4, 1, 1, 4, 8)
+    with pytest.raises(O.OracleError):
+        O.tree_rope(q, k, np.array([0], np.int32), np.array([[-1, 0, 2, 1]], np.int32))
+    with pytest.raises(O.OracleError):
+        O.tree_rope(q, k, np.array([5], np.int32), np.array([[-1, 0, 1, 2]], np.int32))
+
+
+# ---------------------------------------------------------------------------
+# commit of the accepted path
+# ---------------------------------------------------------------------------
+def test_kv_commit_golden():
+    g = _golden("kv_commit_example.json")
+    L = g["L_cap"]
+    r = np.arange(L, dtype=np.float32)
+    k = np.stack([10 * r, 10 * r + 1], -1)[None, None]
+    v = np.stack([-10 * r, -10 * r - 1], -1)[None, None]
+    kn, vn, nxt = O.kv_commit(k, v, np.array(g["kv_len"], np.int32),
+                              np.array(g["accept_len"], np.int32),
+                              np.array(g["accept_nodes"], np.int32))
+    assert np.array_equal(kn[0, 0], np.array(g["k_after_rows"], np.float32))
+    assert np.array_equal(vn[0, 0], np.array(g["v_after_rows"], np.float32))
+    assert nxt.tolist() == g["kv_len_next"]
+
+
+def test_kv_commit_chain_prefix_and_empty_are_identity():
+    rng = np.random.default_rng(17)
+    B, Hkv, L, D, T = 2, 3, 30, 8, 6
+    k = W.f32_to_bf16_bits(rng.standard_normal((B, Hkv, L, D)).astype(np.float32))
+    v = W.f32_to_bf16_bits(rng.standard_normal((B, Hkv, L, D)).astype(np.float32))
+    nodes = np.full((B, T), -1, np.int32)
+    nodes[0, :4] = np.arange(4)                 # the first four nodes of a chain
+    kn, vn, nxt = O.kv_commit(k, v, np.array([5, 9], np.int32), np.array([4, 0], np.int32),
+                              nodes)
+    assert np.array_equal(kn, k) and np.array_equal(vn, v)
+    assert nxt.tolist() == [9, 9]
+
+
+def test_rope_then_commit_matches_rope_at_committed_rows():
+    # Rotating the tree keys at kv_len + |pi(i)| - 1 and committing the
+    # accepted path leaves committed row kv_len + j - 1 rotated at exactly that
+    # row's position, as if the path had been decoded one token at a time.
+    rng = np.random.default_rng(18)
+    B, T, Hkv, D, L = 3, 24, 2, 8, 64
+    parent = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    kv_len = np.array([0, 11, 30], np.int32)
+    k = rng.standard_normal((B, Hkv, L, D)).astype(np.float32)
+    q = np.zeros((B, T, 1, D), np.float32)
+    _, ko, _ = O.tree_rope(q, k, kv_len, parent, theta=1000.0)
+    k_rot = k.copy()
+    for b in range(B):
+        k_rot[b, :, kv_len[b]:kv_len[b] + T] = ko[b].astype(np.float32)
+    # an accepted path: the root path of the deepest node (lowest index on ties)
+    _, depth = O.tree_mask(parent)
+    al = np.zeros(B, np.int32)
+    an = np.full((B, T), -1, np.int32)
+    for b in range(B):
+        t = int(np.argmax(depth[b]))
+        path = []
+        while t >= 0:
+            path.append(t)
+            t = int(parent[b, t])
+        path = path[::-1]
+        al[b] = len(path)
+        an[b, :len(path)] = path
+    kn, _, nxt = O.kv_commit(k_rot, k_rot, kv_len, al, an)
+    assert (nxt == kv_len + al).all()
+    for b in range(B):
+        n = int(al[b])
+        src = k[b][:, kv_len[b] + an[b, :n]]                      # un-rotated keys of the path
+        chain, _ = W.tree_chain(n)
+        kk = np.zeros((1, Hkv, kv_len[b] + n, D), np.float32)
+        kk[0, :, kv_len[b]:] = src
+        _, want, pos = O.tree_rope(np.zeros((1, n, 1, D), np.float32), kk, kv_len[b:b + 1],
+                                   chain[None], theta=1000.0)
+        assert (pos[0] == kv_len[b] + np.arange(n)).all()
+        assert np.allclose(kn[b, :, kv_len[b]:kv_len[b] + n], want[0], rtol=0, atol=1e-6)
+
+
+@pytest.mark.parametrize("al,nodes,kv", [
+    ([2], [[3, 1, -1, -1]], [0]),    # not increasing
+    ([2], [[1, 4, -1, -1]], [0]),    # node id >= T
+    ([5], [[0, 1, 2, 3]], [0]),      # longer than the tree
+    ([-1], [[0, 1, 2, 3]], [0]),     # negative length
+    ([1], [[0, 1, 2, 3]], [5]),      # kv_len + T > L_cap
+])
+def test_kv_commit_rejects_bad_paths(al, nodes, kv):
+    k = np.zeros((1, 1, 8, 2), np.float32)
+    with pytest.raises(O.OracleError):
+        O.kv_commit(k, k, np.array(kv, np.int32), np.array(al, np.int32),
+                    np.array(nodes, np.int32))
