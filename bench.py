@@ -4,7 +4,10 @@
 A step = the whole hot path over one batch of synthetic inputs, on one stream:
 ptd_tree_attention (one layer; ancestor masks derived in the kernel for trees
 of <= 128 nodes, built into the workspace otherwise) -> ptd_topk_argmax ->
-ptd_verify_expand (verification and expansion in one launch).  Inputs are seeded synthetic tensors shaped like the
+ptd_verify_expand (verification and expansion in one launch).  The positions
+with rotary embedding of the tree rows (ptd_tree_rope) and the commit of the
+accepted path (ptd_kv_commit) are timed on their own after the step, on the
+same inputs, and reported under "next_rows".  Inputs are seeded synthetic tensors shaped like the
 paper's workloads (Llama-2-7B attention shape by default), resident in HBM
 before timing starts; R input sets totalling >= 1 GiB are rotated so the
 256 MB MALL cannot serve the KV cache from one step to the next.
@@ -182,6 +185,38 @@ def main():
     att_ms, _ = timed(attention, K)
     att_avg_s = att_ms * 1e-3
 
+    # ptd_tree_rope and ptd_kv_commit on their own, after the step timings:
+    # the rope turns q and the tree key rows of the rotated sets in place, the
+    # commit moves the accepted rows (kv_len is not advanced, so every call
+    # moves the same rows).  Neither changes the bytes a later call moves.
+    acc_len = al.clone()
+    acc_nodes = an.clone()
+    kv_next = torch.empty_like(kv_len)
+    rope_shape = P.AttnShape(B, w.Hq, w.Hkv, w.D, w.L_cap, shape.in_dtype, shape.in_dtype, 0.0)
+    theta = 10000.0
+
+    def rope(i):
+        s = sets[i % R]
+        P.ptd_tree_rope(s["q"], s["k"], kv_len, parent, T, rope_shape, theta, None,
+                        P.PTD_ROPE_HALF, None, status, sp)
+
+    def commit(i):
+        s = sets[i % R]
+        P.ptd_kv_commit(s["k"], s["v"], kv_len, acc_len, acc_nodes, T, rope_shape, kv_next,
+                        status, sp)
+
+    rope_ms, _ = timed(rope, K)
+    commit_ms, _ = timed(commit, K)
+    torch.cuda.synchronize()
+    assert status.item() == 0, P.ptd_status_string(status.item())
+    rope_b = W.rope_bytes(w)
+    commit_b = W.commit_bytes(w, acc_nodes.cpu().numpy(), acc_len.cpu().numpy())
+
+    def next_row(ms, nbytes, what):
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        return {"us": round(ms * 1e3, 3), "alg_bytes": nbytes, "GBps": round(gbps, 1),
+                "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4), "what": what}
+
     alg = W.algorithmic_bytes(w)
     achieved = alg["attention"] / att_avg_s / 1e9
     flops = W.attention_flops(w)
@@ -239,6 +274,14 @@ def main():
                      "kernel": "ptd_tree_attention (k_attn_mfma + k_attn_combine)",
                      "alg_bytes_per_launch": alg["attention"]},
         "cpu_baseline": cpu,
+        "next_rows": {
+            "tree_rope": next_row(rope_ms, rope_b, "ptd_tree_rope: positions kv_len+|pi(i)|-1, "
+                                  "rotary embedding of q and the tree key rows (theta 1e4, "
+                                  "half pairing), %d back-to-back calls" % K),
+            "kv_commit": next_row(commit_ms, commit_b, "ptd_kv_commit of the accepted paths "
+                                  "(accept_len %s), %d back-to-back calls"
+                                  % (acc_len.cpu().tolist(), K)),
+        },
     }
     print(json.dumps(line), flush=True)
 

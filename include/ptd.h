@@ -12,6 +12,9 @@
  *   ptd_verify           greedy longest accepted path (+ bonus token)
  *   ptd_expand           progressive expansion with top-k children
  *   ptd_verify_expand    the two above in one launch
+ *   ptd_tree_rope        positions of the tree nodes; rotary embedding of
+ *                        their queries and keys at those positions
+ *   ptd_kv_commit        the accepted path's keys/values become committed rows
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller (stream-ordered;
@@ -57,8 +60,16 @@ typedef enum {
   PTD_ERR_WORKSPACE = 5, /* workspace missing or too small */
   PTD_ERR_HIP = 6,       /* a HIP runtime call or kernel launch failed */
   PTD_ERR_BAD_TREE = 7,  /* device-detected: parent[i] outside [-1, i) */
-  PTD_ERR_KV_LEN = 8     /* device-detected: kv_len < 0 or kv_len + T > L_cap */
+  PTD_ERR_KV_LEN = 8,    /* device-detected: kv_len < 0 or kv_len + T > L_cap */
+  PTD_ERR_BAD_PATH = 9   /* device-detected: accepted path not strictly increasing
+                            node ids in [0, T), or its length outside [0, T] */
 } ptd_status;
+
+/* Dimension pairs turned together by the rotary embedding. */
+typedef enum {
+  PTD_ROPE_HALF = 0,        /* pair p = (x[p], x[p + D/2]) */
+  PTD_ROPE_INTERLEAVED = 1  /* pair p = (x[2p], x[2p + 1]) */
+} ptd_rope_pairing;
 
 #define PTD_MAX_T 1024   /* tree nodes per sequence */
 #define PTD_MAX_K 16     /* top-k */
@@ -240,6 +251,73 @@ int ptd_verify_expand(const int32_t* argmax, const int32_t* draft_tokens,
                       int32_t* accept_len, int32_t* accept_nodes, int32_t* out_tokens,
                       int32_t* parent_next, int32_t* tokens_next,
                       int32_t* tree_len_next, int32_t* dev_status, void* stream);
+
+/*
+ * ptd_tree_rope -- positions of the tree nodes and the rotary embedding of
+ * their queries and keys.  Sec. 3.1 "Tree Construction": the position of node
+ * v is given by |pi(v)|; a root's parent is the last committed token (at
+ * position kv_len[b] - 1), so
+ *     pos[b][i] = kv_len[b] + |pi(i)| - 1.
+ * The rotary embedding (Su et al., RoFormer) turns dimension pair p,
+ * 0 <= p < D/2, by the angle a = pos * inv_freq[p]:
+ *     (x_a, x_b) -> (x_a cos a - x_b sin a, x_a sin a + x_b cos a).
+ *   q          [B][T][Hq][D] in_dtype, turned in place; NULL to skip queries
+ *   k_cache    [B][Hkv][L_cap][D] in_dtype: the tree rows kv_len[b] + i,
+ *              i < T, are turned in place (no other row is touched); NULL to
+ *              skip keys
+ *   kv_len, parent, T   as for ptd_tree_attention (all T nodes live); kv_len
+ *              needs 0 <= kv_len, and kv_len + T <= L_cap when k_cache is
+ *              given (kv_len + T <= INT32_MAX otherwise)
+ *   shape      B, Hq, Hkv, D (64 or 128), L_cap and in_dtype; out_dtype and
+ *              scale are not used
+ *   theta      base of the default frequencies inv_freq[p] = theta^(-2p/D)
+ *              (finite, > 0; ignored when inv_freq is given)
+ *   inv_freq   HOST double [D/2] or NULL: explicit frequencies (for scaled
+ *              variants of the embedding)
+ *   pairing    a ptd_rope_pairing
+ *   pos_out    int32 [B][T] or NULL: the positions
+ * Angles and their sine and cosine are computed in fp64, the rotation in
+ * fp32, and results are rounded to in_dtype (nearest even).  q and k_cache
+ * must be 16-byte aligned.  A sequence whose tree or kv_len is rejected is
+ * left untouched.
+ * dev_status: PTD_ERR_BAD_TREE, PTD_ERR_KV_LEN.
+ * Errors: PTD_ERR_NULL (shape, kv_len or parent NULL, or all of q, k_cache,
+ * pos_out NULL), PTD_ERR_SHAPE, PTD_ERR_DTYPE, PTD_ERR_ALIGN, PTD_ERR_HIP.
+ */
+int ptd_tree_rope(void* q, void* k_cache, const int32_t* kv_len, const int32_t* parent,
+                  int32_t T, const ptd_attn_shape* shape, double theta,
+                  const double* inv_freq, int32_t pairing, int32_t* pos_out,
+                  int32_t* dev_status, void* stream);
+
+/*
+ * ptd_kv_commit -- commit of the accepted path (Sec. 3.2: the accepted
+ * sequence X' = (n_0, n_1, ..., n_k, V_{n_k})).  The draft nodes n_1..n_k,
+ * whose keys and values the forward pass wrote at cache rows kv_len[b] + n_j,
+ * become committed tokens: for j = 1..k, row kv_len[b] + n_j moves to row
+ * kv_len[b] + j - 1 in every KV head of both caches, and
+ * kv_len_next[b] = kv_len[b] + k.  Other rows keep their content.  The bonus
+ * token V_{n_k} is the next step's input and has no key or value yet.  With
+ * ptd_tree_rope's positions, a node of depth j was rotated at
+ * kv_len[b] + j - 1, its committed row.
+ *   k_cache, v_cache  [B][Hkv][L_cap][D] in_dtype, updated in place, 16-byte
+ *                     aligned
+ *   kv_len            int32 [B]; needs 0 <= kv_len and kv_len + T <= L_cap
+ *   accept_len        int32 [B]: k, 0 .. T
+ *   accept_nodes      int32 [B][T]: n_1 .. n_k first (as written by
+ *                     ptd_verify), strictly increasing in [0, T); entries
+ *                     from k on are not read
+ *   T                 tree rows per sequence, 1 .. PTD_MAX_T
+ *   shape             B, Hkv, D (64 or 128), L_cap and in_dtype are used
+ *   kv_len_next       int32 [B]; must not be the kv_len buffer
+ * A sequence whose kv_len or path is rejected keeps its caches and gets
+ * kv_len_next = kv_len.
+ * dev_status: PTD_ERR_KV_LEN, PTD_ERR_BAD_PATH.
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_DTYPE, PTD_ERR_ALIGN, PTD_ERR_HIP.
+ */
+int ptd_kv_commit(void* k_cache, void* v_cache, const int32_t* kv_len,
+                  const int32_t* accept_len, const int32_t* accept_nodes, int32_t T,
+                  const ptd_attn_shape* shape, int32_t* kv_len_next, int32_t* dev_status,
+                  void* stream);
 
 #ifdef __cplusplus
 }

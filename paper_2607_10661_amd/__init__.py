@@ -9,8 +9,8 @@ device memory and the stream.  There is no CPU fallback: without a built
 ``libptd.so`` the import fails.
 
 The lower-case helpers (``tree_mask``, ``tree_attention``, ``topk_argmax``,
-``verify``, ``expand``, ``verify_expand``) allocate outputs with torch and call
-the entry points.
+``verify``, ``expand``, ``verify_expand``, ``tree_rope``, ``kv_commit``)
+allocate outputs with torch and call the entry points.
 """
 from __future__ import annotations
 
@@ -24,10 +24,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libptd.so")
 
 PTD_F32, PTD_BF16 = 0, 1
+PTD_ROPE_HALF, PTD_ROPE_INTERLEAVED = 0, 1
 PTD_MAX_T, PTD_MAX_K, PTD_MAX_DEPTH = 1024, 16, 64
 STATUS = {0: "PTD_OK", 1: "PTD_ERR_NULL", 2: "PTD_ERR_SHAPE", 3: "PTD_ERR_DTYPE",
           4: "PTD_ERR_ALIGN", 5: "PTD_ERR_WORKSPACE", 6: "PTD_ERR_HIP",
-          7: "PTD_ERR_BAD_TREE", 8: "PTD_ERR_KV_LEN"}
+          7: "PTD_ERR_BAD_TREE", 8: "PTD_ERR_KV_LEN", 9: "PTD_ERR_BAD_PATH"}
 
 
 class PTDError(RuntimeError):
@@ -66,6 +67,10 @@ _SIGS = {
                     _vp, _vp], ctypes.c_int),
     "ptd_verify_expand": ([_vp, _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _i32, _vp,
                            _vp, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
+    "ptd_tree_rope": ([_vp, _vp, _vp, _vp, _i32, ctypes.POINTER(AttnShape), ctypes.c_double,
+                       _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "ptd_kv_commit": ([_vp, _vp, _vp, _vp, _vp, _i32, ctypes.POINTER(AttnShape), _vp, _vp,
+                       _vp], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -170,6 +175,30 @@ def ptd_verify_expand(argmax, draft_tokens, parent, tree_len, B, T, topk_idx, k,
                                   _ptr(tokens_next), _ptr(tree_len_next), _ptr(dev_status),
                                   _stream(stream)),
            "ptd_verify_expand")
+
+
+def ptd_tree_rope(q, k_cache, kv_len, parent, T, shape: AttnShape, theta=10000.0,
+                  inv_freq: Optional[Sequence[float]] = None, pairing=PTD_ROPE_HALF,
+                  pos_out=None, dev_status=None, stream=None):
+    """inv_freq: host sequence of D/2 floats, or None for theta^(-2p/D)."""
+    f = None
+    if inv_freq is not None:
+        if len(inv_freq) != shape.D // 2:
+            raise ValueError("inv_freq needs D/2 entries")
+        f = (ctypes.c_double * len(inv_freq))(*[float(x) for x in inv_freq])
+    _check(_lib.ptd_tree_rope(_ptr(q), _ptr(k_cache), _ptr(kv_len), _ptr(parent), T,
+                              ctypes.byref(shape), float(theta),
+                              None if f is None else ctypes.cast(f, _vp), pairing,
+                              _ptr(pos_out), _ptr(dev_status), _stream(stream)),
+           "ptd_tree_rope")
+
+
+def ptd_kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes, T, shape: AttnShape,
+                  kv_len_next, dev_status=None, stream=None):
+    _check(_lib.ptd_kv_commit(_ptr(k_cache), _ptr(v_cache), _ptr(kv_len), _ptr(accept_len),
+                              _ptr(accept_nodes), T, ctypes.byref(shape), _ptr(kv_len_next),
+                              _ptr(dev_status), _stream(stream)),
+           "ptd_kv_commit")
 
 
 # ---------------------------------------------------------------------------
@@ -292,3 +321,34 @@ def verify_expand(argmax, draft_tokens, parent, topk_idx, width_sched: Sequence[
     ptd_verify_expand(argmax, draft_tokens, parent, tree_len, B, T, topk_idx, k, width_sched,
                       d_max, T_max, al, an, ot, pn, tn, ln, dev_status)
     return al, an, ot, pn, tn, ln
+
+
+def tree_rope(q, k_cache, kv_len, parent, theta: float = 10000.0, inv_freq=None,
+              pairing: int = PTD_ROPE_HALF, dev_status=None):
+    """Turns q [B][T][Hq][D] and the tree rows kv_len + i of k_cache
+    [B][Hkv][L_cap][D] in place (either may be None); returns the positions
+    int32 [B][T]."""
+    _need_gpu(q, k_cache, kv_len, parent)
+    B, T = parent.shape
+    ref = q if q is not None else k_cache
+    Hq, D = (q.shape[2], q.shape[3]) if q is not None else (1, k_cache.shape[3])
+    Hkv, L_cap = (k_cache.shape[1], k_cache.shape[2]) if k_cache is not None else (1, T)
+    dt = _dtype_code(ref)
+    shape = AttnShape(B, Hq, Hkv, D, L_cap, dt, dt, 0.0)
+    pos = torch.empty((B, T), dtype=torch.int32, device=parent.device)
+    ptd_tree_rope(q, k_cache, kv_len, parent, T, shape, theta, inv_freq, pairing, pos,
+                  dev_status)
+    return pos
+
+
+def kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes, dev_status=None):
+    """Moves the accepted nodes' rows in place; returns kv_len_next int32 [B]."""
+    _need_gpu(k_cache, v_cache, kv_len, accept_len, accept_nodes)
+    B, Hkv, L_cap, D = k_cache.shape
+    T = accept_nodes.shape[-1]
+    dt = _dtype_code(k_cache)
+    shape = AttnShape(B, Hkv, Hkv, D, L_cap, dt, dt, 0.0)
+    nxt = torch.empty(B, dtype=torch.int32, device=k_cache.device)
+    ptd_kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes, T, shape, nxt,
+                  dev_status)
+    return nxt

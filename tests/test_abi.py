@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(0, 9):
+    for code in range(0, 10):
         assert P.ptd_status_string(code) != "unknown status"
     assert P.ptd_status_string(99) == "unknown status"
     assert P.ptd_version() >= 100
@@ -104,3 +104,31 @@ def test_topk_verify_expand_mask_validation():
                 FAKE) == 2
     assert _err(P.ptd_build_tree_mask, FAKE, None, 0, 4, FAKE, FAKE) == 2
     assert _err(P.ptd_build_tree_mask, None, None, 1, 4, FAKE, FAKE) == 1
+
+
+def test_rope_commit_validation():
+    s = _shape(Hq=32, Hkv=8, L=4096)
+    R = P.ptd_tree_rope
+    assert _err(R, None, None, FAKE, FAKE, 64, s) == 1                 # nothing to turn or write
+    assert _err(R, FAKE, FAKE, None, FAKE, 64, s) == 1
+    assert _err(R, FAKE, FAKE, FAKE, FAKE, 0, s) == 2
+    assert _err(R, FAKE, FAKE, FAKE, FAKE, 64, _shape(L=32)) == 2      # L_cap < T
+    assert _err(R, FAKE, FAKE, FAKE, FAKE, 64, _shape(D=96)) == 2
+    assert _err(R, FAKE, FAKE, FAKE, FAKE, 64, s, pairing=2) == 2
+    assert _err(R, FAKE, FAKE, FAKE, FAKE, 64, s, theta=0.0) == 2
+    assert _err(R, FAKE, FAKE, FAKE, FAKE, 64, s, theta=float("inf")) == 2
+    bad = _shape()
+    bad.in_dtype = 7
+    assert _err(R, FAKE, FAKE, FAKE, FAKE, 64, bad) == 3
+    assert _err(R, FAKE + 8, FAKE, FAKE, FAKE, 64, s) == 4
+    assert _err(R, FAKE, FAKE + 4, FAKE, FAKE, 64, s) == 4
+    with pytest.raises(ValueError):
+        R(FAKE, FAKE, FAKE, FAKE, 64, s, inv_freq=[1.0] * 3, stream=0)
+    C = P.ptd_kv_commit
+    assert _err(C, FAKE, None, FAKE, FAKE, FAKE, 64, s, FAKE) == 1
+    assert _err(C, FAKE, FAKE, FAKE, FAKE, FAKE, 64, s, None) == 1
+    assert _err(C, FAKE, FAKE, FAKE, FAKE, FAKE, 64, s, FAKE) == 2    # kv_len_next aliases kv_len
+    assert _err(C, FAKE, FAKE, FAKE, FAKE, FAKE, 0, s, FAKE * 2) == 2
+    assert _err(C, FAKE, FAKE, FAKE, FAKE, FAKE, P.PTD_MAX_T + 1, _shape(L=8192), FAKE * 2) == 2
+    assert _err(C, FAKE, FAKE, FAKE, FAKE, FAKE, 64, bad, FAKE * 2) == 3
+    assert _err(C, FAKE, FAKE + 2, FAKE, FAKE, FAKE, 64, s, FAKE * 2) == 4

@@ -342,6 +342,22 @@ def algorithmic_bytes(w: Workload) -> Dict[str, int]:
                 attention=attn, logits=logits, step=attn + logits)
 
 
+def rope_bytes(w: Workload) -> int:
+    """Bytes the rotary embedding of the tree rows moves: every query head
+    and tree key row of every node read and written once."""
+    es = 2 if w.dtype == "bf16" else 4
+    return 2 * w.B * w.T * (w.Hq + w.Hkv) * w.D * es
+
+
+def commit_bytes(w: Workload, accept_nodes: np.ndarray, accept_len: np.ndarray) -> int:
+    """Bytes the commit of the accepted paths moves: each K and V row that
+    changes place (node n_j != j - 1) read and written once, in every KV head."""
+    es = 2 if w.dtype == "bf16" else 4
+    moved = sum(int((np.asarray(accept_nodes[b][:int(accept_len[b])]) !=
+                     np.arange(int(accept_len[b]))).sum()) for b in range(w.B))
+    return 2 * 2 * moved * w.Hkv * w.D * es
+
+
 def attention_flops(w: Workload) -> int:
     """4 * T * Hq * (kv_len + T) * D per sequence (QK^T and PV over every key
     position a node could see, counted densely over the tree block)."""
