@@ -44,7 +44,9 @@ def _load():
     lib.oracle_tree_rope.argtypes = [vp, vp, i, vp, vp, i, i, i, i, i, i, vp, i, vp, vp,
                                      vp]
     lib.oracle_kv_commit.argtypes = [vp, vp, i, vp, vp, vp, i, i, i, i, i, vp]
-    for f in ("oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
+    lib.oracle_verify_sample.argtypes = [vp, i, ctypes.c_longlong, i, vp, vp, vp, i, i, d,
+                                         vp, vp, vp, vp, vp, vp]
+    for f in ("oracle_verify_sample", "oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
               "oracle_topk", "oracle_verify", "oracle_expand", "oracle_tree_rope",
               "oracle_kv_commit"):
         getattr(lib, f).restype = ctypes.c_int
@@ -232,3 +234,27 @@ def kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes):
                                     _p(_c(accept_len, np.int32)), _p(an), B, T, Hkv, D,
                                     L_cap, _p(nxt)))
     return kc, vc, nxt
+
+
+def verify_sample(logits, tokens, parent, temperature: float, u_node, u_bonus, tree_len=None):
+    """Sampling verification.  logits [B][T+1][V] (or [B*(T+1)][V]), uniforms
+    u_node [B][T] (the draw made when node n is examined) and u_bonus [B][T+1]
+    (the draw for the bonus token at each row).
+    -> (accept_len [B], accept_nodes [B][T], out_tokens [B][T+1], margin [B])."""
+    tokens = _c(tokens, np.int32)
+    parent = _c(parent, np.int32)
+    B, T = parent.shape
+    lg = np.ascontiguousarray(logits)
+    V = lg.shape[-1]
+    lg = lg.reshape(B * (T + 1), V)
+    un = _c(u_node, np.float64).reshape(B, T)
+    ub = _c(u_bonus, np.float64).reshape(B, T + 1)
+    al = np.zeros(B, np.int32)
+    an = np.zeros((B, T), np.int32)
+    ot = np.zeros((B, T + 1), np.int32)
+    mg = np.zeros(B, np.float64)
+    tl = None if tree_len is None else _c(tree_len, np.int32)
+    _check(_load().oracle_verify_sample(_p(lg), _dtype_code(lg), V, V, _p(tokens), _p(parent),
+                                        _p(tl), B, T, float(temperature), _p(un), _p(ub),
+                                        _p(al), _p(an), _p(ot), _p(mg)))
+    return al, an, ot, mg

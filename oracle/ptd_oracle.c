@@ -25,6 +25,9 @@
  *                          query and key at that position (RoFormer rotation).
  *   oracle_kv_commit       Sec. 3.2 accepted sequence X': the accepted nodes'
  *                          keys and values become the next committed rows.
+ *   oracle_verify_sample   Sec. 3.2 sampling decoding strategy; App. B
+ *                          recursive candidate-tree sampling, normalized as in
+ *                          the proof of App. C.
  *
  * Error returns: 0 = ok, 7 = malformed tree (parent[i] outside [-1, i)),
  * 2 = bad sizes, 8 = kv_len outside [0, L_cap - T], 9 = accepted path not
@@ -486,5 +489,107 @@ int oracle_kv_commit(void* k_cache, void* v_cache, int dtype, const int32_t* kv_
     kv_len_next[b] = kv_len[b] + k;
   }
   free(tmp);
+  return status;
+}
+
+/* ---------------------------------------------------------------------------
+ * Sampling verification (Sec. 3.2 "sampling decoding strategy"; App. B,
+ * recursive candidate-tree sampling; App. C, distributional consistency).
+ * P_v = softmax(logits row of v / temperature) over the vocabulary; row 0 is
+ * the last committed token n_0 (the parent of every root), row v + 1 is
+ * node v.  Starting at n_0, the children of the current node v are examined
+ * in index order.  Child n (token t_n) is accepted iff
+ *     u_node[n] < P_v[t_n] / S,
+ * where S is the mass of P_v not yet rejected at v (S = 1 before the first
+ * child; App. C divides by it).  A rejected child's token gets probability 0
+ * (S drops by its old value), so a later sibling with the same token is never
+ * accepted.  On acceptance the walk moves to n; when every child of v is
+ * rejected, v is the terminal and the bonus token is drawn from the residual
+ * distribution (P_v with the rejected tokens removed) by inverse CDF in index
+ * order: the smallest x with  sum_{y <= x} P'_y > u_bonus[row of v] * W,
+ * W = sum_y P'_y (the last token with P'_y > 0 if rounding leaves none; -1 if
+ * W = 0).  Outputs as oracle_verify.  margin[b] (nullable) is the smallest
+ * distance, over the sequence's decisions, between a uniform and the value
+ * it was compared with (normalized units); a result whose margin is below
+ * the rounding of another implementation may legitimately differ.
+ * u_node [B][T], u_bonus [B][T+1], logits rows [B*(T+1)] of stride ld.
+ * ------------------------------------------------------------------------- */
+int oracle_verify_sample(const void* logits, int dtype, long long ld, int V,
+                         const int32_t* tokens, const int32_t* parent, const int32_t* tree_len,
+                         int B, int T, double temperature, const double* u_node,
+                         const double* u_bonus, int32_t* accept_len, int32_t* accept_nodes,
+                         int32_t* out_tokens, double* margin) {
+  if (B < 0 || T < 1 || V < 1 || ld < V || !(temperature > 0.0)) return ORC_BAD_SIZE;
+  const size_t es = dtype == 1 ? 2 : 4;
+  int status = ORC_OK;
+  double* prob = (double*)malloc(sizeof(double) * (size_t)V);   /* P_v, rejected tokens zeroed */
+  if (!prob) return ORC_BAD_SIZE;
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int32_t* tok = tokens + (size_t)b * T;
+    int32_t* an = accept_nodes + (size_t)b * T;
+    int32_t* ot = out_tokens + (size_t)b * (T + 1);
+    double mg = INFINITY;
+    for (int i = 0; i < T; ++i) an[i] = -1;
+    for (int i = 0; i <= T; ++i) ot[i] = -1;
+    accept_len[b] = 0;
+    if (margin) margin[b] = INFINITY;
+    const int n = node_count(tree_len, b, T);
+    if (!tree_is_valid(par, n)) { status = ORC_BAD_TREE; continue; }
+
+    int v = -1, depth = 0;                   /* current node (-1: n_0) */
+    for (;;) {
+      const char* row = (const char*)logits + ((size_t)b * (T + 1) + (size_t)(v + 1)) * (size_t)ld * es;
+      /* P_v = softmax(row / temperature), then the children in index order */
+      double m = -INFINITY, z = 0.0;
+      for (int y = 0; y < V; ++y) { const double l = load_elem(row, dtype, (size_t)y); if (l > m) m = l; }
+      for (int y = 0; y < V; ++y) z += exp((load_elem(row, dtype, (size_t)y) - m) / temperature);
+      for (int y = 0; y < V; ++y) prob[y] = exp((load_elem(row, dtype, (size_t)y) - m) / temperature) / z;
+      double S = 1.0;
+      int next = -1;
+      for (int c = v + 1; c < n; ++c) {
+        if (par[c] != v) continue;
+        const int t = tok[c];
+        const double p = (t >= 0 && t < V) ? prob[t] : 0.0;
+        const double thr = S > 0.0 ? p / S : 0.0;
+        const double d = fabs(u_node[(size_t)b * T + c] - thr);
+        if (d < mg) mg = d;
+        if (u_node[(size_t)b * T + c] < thr) { next = c; break; }
+        S -= p;
+        if (t >= 0 && t < V) prob[t] = 0.0;
+      }
+      if (next >= 0) {
+        an[depth] = next;
+        ot[depth] = tok[next];
+        ++depth;
+        v = next;
+        continue;
+      }
+      /* terminal: inverse CDF of the residual distribution */
+      double W = 0.0;
+      for (int y = 0; y < V; ++y) W += prob[y];
+      int x = -1;
+      if (W > 0.0) {
+        const double target = u_bonus[(size_t)b * (T + 1) + (size_t)(v + 1)] * W;
+        double cum = 0.0;
+        for (int y = 0; y < V; ++y) {
+          if (prob[y] <= 0.0) continue;
+          const double before = cum;
+          cum += prob[y];
+          x = y;
+          if (cum > target) {
+            const double d = fmin(target - before, cum - target) / W;
+            if (d < mg) mg = d;
+            break;
+          }
+        }
+      }
+      ot[depth] = x;
+      accept_len[b] = depth;
+      break;
+    }
+    if (margin) margin[b] = mg;
+  }
+  free(prob);
   return status;
 }

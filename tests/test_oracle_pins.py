@@ -669,3 +669,151 @@ def test_kv_commit_rejects_bad_paths(al, nodes, kv):
     with pytest.raises(O.OracleError):
         O.kv_commit(k, k, np.array(kv, np.int32), np.array(al, np.int32),
                     np.array(nodes, np.int32))
+
+
+# ---------------------------------------------------------------------------
+# sampling verification (App. B / App. C)
+# ---------------------------------------------------------------------------
+def _chi2_ok(counts, probs, n):
+    """Pearson chi-square of observed counts against n * probs; accepts at a
+    p-value above 1e-6 (fixed seeds: the outcome is deterministic)."""
+    from scipy.stats import chi2
+    exp_ = n * np.asarray(probs, np.float64)
+    keep = exp_ > 0
+    assert (np.asarray(counts)[~keep] == 0).all()
+    stat = float((((np.asarray(counts) - exp_) ** 2)[keep] / exp_[keep]).sum())
+    return chi2.sf(stat, keep.sum() - 1) > 1e-6
+
+
+def _replicate(parent, tokens, rows, n):
+    B = n
+    T = len(parent)
+    par = np.broadcast_to(np.asarray(parent, np.int32), (B, T)).copy()
+    tok = np.broadcast_to(np.asarray(tokens, np.int32), (B, T)).copy()
+    lg = np.broadcast_to(np.asarray(rows, np.float32), (B, T + 1, len(rows[0]))).copy()
+    return par, tok, lg
+
+
+def test_sample_first_token_follows_the_model_distribution():
+    # App. C: every candidate is selected with its own probability, and the
+    # fallback draw covers the rest, so the first emitted token ~ P_root.
+    # Logits are logs of chosen probabilities (temperature 1).
+    P0 = np.array([0.30, 0.25, 0.20, 0.10, 0.10, 0.05])
+    n = 200_000
+    rng = np.random.default_rng(21)
+    rows = [np.log(P0)] + [np.log(np.full(6, 1 / 6))] * 3
+    # three root children with tokens 1, 4, 2 (one likely, one unlikely, one middling)
+    par, tok, lg = _replicate([-1, -1, -1], [1, 4, 2], rows, n)
+    al, an, ot, _ = O.verify_sample(lg, tok, par, 1.0, rng.random((n, 3)), rng.random((n, 4)))
+    first = ot[:, 0]
+    assert (first >= 0).all()
+    assert _chi2_ok(np.bincount(first, minlength=6), P0, n)
+    # which child was accepted: child i with probability P0[token_i]
+    acc = np.where(al > 0, an[:, 0], 3)
+    assert _chi2_ok(np.bincount(acc, minlength=4), [P0[1], P0[4], P0[2], 1 - P0[[1, 4, 2]].sum()], n)
+
+
+def test_sample_second_token_follows_the_childs_distribution():
+    # after accepting root child A (token 0), the next emitted token ~ P_A
+    P0 = np.array([0.4, 0.3, 0.2, 0.1])
+    PA = np.array([0.1, 0.2, 0.3, 0.4])
+    n = 200_000
+    rng = np.random.default_rng(22)
+    uniform = np.log(np.full(4, 0.25))
+    # nodes: 0 = A (token 0, root child), 1 = B (token 1, root child),
+    #        2 = C (token 2, child of A), 3 = D (token 3, child of A)
+    rows = [np.log(P0), np.log(PA), uniform, uniform, uniform]
+    par, tok, lg = _replicate([-1, -1, 0, 0], [0, 1, 2, 3], rows, n)
+    al, an, ot, _ = O.verify_sample(lg, tok, par, 1.0, rng.random((n, 4)), rng.random((n, 5)))
+    via_a = (al >= 1) & (an[:, 0] == 0)
+    m = int(via_a.sum())
+    assert abs(m / n - P0[0]) < 5 * np.sqrt(P0[0] * (1 - P0[0]) / n)
+    assert _chi2_ok(np.bincount(ot[via_a, 1], minlength=4), PA, m)
+
+
+def test_sample_duplicate_sibling_never_accepted():
+    P0 = np.array([0.5, 0.3, 0.2])
+    n = 50_000
+    rng = np.random.default_rng(23)
+    rows = [np.log(P0)] + [np.log(np.full(3, 1 / 3))] * 2
+    par, tok, lg = _replicate([-1, -1], [1, 1], rows, n)
+    al, an, ot, _ = O.verify_sample(lg, tok, par, 1.0, rng.random((n, 2)), rng.random((n, 3)))
+    assert not ((al > 0) & (an[:, 0] == 1)).any()
+    assert _chi2_ok(np.bincount(ot[:, 0], minlength=3), P0, n)
+
+
+def test_sample_temperature_scales_logits():
+    # softmax(l / t) with l = t * log(P): the model distribution is P again
+    P0 = np.array([0.5, 0.25, 0.125, 0.125])
+    n = 100_000
+    rng = np.random.default_rng(24)
+    t = 0.37
+    rows = [t * np.log(P0), t * np.log(np.full(4, 0.25))]
+    par, tok, lg = _replicate([-1], [2], rows, n)
+    al, an, ot, _ = O.verify_sample(lg, tok, par, t, rng.random((n, 1)), rng.random((n, 2)))
+    assert _chi2_ok(np.bincount(ot[:, 0], minlength=4), P0, n)
+
+
+def test_sample_low_temperature_is_greedy():
+    # as the temperature goes to 0 the model distribution becomes the argmax:
+    # sampling verification reduces to greedy verification (pinned above)
+    rng = np.random.default_rng(25)
+    B, T, V = 8, 30, 50
+    par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    # distinct integer logits: gaps >= 1, so at temperature 1e-3 every
+    # probability but the argmax's is below exp(-1000)
+    lg = np.stack([rng.permutation(V) for _ in range(B * (T + 1))]).astype(np.float32)
+    lg = lg.reshape(B, T + 1, V)
+    am, _, _ = O.topk(lg.reshape(-1, V), 1)
+    am = am.reshape(B, T + 1)
+    # tokens: half the children follow the argmax of their parent's row
+    tok = rng.integers(0, V, (B, T)).astype(np.int32)
+    for b in range(B):
+        for i in range(T):
+            if rng.random() < 0.6:
+                tok[b, i] = am[b, par[b, i] + 1]
+    g_al, g_an, g_ot = O.verify(am, tok, par)
+    u1 = rng.uniform(0.01, 0.99, (B, T))
+    u2 = rng.uniform(0.01, 0.99, (B, T + 1))
+    al, an, ot, _ = O.verify_sample(lg, tok, par, 1e-3, u1, u2)
+    # greedy takes the deepest accepted path; the sampling walk stops at the
+    # first accepted child, which is the only child carrying the argmax token
+    # unless siblings repeat it (then the earliest one is taken).
+    for b in range(B):
+        k = int(al[b])
+        path = an[b, :k]
+        # every step of the sampled path is an argmax match
+        prev = -1
+        for c in path:
+            assert par[b, c] == prev and tok[b, c] == am[b, prev + 1]
+            prev = c
+        # the walk stopped where no child carries the argmax
+        kids = [c for c in range(T) if par[b, c] == prev]
+        assert all(tok[b, c] != am[b, prev + 1] for c in kids)
+        assert ot[b, k] == am[b, prev + 1]
+        assert k <= g_al[b]
+    # with distinct tokens among siblings the two agree exactly
+    par2 = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    tok2 = np.stack([W.sibling_distinct_tokens(rng, par2[b], V) for b in range(B)])
+    for b in range(B):
+        for i in range(T):
+            if rng.random() < 0.7:
+                p = par2[b, i]
+                sib = [c for c in range(T) if par2[b, c] == p]
+                if all(tok2[b, c] != am[b, p + 1] for c in sib):
+                    tok2[b, i] = am[b, p + 1]
+    g_al, g_an, g_ot = O.verify(am, tok2, par2)
+    al, an, ot, _ = O.verify_sample(lg, tok2, par2, 1e-3, u1, u2)
+    assert np.array_equal(al, g_al) and np.array_equal(an, g_an) and np.array_equal(ot, g_ot)
+
+
+def test_sample_empty_tree_draws_from_the_root_row():
+    P0 = np.array([0.2, 0.2, 0.6])
+    n = 60_000
+    rng = np.random.default_rng(26)
+    rows = [np.log(P0), np.log(P0)]
+    par, tok, lg = _replicate([-1], [0], rows, n)
+    al, an, ot, _ = O.verify_sample(lg, tok, par, 1.0, rng.random((n, 1)), rng.random((n, 2)),
+                                    tree_len=np.zeros(n, np.int32))
+    assert (al == 0).all() and (an == -1).all()
+    assert _chi2_ok(np.bincount(ot[:, 0], minlength=3), P0, n)
