@@ -5,9 +5,10 @@ A step = the whole hot path over one batch of synthetic inputs, on one stream:
 ptd_tree_attention (one layer; ancestor masks derived in the kernel for trees
 of <= 128 nodes, built into the workspace otherwise) -> ptd_topk_argmax ->
 ptd_verify_expand (verification and expansion in one launch).  The positions
-with rotary embedding of the tree rows (ptd_tree_rope) and the commit of the
-accepted path (ptd_kv_commit) are timed on their own after the step, on the
-same inputs, and reported under "next_rows".  Inputs are seeded synthetic tensors shaped like the
+with rotary embedding of the tree rows (ptd_tree_rope), the commit of the
+accepted path (ptd_kv_commit) and sampling verification (ptd_verify_sample)
+are timed on their own after the step, on the same inputs, and reported under
+"next_rows".  Inputs are seeded synthetic tensors shaped like the
 paper's workloads (Llama-2-7B attention shape by default), resident in HBM
 before timing starts; R input sets totalling >= 1 GiB are rotated so the
 256 MB MALL cannot serve the KV cache from one step to the next.
@@ -205,6 +206,23 @@ def main():
         P.ptd_kv_commit(s["k"], s["v"], kv_len, acc_len, acc_nodes, T, rope_shape, kv_next,
                         status, sp)
 
+    # sampling verification of the same trees and logits, uniforms drawn once
+    g = torch.Generator(device="cpu").manual_seed(1234)
+    u_node = torch.rand((B, T), generator=g, dtype=torch.float64).to(dev)
+    u_bonus = torch.rand((B, T + 1), generator=g, dtype=torch.float64).to(dev)
+    ws_samp = torch.empty(max(1, P.ptd_verify_sample_workspace_bytes(B, T, w.V)), dtype=torch.uint8,
+                          device=dev)
+    s_al = torch.empty(B, dtype=torch.int32, device=dev)
+    s_an = torch.empty((B, T), dtype=torch.int32, device=dev)
+    s_ot = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+
+    def sample(i):
+        s = sets[i % R]
+        P.ptd_verify_sample(s["logits"], dt_code, w.V, w.V, tokens, parent, None, B, T, 1.0,
+                            u_node, u_bonus, s_al, s_an, s_ot, ws_samp, ws_samp.numel(), status,
+                            sp)
+
+    sample_ms, _ = timed(sample, K)
     rope_ms, _ = timed(rope, K)
     commit_ms, _ = timed(commit, K)
     torch.cuda.synchronize()
@@ -281,6 +299,10 @@ def main():
             "kv_commit": next_row(commit_ms, commit_b, "ptd_kv_commit of the accepted paths "
                                   "(accept_len %s), %d back-to-back calls"
                                   % (acc_len.cpu().tolist(), K)),
+            "verify_sample": next_row(sample_ms, W.sample_bytes(w), "ptd_verify_sample at "
+                                      "temperature 1 (row statistics of all %d logits rows + "
+                                      "walk + bonus draw), %d back-to-back calls"
+                                      % (B * (T + 1), K)),
         },
     }
     print(json.dumps(line), flush=True)

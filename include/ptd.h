@@ -15,6 +15,8 @@
  *   ptd_tree_rope        positions of the tree nodes; rotary embedding of
  *                        their queries and keys at those positions
  *   ptd_kv_commit        the accepted path's keys/values become committed rows
+ *   ptd_verify_sample    sampling verification (recursive candidate-tree
+ *                        sampling) with caller-drawn uniforms
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller (stream-ordered;
@@ -318,6 +320,54 @@ int ptd_kv_commit(void* k_cache, void* v_cache, const int32_t* kv_len,
                   const int32_t* accept_len, const int32_t* accept_nodes, int32_t T,
                   const ptd_attn_shape* shape, int32_t* kv_len_next, int32_t* dev_status,
                   void* stream);
+
+/* Workspace bytes ptd_verify_sample needs: a (maximum, normalizer) pair of
+ * doubles per block of 2048 vocabulary entries per logits row, 256-byte
+ * rounded (0 on invalid arguments).  The workspace needs no initialisation;
+ * calls sharing one must not overlap. */
+size_t ptd_verify_sample_workspace_bytes(int32_t B, int32_t T, int32_t V);
+
+/*
+ * ptd_verify_sample -- sampling verification of the tree (Sec. 3.2 "sampling
+ * decoding strategy"; App. B recursive candidate-tree sampling; App. C proof
+ * of distributional consistency).  P_v = softmax(row of v / temperature),
+ * row 0 being the last committed token n_0 and row v+1 node v.  From n_0 the
+ * children of the current node v are examined in index order; child n with
+ * token t is accepted iff u_node[b][n] < P_v[t] / S, S = mass of P_v not yet
+ * rejected at v (1 before the first child).  A rejected token's probability
+ * becomes 0 (S drops by it), so a later sibling with the same token is
+ * rejected.  The walk moves to an accepted child; when all children of v are
+ * rejected, v is the terminal and the bonus token is the smallest x with
+ * sum_{y<=x} P'_y > u_bonus[b][row of v] * W, P' being P_v with the rejected
+ * tokens removed and W its total (the last token with P'_y > 0 if rounding
+ * leaves none; -1 if W = 0).
+ *   logits        [B*(T+1)][ld] of dtype, finite; V entries per row
+ *   V             1 .. 262144;  ld >= V (elements)
+ *   draft_tokens, parent  int32 [B][T];  tree_len int32 [B] or NULL
+ *   temperature   finite, > 0
+ *   u_node        double [B][T]   the draw made when node n is examined
+ *   u_bonus       double [B][T+1] the draw for the bonus token at each row
+ *                 (uniforms in [0, 1), drawn by the caller)
+ *   accept_len, accept_nodes, out_tokens  as for ptd_verify
+ *   workspace     >= ptd_verify_sample_workspace_bytes(B, T, V), 16-byte aligned
+ *   B*(T+1)       at most 65535 rows
+ * Precision: the normalizer is a fp64 sum of fp32 exponentials taken per
+ * block of 2048 entries relative to the block maximum and rescaled to the
+ * row maximum (each factor ~1.2e-7 relative, argument rounding compensated);
+ * the examined children's numerators are fp64; the bonus CDF sums the same
+ * terms in fp64.  A uniform within ~5e-7 of the probability or cumulative
+ * probability it is compared with may decide differently from an exact
+ * computation.
+ * dev_status: PTD_ERR_BAD_TREE.
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_DTYPE, PTD_ERR_WORKSPACE,
+ * PTD_ERR_ALIGN, PTD_ERR_HIP.
+ */
+int ptd_verify_sample(const void* logits, ptd_dtype dtype, int32_t V, int64_t ld,
+                      const int32_t* draft_tokens, const int32_t* parent,
+                      const int32_t* tree_len, int32_t B, int32_t T, double temperature,
+                      const double* u_node, const double* u_bonus, int32_t* accept_len,
+                      int32_t* accept_nodes, int32_t* out_tokens, void* workspace,
+                      size_t workspace_bytes, int32_t* dev_status, void* stream);
 
 #ifdef __cplusplus
 }

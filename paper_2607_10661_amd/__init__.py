@@ -9,8 +9,8 @@ device memory and the stream.  There is no CPU fallback: without a built
 ``libptd.so`` the import fails.
 
 The lower-case helpers (``tree_mask``, ``tree_attention``, ``topk_argmax``,
-``verify``, ``expand``, ``verify_expand``, ``tree_rope``, ``kv_commit``)
-allocate outputs with torch and call the entry points.
+``verify``, ``expand``, ``verify_expand``, ``tree_rope``, ``kv_commit``,
+``verify_sample``) allocate outputs with torch and call the entry points.
 """
 from __future__ import annotations
 
@@ -71,6 +71,10 @@ _SIGS = {
                        _vp, _i32, _vp, _vp, _vp], ctypes.c_int),
     "ptd_kv_commit": ([_vp, _vp, _vp, _vp, _vp, _i32, ctypes.POINTER(AttnShape), _vp, _vp,
                        _vp], ctypes.c_int),
+    "ptd_verify_sample_workspace_bytes": ([_i32, _i32, _i32], _sz),
+    "ptd_verify_sample": ([_vp, ctypes.c_int, _i32, _i64, _vp, _vp, _vp, _i32, _i32,
+                           ctypes.c_double, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp],
+                          ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -199,6 +203,21 @@ def ptd_kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes, T, shape: 
                               _ptr(accept_nodes), T, ctypes.byref(shape), _ptr(kv_len_next),
                               _ptr(dev_status), _stream(stream)),
            "ptd_kv_commit")
+
+
+def ptd_verify_sample_workspace_bytes(B: int, T: int, V: int) -> int:
+    return _lib.ptd_verify_sample_workspace_bytes(B, T, V)
+
+
+def ptd_verify_sample(logits, dtype, V, ld, draft_tokens, parent, tree_len, B, T, temperature,
+                      u_node, u_bonus, accept_len, accept_nodes, out_tokens, workspace=None,
+                      workspace_bytes=0, dev_status=None, stream=None):
+    _check(_lib.ptd_verify_sample(_ptr(logits), dtype, V, ld, _ptr(draft_tokens), _ptr(parent),
+                                  _ptr(tree_len), B, T, float(temperature), _ptr(u_node),
+                                  _ptr(u_bonus), _ptr(accept_len), _ptr(accept_nodes),
+                                  _ptr(out_tokens), _ptr(workspace), workspace_bytes,
+                                  _ptr(dev_status), _stream(stream)),
+           "ptd_verify_sample")
 
 
 # ---------------------------------------------------------------------------
@@ -352,3 +371,31 @@ def kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes, dev_status=Non
     ptd_kv_commit(k_cache, v_cache, kv_len, accept_len, accept_nodes, T, shape, nxt,
                   dev_status)
     return nxt
+
+
+def verify_sample(logits, draft_tokens, parent, temperature: float, u_node, u_bonus,
+                  tree_len=None, workspace=None, dev_status=None):
+    """logits [B][T+1][V] or [B*(T+1)][V] (unit stride along V); uniforms
+    u_node float64 [B][T], u_bonus float64 [B][T+1].
+    Returns (accept_len, accept_nodes, out_tokens)."""
+    _need_gpu(draft_tokens, parent, tree_len, u_node, u_bonus)
+    if not logits.is_cuda:
+        raise ValueError("expected GPU logits")
+    B, T = parent.shape
+    lg = logits.reshape(B * (T + 1), logits.shape[-1]) if logits.dim() != 2 else logits
+    if lg.stride(1) != 1:
+        raise ValueError("logits need unit stride along the vocabulary")
+    if u_node.dtype != torch.float64 or u_bonus.dtype != torch.float64:
+        raise TypeError("uniforms are float64")
+    V, ld = lg.shape[1], lg.stride(0)
+    dev = parent.device
+    al = torch.empty(B, dtype=torch.int32, device=dev)
+    an = torch.empty((B, T), dtype=torch.int32, device=dev)
+    ot = torch.empty((B, T + 1), dtype=torch.int32, device=dev)
+    nbytes = ptd_verify_sample_workspace_bytes(B, T, V)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    ptd_verify_sample(lg, _dtype_code(lg), V, ld, draft_tokens, parent, tree_len, B, T,
+                      temperature, u_node, u_bonus, al, an, ot, workspace, workspace.numel(),
+                      dev_status)
+    return al, an, ot

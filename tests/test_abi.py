@@ -132,3 +132,31 @@ def test_rope_commit_validation():
     assert _err(C, FAKE, FAKE, FAKE, FAKE, FAKE, P.PTD_MAX_T + 1, _shape(L=8192), FAKE * 2) == 2
     assert _err(C, FAKE, FAKE, FAKE, FAKE, FAKE, 64, bad, FAKE * 2) == 3
     assert _err(C, FAKE, FAKE + 2, FAKE, FAKE, FAKE, 64, s, FAKE * 2) == 4
+
+
+def test_verify_sample_validation():
+    # 65 rows x 16 blocks of 2048 entries x 16 B, 256-rounded
+    assert P.ptd_verify_sample_workspace_bytes(1, 64, 32000) == 65 * 16 * 16
+    assert P.ptd_verify_sample_workspace_bytes(1, 64, 100) == 1280
+    assert P.ptd_verify_sample_workspace_bytes(0, 64, 100) == 0
+    assert P.ptd_verify_sample_workspace_bytes(1, P.PTD_MAX_T + 1, 100) == 0
+    assert P.ptd_verify_sample_workspace_bytes(1, 64, 262145) == 0
+    S = P.ptd_verify_sample
+    args = dict(workspace=FAKE, workspace_bytes=1 << 20)
+    assert _err(S, None, P.PTD_BF16, 100, 100, FAKE, FAKE, None, 1, 4, 1.0, FAKE, FAKE, FAKE,
+                FAKE, FAKE, **args) == 1
+    assert _err(S, FAKE, 5, 100, 100, FAKE, FAKE, None, 1, 4, 1.0, FAKE, FAKE, FAKE, FAKE,
+                FAKE, **args) == 3
+    assert _err(S, FAKE, P.PTD_BF16, 100, 99, FAKE, FAKE, None, 1, 4, 1.0, FAKE, FAKE, FAKE,
+                FAKE, FAKE, **args) == 2                                     # ld < V
+    assert _err(S, FAKE, P.PTD_BF16, 262145, 262145, FAKE, FAKE, None, 1, 4, 1.0, FAKE, FAKE,
+                FAKE, FAKE, FAKE, **args) == 2                               # V above the bitmap
+    for t in (0.0, -1.0, float("inf"), float("nan")):
+        assert _err(S, FAKE, P.PTD_BF16, 100, 100, FAKE, FAKE, None, 1, 4, t, FAKE, FAKE, FAKE,
+                    FAKE, FAKE, **args) == 2
+    assert _err(S, FAKE, P.PTD_BF16, 100, 100, FAKE, FAKE, None, 1, 4, 1.0, FAKE, FAKE, FAKE,
+                FAKE, FAKE, workspace=FAKE, workspace_bytes=16) == 5
+    assert _err(S, FAKE, P.PTD_BF16, 100, 100, FAKE, FAKE, None, 1, 4, 1.0, FAKE, FAKE, FAKE,
+                FAKE, FAKE, workspace=FAKE + 4, workspace_bytes=1 << 20) == 4
+    assert _err(S, FAKE, P.PTD_BF16, 100, 100, FAKE, FAKE, None, 1000, 65, 1.0, FAKE, FAKE,
+                FAKE, FAKE, FAKE, **args) == 2                               # rows > 65535

@@ -358,6 +358,14 @@ def commit_bytes(w: Workload, accept_nodes: np.ndarray, accept_len: np.ndarray) 
     return 2 * 2 * moved * w.Hkv * w.D * es
 
 
+def sample_bytes(w: Workload) -> int:
+    """Bytes sampling verification reads at least: every logits row once (its
+    maximum and normalizer); the gathered candidates and the terminal row's
+    second pass are left out."""
+    es = 2 if w.dtype == "bf16" else 4
+    return w.B * (w.T + 1) * w.V * es
+
+
 def attention_flops(w: Workload) -> int:
     """4 * T * Hq * (kv_len + T) * D per sequence (QK^T and PV over every key
     position a node could see, counted densely over the tree block)."""
