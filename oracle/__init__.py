@@ -46,7 +46,15 @@ def _load():
     lib.oracle_kv_commit.argtypes = [vp, vp, i, vp, vp, vp, i, i, i, i, i, vp]
     lib.oracle_verify_sample.argtypes = [vp, i, ctypes.c_longlong, i, vp, vp, vp, i, i, d,
                                          vp, vp, vp, vp, vp, vp]
-    for f in ("oracle_verify_sample", "oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
+    lib.oracle_step_prune.argtypes = [vp, vp, vp, i, i, i, i, vp, vp, vp]
+    lib.oracle_pool_new.argtypes = [i, i, i]
+    lib.oracle_pool_new.restype = vp
+    lib.oracle_pool_free.argtypes = [vp]
+    lib.oracle_pool_free.restype = None
+    lib.oracle_pool_merge.argtypes = [vp, vp, vp, vp, i, i]
+    lib.oracle_pool_retrieve.argtypes = [vp, vp, i, i, vp, vp, vp]
+    for f in ("oracle_step_prune", "oracle_pool_merge", "oracle_pool_retrieve",
+              "oracle_verify_sample", "oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
               "oracle_topk", "oracle_verify", "oracle_expand", "oracle_tree_rope",
               "oracle_kv_commit"):
         getattr(lib, f).restype = ctypes.c_int
@@ -258,3 +266,53 @@ def verify_sample(logits, tokens, parent, temperature: float, u_node, u_bonus, t
                                         _p(tl), B, T, float(temperature), _p(un), _p(ub),
                                         _p(al), _p(an), _p(ot), _p(mg)))
     return al, an, ot, mg
+
+
+def step_prune(parent, tokens, d_max: int, T_max: int, tree_len=None):
+    """Stepping (depth control) of a draft forest.
+    -> (parent_next [B][T_max], tokens_next [B][T_max], tree_len_next [B])."""
+    parent = _c(parent, np.int32)
+    tokens = _c(tokens, np.int32)
+    B, T = parent.shape
+    pn = np.zeros((B, T_max), np.int32)
+    tn = np.zeros((B, T_max), np.int32)
+    ln = np.zeros(B, np.int32)
+    tl = None if tree_len is None else _c(tree_len, np.int32)
+    _check(_load().oracle_step_prune(_p(parent), _p(tokens), _p(tl), B, T, int(d_max),
+                                     int(T_max), _p(pn), _p(tn), _p(ln)))
+    return pn, tn, ln
+
+
+class Pool:
+    """Candidate pool of B sequences: trees of tokens keyed by their root's
+    token, at most e_max trees of at most n_cap nodes per sequence."""
+
+    def __init__(self, B: int, e_max: int, n_cap: int):
+        self.B = B
+        self._lib = _load()
+        self._h = self._lib.oracle_pool_new(B, e_max, n_cap)
+        if not self._h:
+            raise OracleError("bad sizes")
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h:
+            self._lib.oracle_pool_free(h)
+            self._h = None
+
+    def merge(self, parent, tokens, tree_len=None):
+        parent = _c(parent, np.int32)
+        tokens = _c(tokens, np.int32)
+        B, T = parent.shape
+        tl = None if tree_len is None else _c(tree_len, np.int32)
+        _check(self._lib.oracle_pool_merge(self._h, _p(parent), _p(tokens), _p(tl), B, T))
+
+    def retrieve(self, last_token, T_max: int):
+        """-> (parent [B][T_max], tokens [B][T_max], tree_len [B])."""
+        lt = _c(last_token, np.int32)
+        po = np.zeros((self.B, T_max), np.int32)
+        to = np.zeros((self.B, T_max), np.int32)
+        ln = np.zeros(self.B, np.int32)
+        _check(self._lib.oracle_pool_retrieve(self._h, _p(lt), self.B, int(T_max), _p(po),
+                                              _p(to), _p(ln)))
+        return po, to, ln

@@ -593,3 +593,219 @@ int oracle_verify_sample(const void* logits, int dtype, long long ld, int V,
   free(prob);
   return status;
 }
+
+/* ---------------------------------------------------------------------------
+ * Stepping: depth control of the draft tree (Sec. 3.1 "Overhead Constraints",
+ * Stepping Mechanism; Alg. 1 step 3).  When a sub-tree (the tree under one
+ * root of the forest) is deeper than d_max, its earliest-added child and that
+ * child's descendants become the sub-tree and every other branch is pruned.
+ * Depth of a sub-tree = number of nodes on its longest root path.  The
+ * earliest-added child of a node is its lowest-index child (breadth-first
+ * numbering puts old children before new ones, and new ones in candidate
+ * order).  Stepping repeats until the depth is at most d_max, so a chain
+ * keeps its last d_max nodes (a sliding window).  The kept forest is
+ * renumbered breadth-first -- by depth; by the parent's new index; siblings
+ * in old index order; roots in the order of the roots they replace -- and cut
+ * to T_max nodes; slots from tree_len_next on hold -1.
+ * ------------------------------------------------------------------------- */
+int oracle_step_prune(const int32_t* parent, const int32_t* tokens, const int32_t* tree_len,
+                      int B, int T, int d_max, int T_max, int32_t* parent_next,
+                      int32_t* tokens_next, int32_t* tree_len_next) {
+  if (B < 0 || T < 1 || d_max < 1 || T_max < 1) return ORC_BAD_SIZE;
+  int status = ORC_OK;
+  int* h = (int*)malloc(sizeof(int) * (size_t)T);       /* depth of the sub-tree under v */
+  int* fc = (int*)malloc(sizeof(int) * (size_t)T);      /* lowest-index child */
+  int* keep = (int*)malloc(sizeof(int) * (size_t)T);
+  int* order = (int*)malloc(sizeof(int) * (size_t)T);
+  int* newid = (int*)malloc(sizeof(int) * (size_t)T);
+  if (!h || !fc || !keep || !order || !newid) {
+    free(h); free(fc); free(keep); free(order); free(newid);
+    return ORC_BAD_SIZE;
+  }
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int32_t* tok = tokens + (size_t)b * T;
+    int32_t* pn = parent_next + (size_t)b * T_max;
+    int32_t* tn = tokens_next + (size_t)b * T_max;
+    for (int i = 0; i < T_max; ++i) { pn[i] = -1; tn[i] = -1; }
+    tree_len_next[b] = 0;
+    const int n = node_count(tree_len, b, T);
+    if (!tree_is_valid(par, n)) { status = ORC_BAD_TREE; continue; }
+    for (int v = 0; v < n; ++v) { h[v] = 1; fc[v] = -1; keep[v] = 0; }
+    for (int v = n - 1; v >= 0; --v)          /* children have larger indices */
+      if (par[v] >= 0 && h[v] + 1 > h[par[v]]) h[par[v]] = h[v] + 1;
+    for (int v = 0; v < n; ++v)
+      if (par[v] >= 0 && fc[par[v]] < 0) fc[par[v]] = v;
+    /* the new root of each sub-tree, in the order of the old roots */
+    int nroots = 0;
+    for (int r = 0; r < n; ++r) {
+      if (par[r] != -1) continue;
+      int x = r;
+      while (h[x] > d_max) x = fc[x];         /* h > 1 means a child exists */
+      keep[x] = 2;                            /* 2: a root of the kept forest */
+      order[nroots++] = x;
+    }
+    for (int v = 0; v < n; ++v)
+      if (!keep[v] && par[v] >= 0 && keep[par[v]]) keep[v] = 1;
+    /* breadth-first renumbering of the kept forest */
+    int cnt = nroots;
+    for (int i = 0; i < nroots; ++i) newid[order[i]] = i;
+    for (int head = 0; head < cnt; ++head) {
+      const int p = order[head];
+      for (int c = p + 1; c < n; ++c)
+        if (keep[c] == 1 && par[c] == p) { newid[c] = cnt; order[cnt++] = c; }
+    }
+    const int out = cnt < T_max ? cnt : T_max;
+    for (int t = 0; t < out; ++t) {
+      const int c = order[t];
+      pn[t] = keep[c] == 2 ? -1 : newid[par[c]];
+      tn[t] = tok[c];
+    }
+    tree_len_next[b] = out;
+  }
+  free(h); free(fc); free(keep); free(order); free(newid);
+  return status;
+}
+
+/* ---------------------------------------------------------------------------
+ * Candidate pool (Sec. 3.1 "Draft Extraction via Merging"; Alg. 1 steps 1
+ * and 4).  Per sequence: candidate trees of tokens keyed by their root's
+ * token.
+ * Merge of a draft tree: for every node u (index order), the sub-tree of u --
+ * u and its descendants, a tree rooted at token(u) -- is merged by M into the
+ * pool tree keyed token(u) (created with a lone root if absent): a child of
+ * the draft node whose token is not among the children of the matching pool
+ * node is added, one whose token is there is merged into it, recursively.
+ * Children are taken in index order and a node is added before its own
+ * children (depth first), which fixes the insertion order.  Bounds: a pool
+ * tree holds at most n_cap nodes (its root included), a sequence at most
+ * e_max trees; an insertion beyond either bound is skipped together with the
+ * sub-tree it would carry.
+ * Retrieve: the pool tree keyed by the last committed token, without its
+ * root, as a packed draft tree: breadth first (by depth; by the parent's
+ * output index; siblings in insertion order), the root's children with
+ * parent -1, cut to T_max nodes; tree_len 0 if there is no such tree.
+ * The state is this file's own (struct OraclePool); callers hold an opaque
+ * pointer.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int B, e_max, n_cap;
+  int* ntrees;   /* [B] */
+  int* key;      /* [B][e_max] */
+  int* count;    /* [B][e_max] */
+  int* tok;      /* [B][e_max][n_cap] */
+  int* par;      /* [B][e_max][n_cap]: index of the parent in the same tree, -1 at the root */
+} OraclePool;
+
+void* oracle_pool_new(int B, int e_max, int n_cap) {
+  if (B < 1 || e_max < 1 || n_cap < 1) return NULL;
+  OraclePool* p = (OraclePool*)calloc(1, sizeof(OraclePool));
+  if (!p) return NULL;
+  p->B = B; p->e_max = e_max; p->n_cap = n_cap;
+  p->ntrees = (int*)calloc((size_t)B, sizeof(int));
+  p->key = (int*)calloc((size_t)B * e_max, sizeof(int));
+  p->count = (int*)calloc((size_t)B * e_max, sizeof(int));
+  p->tok = (int*)calloc((size_t)B * e_max * n_cap, sizeof(int));
+  p->par = (int*)calloc((size_t)B * e_max * n_cap, sizeof(int));
+  if (!p->ntrees || !p->key || !p->count || !p->tok || !p->par) {
+    free(p->ntrees); free(p->key); free(p->count); free(p->tok); free(p->par); free(p);
+    return NULL;
+  }
+  return p;
+}
+
+void oracle_pool_free(void* pool) {
+  OraclePool* p = (OraclePool*)pool;
+  if (!p) return;
+  free(p->ntrees); free(p->key); free(p->count); free(p->tok); free(p->par); free(p);
+}
+
+/* M(pool tree e at node pn, draft sub-tree under draft node u) */
+static void pool_merge_rec(OraclePool* p, int b, int e, int pn, const int32_t* par,
+                           const int32_t* tok, int n, int u) {
+  int* cnt = &p->count[(size_t)b * p->e_max + e];
+  int* ttok = p->tok + ((size_t)b * p->e_max + e) * p->n_cap;
+  int* tpar = p->par + ((size_t)b * p->e_max + e) * p->n_cap;
+  for (int c = u + 1; c < n; ++c) {
+    if (par[c] != u) continue;
+    int match = -1;
+    for (int k = 0; k < *cnt; ++k)
+      if (tpar[k] == pn && ttok[k] == tok[c]) { match = k; break; }
+    if (match < 0) {
+      if (*cnt >= p->n_cap) continue;          /* full: skip c and its sub-tree */
+      match = *cnt;
+      ttok[match] = tok[c];
+      tpar[match] = pn;
+      ++*cnt;
+    }
+    pool_merge_rec(p, b, e, match, par, tok, n, c);
+  }
+}
+
+int oracle_pool_merge(void* pool, const int32_t* parent, const int32_t* tokens,
+                      const int32_t* tree_len, int B, int T) {
+  OraclePool* p = (OraclePool*)pool;
+  if (!p || B != p->B || T < 1) return ORC_BAD_SIZE;
+  int status = ORC_OK;
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int32_t* tok = tokens + (size_t)b * T;
+    const int n = node_count(tree_len, b, T);
+    if (!tree_is_valid(par, n)) { status = ORC_BAD_TREE; continue; }
+    for (int u = 0; u < n; ++u) {
+      int e = -1;
+      for (int k = 0; k < p->ntrees[b]; ++k)
+        if (p->key[(size_t)b * p->e_max + k] == tok[u]) { e = k; break; }
+      if (e < 0) {
+        if (p->ntrees[b] >= p->e_max) continue;  /* no room for another tree */
+        e = p->ntrees[b]++;
+        p->key[(size_t)b * p->e_max + e] = tok[u];
+        p->count[(size_t)b * p->e_max + e] = 1;
+        p->tok[((size_t)b * p->e_max + e) * p->n_cap] = tok[u];
+        p->par[((size_t)b * p->e_max + e) * p->n_cap] = -1;
+      }
+      pool_merge_rec(p, b, e, 0, par, tok, n, u);
+    }
+  }
+  return status;
+}
+
+int oracle_pool_retrieve(void* pool, const int32_t* last_token, int B, int T_max,
+                         int32_t* parent_out, int32_t* tokens_out, int32_t* tree_len_out) {
+  OraclePool* p = (OraclePool*)pool;
+  if (!p || B != p->B || T_max < 1) return ORC_BAD_SIZE;
+  int* order = (int*)malloc(sizeof(int) * (size_t)p->n_cap);
+  int* outid = (int*)malloc(sizeof(int) * (size_t)p->n_cap);
+  if (!order || !outid) { free(order); free(outid); return ORC_BAD_SIZE; }
+  for (int b = 0; b < B; ++b) {
+    int32_t* po = parent_out + (size_t)b * T_max;
+    int32_t* to = tokens_out + (size_t)b * T_max;
+    for (int i = 0; i < T_max; ++i) { po[i] = -1; to[i] = -1; }
+    tree_len_out[b] = 0;
+    int e = -1;
+    for (int k = 0; k < p->ntrees[b]; ++k)
+      if (p->key[(size_t)b * p->e_max + k] == last_token[b]) { e = k; break; }
+    if (e < 0) continue;
+    const int cnt = p->count[(size_t)b * p->e_max + e];
+    const int* ttok = p->tok + ((size_t)b * p->e_max + e) * p->n_cap;
+    const int* tpar = p->par + ((size_t)b * p->e_max + e) * p->n_cap;
+    /* breadth first from the root (node 0); children in insertion order */
+    int q = 0;
+    order[q++] = 0;
+    outid[0] = -1;
+    for (int head = 0; head < q; ++head) {
+      const int x = order[head];
+      for (int k = 0; k < cnt; ++k)
+        if (tpar[k] == x) { outid[k] = q - 1; order[q++] = k; }
+    }
+    const int len = (q - 1) < T_max ? (q - 1) : T_max;
+    for (int i = 0; i < len; ++i) {
+      const int k = order[i + 1];
+      to[i] = ttok[k];
+      po[i] = outid[tpar[k]];
+    }
+    tree_len_out[b] = len;
+  }
+  free(order); free(outid);
+  return ORC_OK;
+}

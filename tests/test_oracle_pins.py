@@ -817,3 +817,147 @@ def test_sample_empty_tree_draws_from_the_root_row():
                                     tree_len=np.zeros(n, np.int32))
     assert (al == 0).all() and (an == -1).all()
     assert _chi2_ok(np.bincount(ot[:, 0], minlength=3), P0, n)
+
+
+# ---------------------------------------------------------------------------
+# stepping (depth control) and the candidate pool
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("L,d_max", [(1, 1), (5, 1), (8, 3), (8, 8), (20, 6)])
+def test_step_prune_chain_is_a_sliding_window(L, d_max):
+    par, _ = W.tree_chain(L)
+    tok = (np.arange(L) * 7 + 3).astype(np.int32)
+    pn, tn, ln = O.step_prune(par[None], tok[None], d_max, L)
+    keep = min(L, d_max)
+    assert ln[0] == keep
+    assert tn[0, :keep].tolist() == tok[L - keep:].tolist()
+    assert pn[0, :keep].tolist() == [-1] + list(range(keep - 1))
+    assert (pn[0, keep:] == -1).all() and (tn[0, keep:] == -1).all()
+
+
+def test_step_prune_heap_tree_closed_form():
+    # heap numbering, 5 levels: the root steps to node 1 (depth 4 > 3), then
+    # to node 3 (depth 3); node 3's sub-tree is {3, 7, 8, 15, 16, 17, 18}
+    T = 31
+    par = np.array([-1] + [(i - 1) // 2 for i in range(1, T)], np.int32)
+    pn, tn, ln = O.step_prune(par[None], np.arange(T, dtype=np.int32)[None], 3, T)
+    assert ln[0] == 7
+    assert tn[0, :7].tolist() == [3, 7, 8, 15, 16, 17, 18]
+    assert pn[0, :7].tolist() == [-1, 0, 0, 1, 1, 2, 2]
+
+
+def test_step_prune_shallow_bfs_forest_is_unchanged():
+    par, _ = W.tree_branching([3, 2, 2], 20)
+    tok = np.arange(20, dtype=np.int32) + 100
+    pn, tn, ln = O.step_prune(par[None], tok[None], 3, 20)
+    assert ln[0] == 20 and np.array_equal(pn[0], par) and np.array_equal(tn[0], tok)
+
+
+@pytest.mark.parametrize("d_max", [1, 2, 3, 5])
+def test_step_prune_invariants(d_max):
+    rng = np.random.default_rng(30 + d_max)
+    B, T = 6, 40
+    par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    tok = np.broadcast_to(np.arange(T, dtype=np.int32), (B, T)).copy()   # token = old id
+    pn, tn, ln = O.step_prune(par, tok, d_max, T)
+    _, depth = O.tree_mask(pn, ln)
+    for b in range(B):
+        n = int(ln[b])
+        assert depth[b, :n].max() <= d_max
+        kids = {v: [c for c in range(T) if par[b, c] == v] for v in range(T)}
+        roots_in = [r for r in range(T) if par[b, r] == -1]
+        roots_out = [int(tn[b, i]) for i in range(n) if pn[b, i] == -1]
+        # one new root per old sub-tree, in the old roots' order, each on the
+        # old root's chain of lowest-index children
+        assert len(roots_out) == len(roots_in)
+        for r, x in zip(roots_in, roots_out):
+            chain = [r]
+            while kids[chain[-1]]:
+                chain.append(kids[chain[-1]][0])
+            assert x in chain
+        for i in range(n):
+            # an output node's root path is the tail of its old root path
+            path_out = []
+            j = i
+            while j >= 0:
+                path_out.append(int(tn[b, j]))
+                j = int(pn[b, j])
+            path_in = []
+            v = int(tn[b, i])
+            while v >= 0:
+                path_in.append(v)
+                v = int(par[b, v])
+            assert path_in[:len(path_out)] == path_out
+        # the kept node set is closed under children
+        kept = set(tn[b, :n].tolist())
+        for v in kept:
+            assert all(c in kept for c in kids[v])
+
+
+def _token_paths(par, tok, n):
+    """key token -> set of token tuples, one per (node u, proper descendant v):
+    the tokens from u's child down to v (every sub-tree of the draft)."""
+    out = {}
+    for v in range(n):
+        chain = []
+        a = v
+        while a >= 0:
+            chain.append(a)
+            a = int(par[a])
+        chain = chain[::-1]                       # root .. v
+        for i in range(len(chain) - 1):           # u = chain[i]
+            out.setdefault(int(tok[chain[i]]), set()).add(tuple(int(tok[x]) for x in chain[i + 1:]))
+    return out
+
+
+def _retrieved_paths(pn, tn, n):
+    paths = set()
+    for i in range(n):
+        p = []
+        j = i
+        while j >= 0:
+            p.append(int(tn[j]))
+            j = int(pn[j])
+        paths.add(tuple(p[::-1]))
+    return paths
+
+
+def test_pool_merge_is_the_union_of_token_paths():
+    # M adds the children missing by value and merges the common ones, so a
+    # pool tree's root paths are the union of those of the merged sub-trees
+    rng = np.random.default_rng(40)
+    B, T, V = 3, 24, 6                      # few token values: many merges hit
+    pool = O.Pool(B, 512, 1024)
+    want = [dict() for _ in range(B)]
+    for step in range(4):
+        par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+        tok = rng.integers(0, V, (B, T)).astype(np.int32)
+        tl = rng.integers(1, T + 1, B).astype(np.int32)
+        pool.merge(par, tok, tl)
+        for b in range(B):
+            for k, ps in _token_paths(par[b], tok[b], int(tl[b])).items():
+                want[b].setdefault(k, set()).update(ps)
+    for key in range(V + 1):
+        pn, tn, ln = pool.retrieve(np.full(B, key, np.int32), 1024)
+        for b in range(B):
+            n = int(ln[b])
+            assert _retrieved_paths(pn[b], tn[b], n) == want[b].get(key, set())
+            # siblings carry distinct tokens, parents come first
+            for i in range(n):
+                assert pn[b, i] < i
+                sib = [tn[b, j] for j in range(n) if pn[b, j] == pn[b, i]]
+                assert len(sib) == len(set(sib))
+
+
+def test_pool_golden():
+    g = _golden("pool_example.json")
+    par = np.array([g["draft"]["parent"]], np.int32)
+    tok = np.array([g["draft"]["tokens"]], np.int32)
+    for case in ("small", "large"):
+        c = g[case]
+        pool = O.Pool(1, c["e_max"], c["n_cap"])
+        pool.merge(par, tok)
+        for last, wp, wt in zip(c["last"], c["parent"], c["tokens"]):
+            pn, tn, ln = pool.retrieve(np.array([last], np.int32), 8)
+            assert ln[0] == len(wt), (case, last)
+            assert pn[0, :ln[0]].tolist() == wp and tn[0, :ln[0]].tolist() == wt, (case, last)
+            assert (pn[0, ln[0]:] == -1).all() and (tn[0, ln[0]:] == -1).all()
