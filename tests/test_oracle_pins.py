@@ -893,7 +893,7 @@ def test_step_prune_invariants(d_max):
             assert all(c in kept for c in kids[v])
 
 
-def _token_paths(par, tok, n):
+def _subtree_paths(par, tok, n):
     """key token -> set of token tuples, one per (node u, proper descendant v):
     the tokens from u's child down to v (every sub-tree of the draft)."""
     out = {}
@@ -934,7 +934,7 @@ def test_pool_merge_is_the_union_of_token_paths():
         tl = rng.integers(1, T + 1, B).astype(np.int32)
         pool.merge(par, tok, tl)
         for b in range(B):
-            for k, ps in _token_paths(par[b], tok[b], int(tl[b])).items():
+            for k, ps in _subtree_paths(par[b], tok[b], int(tl[b])).items():
                 want[b].setdefault(k, set()).update(ps)
     for key in range(V + 1):
         pn, tn, ln = pool.retrieve(np.full(B, key, np.int32), 1024)
