@@ -676,8 +676,8 @@ int oracle_step_prune(const int32_t* parent, const int32_t* tokens, const int32_
  * pool tree keyed token(u) (created with a lone root if absent): a child of
  * the draft node whose token is not among the children of the matching pool
  * node is added, one whose token is there is merged into it, recursively.
- * Children are taken in index order and a node is added before its own
- * children (depth first), which fixes the insertion order.  Bounds: a pool
+ * The sub-tree's nodes are taken in index order (each after its parent),
+ * which fixes the insertion order.  Bounds: a pool
  * tree holds at most n_cap nodes (its root included), a sequence at most
  * e_max trees; an insertion beyond either bound is skipped together with the
  * sub-tree it would carry.
@@ -720,25 +720,29 @@ void oracle_pool_free(void* pool) {
   free(p->ntrees); free(p->key); free(p->count); free(p->tok); free(p->par); free(p);
 }
 
-/* M(pool tree e at node pn, draft sub-tree under draft node u) */
-static void pool_merge_rec(OraclePool* p, int b, int e, int pn, const int32_t* par,
-                           const int32_t* tok, int n, int u) {
+/* M(pool tree e, draft sub-tree under draft node u): the sub-tree's nodes in
+ * index order (every node after its parent); map[v] = pool node of draft
+ * node v, -1 outside the sub-tree or skipped. */
+static void pool_merge_subtree(OraclePool* p, int b, int e, const int32_t* par,
+                               const int32_t* tok, int n, int u, int* map) {
   int* cnt = &p->count[(size_t)b * p->e_max + e];
   int* ttok = p->tok + ((size_t)b * p->e_max + e) * p->n_cap;
   int* tpar = p->par + ((size_t)b * p->e_max + e) * p->n_cap;
+  for (int v = 0; v < n; ++v) map[v] = -1;
+  map[u] = 0;                                  /* the pool tree's root */
   for (int c = u + 1; c < n; ++c) {
-    if (par[c] != u) continue;
+    const int pn = map[par[c]];
+    if (par[c] < u || pn < 0) continue;        /* outside the sub-tree, or skipped */
     int match = -1;
     for (int k = 0; k < *cnt; ++k)
       if (tpar[k] == pn && ttok[k] == tok[c]) { match = k; break; }
-    if (match < 0) {
-      if (*cnt >= p->n_cap) continue;          /* full: skip c and its sub-tree */
+    if (match < 0 && *cnt < p->n_cap) {
       match = *cnt;
       ttok[match] = tok[c];
       tpar[match] = pn;
       ++*cnt;
     }
-    pool_merge_rec(p, b, e, match, par, tok, n, c);
+    map[c] = match;                            /* -1: full, c and its sub-tree skipped */
   }
 }
 
@@ -747,6 +751,8 @@ int oracle_pool_merge(void* pool, const int32_t* parent, const int32_t* tokens,
   OraclePool* p = (OraclePool*)pool;
   if (!p || B != p->B || T < 1) return ORC_BAD_SIZE;
   int status = ORC_OK;
+  int* map = (int*)malloc(sizeof(int) * (size_t)T);
+  if (!map) return ORC_BAD_SIZE;
   for (int b = 0; b < B; ++b) {
     const int32_t* par = parent + (size_t)b * T;
     const int32_t* tok = tokens + (size_t)b * T;
@@ -764,9 +770,10 @@ int oracle_pool_merge(void* pool, const int32_t* parent, const int32_t* tokens,
         p->tok[((size_t)b * p->e_max + e) * p->n_cap] = tok[u];
         p->par[((size_t)b * p->e_max + e) * p->n_cap] = -1;
       }
-      pool_merge_rec(p, b, e, 0, par, tok, n, u);
+      pool_merge_subtree(p, b, e, par, tok, n, u, map);
     }
   }
+  free(map);
   return status;
 }
 
