@@ -222,7 +222,37 @@ def main():
                             u_node, u_bonus, s_al, s_an, s_ot, ws_samp, ws_samp.numel(), status,
                             sp)
 
+    # stepping of the expanded tree, its merge into a candidate pool, and the
+    # retrieval of the next candidate tree by the bonus token
+    d_prune = max(1, w.d_max - 1)
+    sp_pn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
+    sp_tn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
+    sp_ln = torch.empty(B, dtype=torch.int32, device=dev)
+    pool_e, pool_n = 2048, 64
+    pool_bytes = P.ptd_pool_bytes(B, pool_e, pool_n)
+    pool = torch.empty(pool_bytes, dtype=torch.uint8, device=dev)
+    P.ptd_pool_init(pool, pool_bytes, B, pool_e, pool_n, stream=sp)
+    bonus = torch.gather(ot, 1, al.long().view(B, 1)).view(B).contiguous()
+    rt_pn = torch.empty((B, 64), dtype=torch.int32, device=dev)
+    rt_tn = torch.empty((B, 64), dtype=torch.int32, device=dev)
+    rt_ln = torch.empty(B, dtype=torch.int32, device=dev)
+    small_tree = w.T_max <= 64
+
+    def prune(i):
+        P.ptd_step_prune(pn, tn, ln, B, w.T_max, d_prune, w.T_max, sp_pn, sp_tn, sp_ln, status, sp)
+
+    def merge(i):
+        P.ptd_pool_merge(pool, pool_bytes, B, pool_e, pool_n, pn, tn, ln, w.T_max, status, sp)
+
+    def retrieve(i):
+        P.ptd_pool_retrieve(pool, pool_bytes, B, pool_e, pool_n, bonus, 64, rt_pn, rt_tn, rt_ln,
+                            sp)
+
     sample_ms, _ = timed(sample, K)
+    if small_tree:
+        prune_ms, _ = timed(prune, K)
+        merge_ms, _ = timed(merge, K)
+        retrieve_ms, _ = timed(retrieve, K)
     rope_ms, _ = timed(rope, K)
     commit_ms, _ = timed(commit, K)
     torch.cuda.synchronize()
@@ -305,6 +335,19 @@ def main():
                                       % (B * (T + 1), K)),
         },
     }
+    if small_tree:
+        tree_b = B * w.T_max * 4 * 2
+        line["next_rows"].update({
+            "step_prune": next_row(prune_ms, 2 * tree_b, "ptd_step_prune of the expanded trees "
+                                   "(T_max %d) at d_max %d, %d back-to-back calls"
+                                   % (w.T_max, d_prune, K)),
+            "pool_merge": next_row(merge_ms, tree_b, "ptd_pool_merge of the expanded trees into "
+                                   "a pool of %d trees x %d nodes per sequence (first call grows "
+                                   "it, later calls find every node), %d back-to-back calls"
+                                   % (pool_e, pool_n, K)),
+            "pool_retrieve": next_row(retrieve_ms, tree_b, "ptd_pool_retrieve of the candidate "
+                                      "trees keyed by the bonus tokens, %d back-to-back calls" % K),
+        })
     print(json.dumps(line), flush=True)
 
 

@@ -17,6 +17,9 @@
  *   ptd_kv_commit        the accepted path's keys/values become committed rows
  *   ptd_verify_sample    sampling verification (recursive candidate-tree
  *                        sampling) with caller-drawn uniforms
+ *   ptd_step_prune       stepping: depth control of the draft forest
+ *   ptd_pool_*           the value-keyed candidate pool: merge of every
+ *                        draft sub-tree, retrieval by the last token
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers owned by the caller (stream-ordered;
@@ -368,6 +371,76 @@ int ptd_verify_sample(const void* logits, ptd_dtype dtype, int32_t V, int64_t ld
                       const double* u_node, const double* u_bonus, int32_t* accept_len,
                       int32_t* accept_nodes, int32_t* out_tokens, void* workspace,
                       size_t workspace_bytes, int32_t* dev_status, void* stream);
+
+/*
+ * ptd_step_prune -- stepping, the depth control of the draft tree (Sec. 3.1
+ * "Overhead Constraints", Stepping Mechanism; Alg. 1 step 3).  A sub-tree
+ * (the tree under one root of the forest) deeper than d_max is replaced by
+ * the sub-tree of its earliest-added child -- the lowest-index child -- and
+ * its other branches are pruned, repeatedly, so a chain keeps its last d_max
+ * nodes.  Depth = number of nodes on the longest root path.  The kept forest
+ * is renumbered breadth first (by depth; by the parent's new index; siblings
+ * in old index order; roots in the order of the roots they replace) and cut
+ * to T_max nodes; slots from tree_len_next on hold -1.
+ *   parent, tokens  int32 [B][T], T 1 .. 64;  tree_len int32 [B] or NULL
+ *   d_max           >= 1;  T_max 1 .. PTD_MAX_T
+ *   parent_next, tokens_next  int32 [B][T_max];  tree_len_next int32 [B]
+ * dev_status: PTD_ERR_BAD_TREE (that sequence's output is empty).
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_HIP.
+ */
+int ptd_step_prune(const int32_t* parent, const int32_t* tokens, const int32_t* tree_len,
+                   int32_t B, int32_t T, int32_t d_max, int32_t T_max, int32_t* parent_next,
+                   int32_t* tokens_next, int32_t* tree_len_next, int32_t* dev_status,
+                   void* stream);
+
+/*
+ * Candidate pool (Sec. 3.1 "Draft Extraction via Merging"; Alg. 1 steps 1
+ * and 4): per sequence, trees of tokens keyed by the token of their root, at
+ * most e_max trees (1 .. 2048) of at most n_cap nodes (1 .. 64, root
+ * included).  The pool is a caller-owned device buffer of ptd_pool_bytes
+ * bytes, 256-byte aligned, set up once by ptd_pool_init; every call that
+ * names it must pass the same B, e_max and n_cap.  Calls on one pool must not
+ * overlap.  Returns 0 from ptd_pool_bytes on invalid arguments.
+ */
+size_t ptd_pool_bytes(int32_t B, int32_t e_max, int32_t n_cap);
+int ptd_pool_init(void* pool, size_t pool_bytes, int32_t B, int32_t e_max, int32_t n_cap,
+                  void* stream);
+
+/*
+ * ptd_pool_merge -- for every node u of the draft tree (index order), the
+ * sub-tree of u (u and its descendants, a tree rooted at token(u)) is merged
+ * by M into the pool tree keyed token(u), which is created with a lone root
+ * if absent: a child whose token is not among the matching pool node's
+ * children is added, one whose token is there is merged into it.  A
+ * sub-tree's nodes are taken in index order (each after its parent), which
+ * fixes the insertion order.  An insertion beyond n_cap nodes, or a new tree
+ * beyond e_max trees, is skipped together with what it would carry.
+ *   parent, tokens  int32 [B][T], T 1 .. 64;  tree_len int32 [B] or NULL
+ * dev_status: PTD_ERR_BAD_TREE (that sequence's pool is left unchanged).
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_WORKSPACE (pool_bytes too
+ * small), PTD_ERR_ALIGN, PTD_ERR_HIP.
+ */
+int ptd_pool_merge(void* pool, size_t pool_bytes, int32_t B, int32_t e_max, int32_t n_cap,
+                   const int32_t* parent, const int32_t* tokens, const int32_t* tree_len,
+                   int32_t T, int32_t* dev_status, void* stream);
+
+/*
+ * ptd_pool_retrieve -- the candidate tree C_X of the next step: the pool tree
+ * keyed by last_token[b] (the last committed token), without its root, as a
+ * packed tree: breadth first (by depth; by the parent's output index;
+ * siblings in insertion order), the root's children with parent -1, cut to
+ * T_max nodes; slots from tree_len_out on hold -1; tree_len_out 0 if there is
+ * no such tree.
+ *   last_token      int32 [B]
+ *   parent_out, tokens_out  int32 [B][T_max], T_max 1 .. PTD_MAX_T;
+ *   tree_len_out    int32 [B]
+ * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_WORKSPACE, PTD_ERR_ALIGN,
+ * PTD_ERR_HIP.
+ */
+int ptd_pool_retrieve(const void* pool, size_t pool_bytes, int32_t B, int32_t e_max,
+                      int32_t n_cap, const int32_t* last_token, int32_t T_max,
+                      int32_t* parent_out, int32_t* tokens_out, int32_t* tree_len_out,
+                      void* stream);
 
 #ifdef __cplusplus
 }

@@ -10,7 +10,8 @@ device memory and the stream.  There is no CPU fallback: without a built
 
 The lower-case helpers (``tree_mask``, ``tree_attention``, ``topk_argmax``,
 ``verify``, ``expand``, ``verify_expand``, ``tree_rope``, ``kv_commit``,
-``verify_sample``) allocate outputs with torch and call the entry points.
+``verify_sample``, ``step_prune``, the ``Pool`` class) allocate outputs with
+torch and call the entry points.
 """
 from __future__ import annotations
 
@@ -72,6 +73,14 @@ _SIGS = {
     "ptd_kv_commit": ([_vp, _vp, _vp, _vp, _vp, _i32, ctypes.POINTER(AttnShape), _vp, _vp,
                        _vp], ctypes.c_int),
     "ptd_verify_sample_workspace_bytes": ([_i32, _i32, _i32], _sz),
+    "ptd_step_prune": ([_vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp],
+                       ctypes.c_int),
+    "ptd_pool_bytes": ([_i32, _i32, _i32], _sz),
+    "ptd_pool_init": ([_vp, _sz, _i32, _i32, _i32, _vp], ctypes.c_int),
+    "ptd_pool_merge": ([_vp, _sz, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp],
+                       ctypes.c_int),
+    "ptd_pool_retrieve": ([_vp, _sz, _i32, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp],
+                          ctypes.c_int),
     "ptd_verify_sample": ([_vp, ctypes.c_int, _i32, _i64, _vp, _vp, _vp, _i32, _i32,
                            ctypes.c_double, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _vp],
                           ctypes.c_int),
@@ -218,6 +227,39 @@ def ptd_verify_sample(logits, dtype, V, ld, draft_tokens, parent, tree_len, B, T
                                   _ptr(out_tokens), _ptr(workspace), workspace_bytes,
                                   _ptr(dev_status), _stream(stream)),
            "ptd_verify_sample")
+
+
+def ptd_step_prune(parent, tokens, tree_len, B, T, d_max, T_max, parent_next, tokens_next,
+                   tree_len_next, dev_status=None, stream=None):
+    _check(_lib.ptd_step_prune(_ptr(parent), _ptr(tokens), _ptr(tree_len), B, T, d_max, T_max,
+                               _ptr(parent_next), _ptr(tokens_next), _ptr(tree_len_next),
+                               _ptr(dev_status), _stream(stream)),
+           "ptd_step_prune")
+
+
+def ptd_pool_bytes(B: int, e_max: int, n_cap: int) -> int:
+    return _lib.ptd_pool_bytes(B, e_max, n_cap)
+
+
+def ptd_pool_init(pool, pool_bytes, B, e_max, n_cap, stream=None):
+    _check(_lib.ptd_pool_init(_ptr(pool), pool_bytes, B, e_max, n_cap, _stream(stream)),
+           "ptd_pool_init")
+
+
+def ptd_pool_merge(pool, pool_bytes, B, e_max, n_cap, parent, tokens, tree_len, T,
+                   dev_status=None, stream=None):
+    _check(_lib.ptd_pool_merge(_ptr(pool), pool_bytes, B, e_max, n_cap, _ptr(parent),
+                               _ptr(tokens), _ptr(tree_len), T, _ptr(dev_status),
+                               _stream(stream)),
+           "ptd_pool_merge")
+
+
+def ptd_pool_retrieve(pool, pool_bytes, B, e_max, n_cap, last_token, T_max, parent_out,
+                      tokens_out, tree_len_out, stream=None):
+    _check(_lib.ptd_pool_retrieve(_ptr(pool), pool_bytes, B, e_max, n_cap, _ptr(last_token),
+                                  T_max, _ptr(parent_out), _ptr(tokens_out),
+                                  _ptr(tree_len_out), _stream(stream)),
+           "ptd_pool_retrieve")
 
 
 # ---------------------------------------------------------------------------
@@ -399,3 +441,44 @@ def verify_sample(logits, draft_tokens, parent, temperature: float, u_node, u_bo
                       temperature, u_node, u_bonus, al, an, ot, workspace, workspace.numel(),
                       dev_status)
     return al, an, ot
+
+
+def step_prune(parent, tokens, d_max: int, T_max: int, tree_len=None, dev_status=None):
+    """Returns (parent_next, tokens_next, tree_len_next)."""
+    _need_gpu(parent, tokens, tree_len)
+    B, T = parent.shape
+    dev = parent.device
+    pn = torch.empty((B, T_max), dtype=torch.int32, device=dev)
+    tn = torch.empty((B, T_max), dtype=torch.int32, device=dev)
+    ln = torch.empty(B, dtype=torch.int32, device=dev)
+    ptd_step_prune(parent, tokens, tree_len, B, T, d_max, T_max, pn, tn, ln, dev_status)
+    return pn, tn, ln
+
+
+class Pool:
+    """A device candidate pool of B sequences (at most e_max trees of at
+    most n_cap nodes per sequence), set up on construction."""
+
+    def __init__(self, B: int, e_max: int, n_cap: int, device="cuda"):
+        self.B, self.e_max, self.n_cap = B, e_max, n_cap
+        self.nbytes = ptd_pool_bytes(B, e_max, n_cap)
+        if not self.nbytes:
+            raise ValueError("invalid pool sizes")
+        self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+        ptd_pool_init(self.buf, self.nbytes, B, e_max, n_cap)
+
+    def merge(self, parent, tokens, tree_len=None, dev_status=None):
+        _need_gpu(parent, tokens, tree_len)
+        ptd_pool_merge(self.buf, self.nbytes, self.B, self.e_max, self.n_cap, parent, tokens,
+                       tree_len, parent.shape[1], dev_status)
+
+    def retrieve(self, last_token, T_max: int):
+        """Returns (parent, tokens, tree_len) of the candidate trees."""
+        _need_gpu(last_token)
+        dev = self.buf.device
+        po = torch.empty((self.B, T_max), dtype=torch.int32, device=dev)
+        to = torch.empty((self.B, T_max), dtype=torch.int32, device=dev)
+        ln = torch.empty(self.B, dtype=torch.int32, device=dev)
+        ptd_pool_retrieve(self.buf, self.nbytes, self.B, self.e_max, self.n_cap, last_token,
+                          T_max, po, to, ln)
+        return po, to, ln
