@@ -53,7 +53,8 @@ def _load():
     lib.oracle_pool_free.restype = None
     lib.oracle_pool_merge.argtypes = [vp, vp, vp, vp, i, i]
     lib.oracle_pool_retrieve.argtypes = [vp, vp, i, i, vp, vp, vp]
-    for f in ("oracle_step_prune", "oracle_pool_merge", "oracle_pool_retrieve",
+    lib.oracle_gather_pages.argtypes = [vp, i, vp, i, i, i, i, i, i, vp]
+    for f in ("oracle_gather_pages", "oracle_step_prune", "oracle_pool_merge", "oracle_pool_retrieve",
               "oracle_verify_sample", "oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
               "oracle_topk", "oracle_verify", "oracle_expand", "oracle_tree_rope",
               "oracle_kv_commit"):
@@ -77,7 +78,7 @@ def _c(a, dt):
 def _check(st: int):
     if st != 0:
         raise OracleError({2: "bad sizes", 7: "malformed tree", 8: "kv_len out of range",
-                           9: "malformed accepted path"}.get(st, st))
+                           9: "malformed accepted path", 10: "page id out of range"}.get(st, st))
 
 
 def _dtype_code(arr: np.ndarray) -> int:
@@ -316,3 +317,19 @@ class Pool:
         _check(self._lib.oracle_pool_retrieve(self._h, _p(lt), self.B, int(T_max), _p(po),
                                               _p(to), _p(ln)))
         return po, to, ln
+
+
+def gather_pages(pages, page_table, page_size: int):
+    """Paged cache pages [num_pages][Hkv][page_size][D] (bf16 bits or fp32)
+    and page_table int32 [B][max_pages] -> the contiguous cache
+    [B][Hkv][max_pages * page_size][D]."""
+    pages = np.ascontiguousarray(pages)
+    pt = _c(page_table, np.int32)
+    num_pages, Hkv, ps, D = pages.shape
+    if ps != page_size:
+        raise ValueError("pages' second-to-last axis is the page size")
+    B, max_pages = pt.shape
+    cache = np.zeros((B, Hkv, max_pages * page_size, D), pages.dtype)
+    _check(_load().oracle_gather_pages(_p(pages), _dtype_code(pages), _p(pt), B, Hkv, D,
+                                       page_size, max_pages, num_pages, _p(cache)))
+    return cache

@@ -816,3 +816,34 @@ int oracle_pool_retrieve(void* pool, const int32_t* last_token, int B, int T_max
   free(order); free(outid);
   return ORC_OK;
 }
+
+/* ---------------------------------------------------------------------------
+ * Paged key/value caches: a storage layout of the committed cache and the
+ * tree rows (the attention they feed is oracle_tree_attention's).  Row r of
+ * sequence b and KV head g is row r % page_size of page
+ * page_table[b][r / page_size]:
+ *     cache[b][g][r][:] = pages[page_table[b][r / page_size]][g][r % page_size][:]
+ * for r < max_pages * page_size.  Elements are copied as they are (dtype
+ * only sets their size: 1 = bf16, 0 = fp32).  Returns 10 if a page id is
+ * outside [0, num_pages) (that row is left zero).
+ * ------------------------------------------------------------------------- */
+int oracle_gather_pages(const void* pages, int dtype, const int32_t* page_table, int B, int Hkv,
+                        int D, int page_size, int max_pages, int num_pages, void* cache) {
+  if (B < 1 || Hkv < 1 || D < 1 || page_size < 1 || max_pages < 1 || num_pages < 1)
+    return ORC_BAD_SIZE;
+  const size_t es = dtype == 1 ? 2 : 4;
+  const size_t row = es * (size_t)D;
+  const size_t L = (size_t)max_pages * page_size;
+  int status = ORC_OK;
+  memset(cache, 0, row * L * (size_t)Hkv * (size_t)B);
+  for (int b = 0; b < B; ++b)
+    for (int g = 0; g < Hkv; ++g)
+      for (size_t r = 0; r < L; ++r) {
+        const int pg = page_table[(size_t)b * max_pages + r / (size_t)page_size];
+        if (pg < 0 || pg >= num_pages) { status = 10; continue; }
+        const size_t src = (((size_t)pg * Hkv + g) * page_size + r % (size_t)page_size) * row;
+        const size_t dst = (((size_t)b * Hkv + g) * L + r) * row;
+        memcpy((char*)cache + dst, (const char*)pages + src, row);
+      }
+  return status;
+}

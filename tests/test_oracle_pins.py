@@ -961,3 +961,34 @@ def test_pool_golden():
             assert ln[0] == len(wt), (case, last)
             assert pn[0, :ln[0]].tolist() == wp and tn[0, :ln[0]].tolist() == wt, (case, last)
             assert (pn[0, ln[0]:] == -1).all() and (tn[0, ln[0]:] == -1).all()
+
+
+# ---------------------------------------------------------------------------
+# paged caches
+# ---------------------------------------------------------------------------
+def test_gather_pages_inverts_a_scatter():
+    # scatter a contiguous cache into pages through a random page table (numpy
+    # indexing), then gather it back
+    rng = np.random.default_rng(50)
+    B, Hkv, D, ps, maxp = 3, 2, 8, 32, 5
+    cache = rng.standard_normal((B, Hkv, maxp * ps, D)).astype(np.float32)
+    num_pages = B * maxp + 4
+    perm = rng.permutation(num_pages)[:B * maxp].reshape(B, maxp).astype(np.int32)
+    pages = np.zeros((num_pages, Hkv, ps, D), np.float32)
+    for b in range(B):
+        for j in range(maxp):
+            pages[perm[b, j]] = cache[b, :, j * ps:(j + 1) * ps]
+    assert np.array_equal(O.gather_pages(pages, perm, ps), cache)
+    # bf16 bits are moved as they are
+    bits = W.f32_to_bf16_bits(pages)
+    assert np.array_equal(O.gather_pages(bits, perm, ps), W.f32_to_bf16_bits(cache))
+
+
+def test_gather_pages_identity_table_is_the_page_layout():
+    rng = np.random.default_rng(51)
+    Hkv, D, ps, maxp = 2, 4, 32, 3
+    pages = rng.standard_normal((maxp, Hkv, ps, D)).astype(np.float32)
+    got = O.gather_pages(pages, np.arange(maxp, dtype=np.int32)[None], ps)
+    assert np.array_equal(got[0], pages.transpose(1, 0, 2, 3).reshape(Hkv, maxp * ps, D))
+    with pytest.raises(O.OracleError):
+        O.gather_pages(pages, np.array([[0, 1, 3]], np.int32), ps)
