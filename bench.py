@@ -248,6 +248,32 @@ def main():
         P.ptd_pool_retrieve(pool, pool_bytes, B, pool_e, pool_n, bonus, 64, rt_pn, rt_tn, rt_ln,
                             sp)
 
+    # attention on paged caches: 64-row pages scattered through a random page
+    # table (one table for all rotated sets), same inputs otherwise
+    PS = 64
+    paged_ms = None
+    if w.dtype == "bf16" and w.L_cap % PS == 0:
+        maxp = w.L_cap // PS
+        num_pages = B * maxp
+        gtab = torch.Generator(device="cpu").manual_seed(99)
+        table = torch.randperm(num_pages, generator=gtab).to(torch.int32).view(B, maxp).to(dev)
+
+        def paginate(c):
+            pages = torch.empty((num_pages, w.Hkv, PS, w.D), dtype=c.dtype, device=dev)
+            pages[table.view(-1).long()] = (c.view(B, w.Hkv, maxp, PS, w.D).permute(0, 2, 1, 3, 4)
+                                            .reshape(B * maxp, w.Hkv, PS, w.D))
+            return pages
+
+        paged_sets = [(paginate(st_["k"]), paginate(st_["v"])) for st_ in sets]
+        kvps = [P.KVPages(kp.data_ptr(), vp.data_ptr(), table.data_ptr(), PS, maxp, num_pages)
+                for kp, vp in paged_sets]
+
+        def attention_paged(i):
+            s = sets[i % R]
+            P.ptd_tree_attention_paged(s["q"], kvps[i % R], kv_len, parent, T, out, shape, None,
+                                       ws_attn, ws_attn.numel(), status, sp)
+
+        paged_ms, _ = timed(attention_paged, K)
     sample_ms, _ = timed(sample, K)
     if small_tree:
         prune_ms, _ = timed(prune, K)
@@ -335,6 +361,11 @@ def main():
                                       % (B * (T + 1), K)),
         },
     }
+    if paged_ms is not None:
+        line["next_rows"]["paged_attention"] = next_row(
+            paged_ms, alg["attention"], "ptd_tree_attention_paged: the attention call on %d-row "
+            "pages through a random page table (%d pages), %d back-to-back calls; contiguous: "
+            "%.3f us" % (PS, num_pages, K, att_avg_s * 1e6))
     if small_tree:
         tree_b = B * w.T_max * 4 * 2
         line["next_rows"].update({

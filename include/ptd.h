@@ -8,6 +8,7 @@
  *
  *   ptd_build_tree_mask  ancestor-or-self bitmasks and depths of the tree
  *   ptd_tree_attention   tree-masked attention over committed KV + ancestors
+ *                        (ptd_tree_attention_paged: the same on paged caches)
  *   ptd_topk_argmax      per-row argmax / top-k of the verification logits
  *   ptd_verify           greedy longest accepted path (+ bonus token)
  *   ptd_expand           progressive expansion with top-k children
@@ -66,8 +67,9 @@ typedef enum {
   PTD_ERR_HIP = 6,       /* a HIP runtime call or kernel launch failed */
   PTD_ERR_BAD_TREE = 7,  /* device-detected: parent[i] outside [-1, i) */
   PTD_ERR_KV_LEN = 8,    /* device-detected: kv_len < 0 or kv_len + T > L_cap */
-  PTD_ERR_BAD_PATH = 9   /* device-detected: accepted path not strictly increasing
+  PTD_ERR_BAD_PATH = 9,  /* device-detected: accepted path not strictly increasing
                             node ids in [0, T), or its length outside [0, T] */
+  PTD_ERR_PAGE = 10      /* device-detected: a page id outside [0, num_pages) */
 } ptd_status;
 
 /* Dimension pairs turned together by the rotary embedding. */
@@ -157,6 +159,35 @@ int ptd_tree_attention(const void* q, const void* k_cache, const void* v_cache,
                        size_t workspace_bytes, int32_t* dev_status, void* stream);
 
 /* Workspace bytes ptd_topk_argmax needs (0 on invalid arguments). */
+/* Paged key/value caches (host struct, read during the call only). */
+typedef struct {
+  const void* k_pages;        /* [num_pages][Hkv][page_size][D] in_dtype */
+  const void* v_pages;        /* likewise */
+  const int32_t* page_table;  /* [B][max_pages]: row r of sequence b lives in
+                                 page page_table[b][r / page_size], at
+                                 r % page_size */
+  int32_t page_size;          /* rows per page: a power of two >= 32 */
+  int32_t max_pages;          /* page-table entries per sequence */
+  int32_t num_pages;          /* pages in k_pages / v_pages */
+} ptd_kv_pages;
+
+/*
+ * ptd_tree_attention_paged -- ptd_tree_attention on paged caches: the same
+ * operation, arguments and workspace, with sequence b's cache row r (committed
+ * rows, then tree node i at row kv_len[b] + i) read from page
+ * page_table[b][r / page_size].  shape->L_cap must equal
+ * max_pages * page_size; bf16 inputs only (the MFMA path).  Entries of the
+ * page table past a sequence's kv_len + T rows are not read.  A page id
+ * outside [0, num_pages) is reported and page 0 is read in its place.
+ * dev_status: PTD_ERR_BAD_TREE, PTD_ERR_KV_LEN, PTD_ERR_PAGE.
+ * Errors: as ptd_tree_attention; PTD_ERR_DTYPE for fp32 inputs.
+ */
+int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv, const int32_t* kv_len,
+                             const int32_t* parent, int32_t T, void* out,
+                             const ptd_attn_shape* shape, const uint64_t* mask,
+                             void* workspace, size_t workspace_bytes, int32_t* dev_status,
+                             void* stream);
+
 size_t ptd_topk_workspace_bytes(int32_t R, int32_t V, int32_t k);
 
 /*

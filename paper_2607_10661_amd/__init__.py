@@ -29,7 +29,8 @@ PTD_ROPE_HALF, PTD_ROPE_INTERLEAVED = 0, 1
 PTD_MAX_T, PTD_MAX_K, PTD_MAX_DEPTH = 1024, 16, 64
 STATUS = {0: "PTD_OK", 1: "PTD_ERR_NULL", 2: "PTD_ERR_SHAPE", 3: "PTD_ERR_DTYPE",
           4: "PTD_ERR_ALIGN", 5: "PTD_ERR_WORKSPACE", 6: "PTD_ERR_HIP",
-          7: "PTD_ERR_BAD_TREE", 8: "PTD_ERR_KV_LEN", 9: "PTD_ERR_BAD_PATH"}
+          7: "PTD_ERR_BAD_TREE", 8: "PTD_ERR_KV_LEN", 9: "PTD_ERR_BAD_PATH",
+          10: "PTD_ERR_PAGE"}
 
 
 class PTDError(RuntimeError):
@@ -47,6 +48,13 @@ class AttnShape(ctypes.Structure):
                 ("out_dtype", ctypes.c_int), ("scale", ctypes.c_float)]
 
 
+class KVPages(ctypes.Structure):
+    """ptd_kv_pages"""
+    _fields_ = [("k_pages", ctypes.c_void_p), ("v_pages", ctypes.c_void_p),
+                ("page_table", ctypes.c_void_p), ("page_size", ctypes.c_int32),
+                ("max_pages", ctypes.c_int32), ("num_pages", ctypes.c_int32)]
+
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                       "(hipcc --offload-arch=gfx950)")
@@ -60,6 +68,9 @@ _SIGS = {
     "ptd_tree_attention_workspace_bytes": ([ctypes.POINTER(AttnShape), _i32], _sz),
     "ptd_tree_attention": ([_vp, _vp, _vp, _vp, _vp, _i32, _vp, ctypes.POINTER(AttnShape),
                             _vp, _vp, _sz, _vp, _vp], ctypes.c_int),
+    "ptd_tree_attention_paged": ([_vp, ctypes.POINTER(KVPages), _vp, _vp, _i32, _vp,
+                                  ctypes.POINTER(AttnShape), _vp, _vp, _sz, _vp, _vp],
+                                 ctypes.c_int),
     "ptd_topk_workspace_bytes": ([_i32, _i32, _i32], _sz),
     "ptd_topk_argmax": ([_vp, ctypes.c_int, _i32, _i32, _i64, _i32, _vp, _vp, _vp, _vp,
                          _sz, _vp], ctypes.c_int),
@@ -141,6 +152,16 @@ def ptd_tree_attention(q, k_cache, v_cache, kv_len, parent, T, out, shape: AttnS
                                    _ptr(mask), _ptr(workspace), workspace_bytes,
                                    _ptr(dev_status), _stream(stream)),
            "ptd_tree_attention")
+
+
+def ptd_tree_attention_paged(q, kv: KVPages, kv_len, parent, T, out, shape: AttnShape,
+                             mask=None, workspace=None, workspace_bytes=0, dev_status=None,
+                             stream=None):
+    _check(_lib.ptd_tree_attention_paged(_ptr(q), ctypes.byref(kv), _ptr(kv_len), _ptr(parent),
+                                         T, _ptr(out), ctypes.byref(shape), _ptr(mask),
+                                         _ptr(workspace), workspace_bytes, _ptr(dev_status),
+                                         _stream(stream)),
+           "ptd_tree_attention_paged")
 
 
 def ptd_topk_workspace_bytes(R: int, V: int, k: int) -> int:
@@ -314,6 +335,30 @@ def tree_attention(q, k_cache, v_cache, kv_len, parent, mask=None, out=None,
     ptd_tree_attention(q, k_cache, v_cache, kv_len, parent, T, out, shape, mask,
                        workspace, 0 if workspace is None else workspace.numel(),
                        dev_status)
+    return out
+
+
+def tree_attention_paged(q, k_pages, v_pages, page_table, kv_len, parent, out=None,
+                         out_dtype=None, scale: float = 0.0, workspace=None, dev_status=None):
+    """k_pages, v_pages [num_pages][Hkv][page_size][D] (bf16), page_table
+    int32 [B][max_pages]; otherwise as tree_attention."""
+    _need_gpu(q, k_pages, v_pages, page_table, kv_len, parent)
+    B, T, Hq, D = q.shape
+    num_pages, Hkv, ps, _ = k_pages.shape
+    max_pages = page_table.shape[1]
+    shape = AttnShape(B, Hq, Hkv, D, max_pages * ps, _dtype_code(q),
+                      _dtype_code(q) if out_dtype is None else
+                      (PTD_BF16 if out_dtype == torch.bfloat16 else PTD_F32), float(scale))
+    if out is None:
+        od = torch.bfloat16 if shape.out_dtype == PTD_BF16 else torch.float32
+        out = torch.empty((B, T, Hq, D), dtype=od, device=q.device)
+    nbytes = ptd_tree_attention_workspace_bytes(shape, T)
+    if workspace is None and nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    kv = KVPages(k_pages.data_ptr(), v_pages.data_ptr(), page_table.data_ptr(), ps, max_pages,
+                 num_pages)
+    ptd_tree_attention_paged(q, kv, kv_len, parent, T, out, shape, None, workspace,
+                             0 if workspace is None else workspace.numel(), dev_status)
     return out
 
 

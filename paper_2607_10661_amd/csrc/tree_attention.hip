@@ -66,6 +66,10 @@ struct AttnParams {
   int32_t* dev_status;
   int B, T, Hq, Hkv, G, M, L_cap, W;
   int splits, passes, rows_per_pass;
+  // paged caches: k and v are [num_pages][Hkv][2^page_shift][D] and row r of
+  // sequence b lives in page page_table[b][r >> page_shift]; null: contiguous
+  const int32_t* page_table;
+  int page_shift, max_pages, num_pages;
   float scale;  // softmax scale
   float c;      // scale * log2(e)
   int out_bf16;
@@ -196,10 +200,22 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   const int end = min(N, start + csz);
   if (start >= end) return;  // empty split: the combine skips it
 
+  const bool paged = p.page_table != nullptr;  // uniform
   const uint16_t* kbase = static_cast<const uint16_t*>(p.k) +
-                          (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D;
+                          (paged ? 0 : (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D);
   const uint16_t* vbase = static_cast<const uint16_t*>(p.v) +
-                          (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D;
+                          (paged ? 0 : (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D);
+  // paged: the split's first 256 page ids, one per lane and register, loaded
+  // untracked ahead of the query rows
+  const int first_page = paged ? (start >> p.page_shift) : 0;
+  u32x4 pg = {0u, 0u, 0u, 0u};
+  if (paged) {
+    const int npg = ((end - 1) >> p.page_shift) - first_page + 1;
+    const int32_t* pt = p.page_table + static_cast<size_t>(b) * p.max_pages + first_page;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (r * PTD_WAVE + lane < npg) pg[r] = ptd::gload4(pt + r * PTD_WAVE + lane);
+  }
   const int pr0 = pass * p.rows_per_pass;
   const int rowbase = pr0 + wr * 16 * QB;
   const bool wave_live = rowbase < p.M;  // padding waves only copy and sync
@@ -215,6 +231,19 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
                           ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D + 8 * l4;
 #pragma unroll
     for (int db = 0; db < DB; ++db) qraw[qb][db] = gload16(src + 32 * db);
+  }
+  if (paged) {  // the page ids (issued before the query rows) are needed by the first copy
+    wait_vmcnt_le(QB * DB);
+    reg_fence(pg);
+    const int npg = ((end - 1) >> p.page_shift) - first_page + 1;
+    bool bad = false;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool used = r * PTD_WAVE + lane < npg;
+      bad |= used && pg[r] >= static_cast<uint32_t>(p.num_pages);
+      if (!used || pg[r] >= static_cast<uint32_t>(p.num_pages)) pg[r] = 0u;  // read page 0 instead
+    }
+    if (__any(bad) && tid == 0) ptd::report(p.dev_status, PTD_ERR_PAGE);
   }
 
   // ---- sub-tile copies: thread tid moves chunks u*512 + tid of the
@@ -234,12 +263,38 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     cp_voff[u] = static_cast<uint32_t>((cp_row[u] * D + cp_off[u]) * 2);
     cp_lds[u] = static_cast<uint32_t>((u * kThreads + wave * PTD_WAVE) * 16);
   }
+  // element offset of key row `row0` (a multiple of 32): contiguous, or in
+  // its page (a page holds a multiple of 32 rows, so the sub-tile's 32 rows
+  // are consecutive there)
+  auto tile_offset = [&](int row0) __attribute__((always_inline)) -> size_t {
+    if (!paged) return static_cast<size_t>(row0) * D;
+    const int ti = (row0 >> p.page_shift) - first_page;  // uniform
+    uint32_t phys;
+    if (ti < 4 * PTD_WAVE) {
+      const uint32_t v0 = __builtin_amdgcn_readlane(pg[0], ti & 63);
+      const uint32_t v1 = __builtin_amdgcn_readlane(pg[1], ti & 63);
+      const uint32_t v2 = __builtin_amdgcn_readlane(pg[2], ti & 63);
+      const uint32_t v3 = __builtin_amdgcn_readlane(pg[3], ti & 63);
+      const int k = ti >> 6;
+      phys = k == 0 ? v0 : k == 1 ? v1 : k == 2 ? v2 : v3;
+    } else {  // beyond the staged ids: a scalar load (checked the same way)
+      phys = static_cast<uint32_t>(
+          p.page_table[static_cast<size_t>(b) * p.max_pages + (row0 >> p.page_shift)]);
+      if (phys >= static_cast<uint32_t>(p.num_pages)) {
+        if (tid == 0) ptd::report(p.dev_status, PTD_ERR_PAGE);
+        phys = 0u;
+      }
+    }
+    const size_t prow = ((static_cast<size_t>(phys) * p.Hkv + g) << p.page_shift) +
+                        (row0 & ((1 << p.page_shift) - 1));
+    return prow * D;
+  };
   // copy sub-tile t (keys start + 32t ..) into ring slot `slot`
   auto issue = [&](int t, int slot) __attribute__((always_inline)) {
     const uint32_t slot_lds = ring + slot * R::SLOT;
     const int row0 = start + t * R::SUB;
+    const size_t tile = tile_offset(row0);
     if (row0 + R::SUB <= N) {  // whole sub-tile inside the keys: scalar base
-      const size_t tile = static_cast<size_t>(row0) * D;
       if constexpr (R::DPS == 1) {
         dma16_s((cp_v[0] ? vbase : kbase) + tile, cp_voff[0], slot_lds + cp_lds[0]);
       } else {
@@ -252,7 +307,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 #pragma unroll
       for (int u = 0; u < R::DPS; ++u) {
         const int grow = min(row0 + cp_row[u], N - 1);
-        dma16((cp_v[u] ? vbase : kbase) + static_cast<size_t>(grow) * D + cp_off[u],
+        dma16((cp_v[u] ? vbase : kbase) + tile + static_cast<size_t>(grow - row0) * D + cp_off[u],
               slot_lds + cp_lds[u]);
       }
     }
@@ -966,12 +1021,14 @@ extern "C" size_t ptd_tree_attention_workspace_bytes(const ptd_attn_shape* shape
   return pl.total_bytes;
 }
 
-extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void* v_cache,
-                                  const int32_t* kv_len, const int32_t* parent, int32_t T,
-                                  void* out, const ptd_attn_shape* shape,
-                                  const uint64_t* mask, void* workspace,
-                                  size_t workspace_bytes, int32_t* dev_status,
-                                  void* stream) {
+namespace {
+
+// The attention call on contiguous caches (page_table null) or paged ones.
+int attention_impl(const void* q, const void* k_cache, const void* v_cache,
+                   const int32_t* kv_len, const int32_t* parent, int32_t T, void* out,
+                   const ptd_attn_shape* shape, const uint64_t* mask, void* workspace,
+                   size_t workspace_bytes, int32_t* dev_status, void* stream,
+                   const int32_t* page_table, int page_shift, int max_pages, int num_pages) {
   PTD_RETURN_IF(!q || !k_cache || !v_cache || !kv_len || !parent || !out || !shape,
                 PTD_ERR_NULL);
   if (shape->in_dtype != PTD_F32 && shape->in_dtype != PTD_BF16) return PTD_ERR_DTYPE;
@@ -1021,6 +1078,10 @@ extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void
   prm.scale = shape->scale > 0.f ? shape->scale : 1.0f / sqrtf(static_cast<float>(shape->D));
   prm.c = prm.scale * kLog2e;
   prm.out_bf16 = shape->out_dtype == PTD_BF16;
+  prm.page_table = page_table;
+  prm.page_shift = page_shift;
+  prm.max_pages = max_pages;
+  prm.num_pages = num_pages;
   if (pl.splits > 1) {
     const size_t rows = static_cast<size_t>(pl.splits) * prm.B * prm.Hkv * prm.M;
     prm.part_ml = reinterpret_cast<float2*>(prm.part_o + rows * shape->D);
@@ -1041,4 +1102,36 @@ extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void
     else hipLaunchKernelGGL(k_attn_valu<64>, grid, dim3(kValuThreads), 0, st, prm);
   }
   return ptd_launch_status();
+}
+
+}  // namespace
+
+extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void* v_cache,
+                                  const int32_t* kv_len, const int32_t* parent, int32_t T,
+                                  void* out, const ptd_attn_shape* shape,
+                                  const uint64_t* mask, void* workspace,
+                                  size_t workspace_bytes, int32_t* dev_status,
+                                  void* stream) {
+  return attention_impl(q, k_cache, v_cache, kv_len, parent, T, out, shape, mask, workspace,
+                        workspace_bytes, dev_status, stream, nullptr, 0, 0, 0);
+}
+
+extern "C" int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv,
+                                        const int32_t* kv_len, const int32_t* parent, int32_t T,
+                                        void* out, const ptd_attn_shape* shape,
+                                        const uint64_t* mask, void* workspace,
+                                        size_t workspace_bytes, int32_t* dev_status,
+                                        void* stream) {
+  PTD_RETURN_IF(!kv || !shape, PTD_ERR_NULL);
+  PTD_RETURN_IF(!kv->k_pages || !kv->v_pages || !kv->page_table, PTD_ERR_NULL);
+  PTD_RETURN_IF(shape->in_dtype != PTD_BF16, PTD_ERR_DTYPE);  // the MFMA path only
+  const int ps = kv->page_size;
+  PTD_RETURN_IF(ps < 32 || ps > (1 << 20) || (ps & (ps - 1)) != 0, PTD_ERR_SHAPE);
+  PTD_RETURN_IF(kv->max_pages < 1 || kv->num_pages < 1, PTD_ERR_SHAPE);
+  PTD_RETURN_IF(static_cast<long long>(kv->max_pages) * ps != shape->L_cap, PTD_ERR_SHAPE);
+  int shift = 0;
+  while ((1 << shift) < ps) ++shift;
+  return attention_impl(q, kv->k_pages, kv->v_pages, kv_len, parent, T, out, shape, mask,
+                        workspace, workspace_bytes, dev_status, stream, kv->page_table, shift,
+                        kv->max_pages, kv->num_pages);
 }

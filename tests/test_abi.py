@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(0, 10):
+    for code in range(0, 11):
         assert P.ptd_status_string(code) != "unknown status"
     assert P.ptd_status_string(99) == "unknown status"
     assert P.ptd_version() >= 100
@@ -178,3 +178,18 @@ def test_step_prune_and_pool_validation():
     assert _err(P.ptd_pool_merge, FAKE, nb, 2, 16, 8, None, FAKE, None, 8) == 1
     assert _err(P.ptd_pool_retrieve, FAKE, nb, 2, 16, 8, FAKE, 0, FAKE, FAKE, FAKE) == 2
     assert _err(P.ptd_pool_retrieve, FAKE, nb, 2, 16, 100, FAKE, 8, FAKE, FAKE, FAKE) == 2
+
+
+def test_paged_attention_validation():
+    s = _shape(L=2048)
+    kv = P.KVPages(FAKE, FAKE, FAKE, 64, 32, 64)
+    A = P.ptd_tree_attention_paged
+    bad_null = P.KVPages(FAKE, None, FAKE, 64, 32, 64)
+    assert _err(A, FAKE, bad_null, FAKE, FAKE, 64, FAKE, s) == 1
+    f32 = _shape(L=2048, dt=P.PTD_F32, od=P.PTD_F32)
+    assert _err(A, FAKE, kv, FAKE, FAKE, 64, FAKE, f32) == 3            # bf16 only
+    for ps in (16, 48, 96):                                              # power of two >= 32
+        assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, ps, 2048 // ps, 64), FAKE, FAKE, 64,
+                    FAKE, s) == 2
+    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 64, 31, 64), FAKE, FAKE, 64, FAKE, s) == 2
+    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 64, 32, 0), FAKE, FAKE, 64, FAKE, s) == 2
