@@ -11,7 +11,7 @@
 // Kernels
 //   k_topk_row      one workgroup per (row, vocabulary slice), a slice being
 //                   at most 4096 chunks of 16 bytes (32768 bf16 or 16384
-//                   fp32 values) copied into LDS: a cheap lower bound of the
+//                   fp32 values) held in registers: a cheap lower bound of the
 //                   KMAX-th best value leaves a few candidates, ranked by
 //                   counting (details below).
 //   k_topk_scalar   rows that are not 16-byte aligned: one wave per (row,
@@ -132,9 +132,7 @@ __device__ __forceinline__ void store_part(uint64_t* part, int item, int kmax, i
 }
 
 // One workgroup (16 waves) per (row, slice), a slice being at most one batch
-// of 4 chunks of 16 bytes per lane (64 KB), copied asynchronously into LDS
-// at the start.  The workgroup takes under half of a CU's LDS, so two share a
-// CU and each hides the other's memory latency.
+// of 4 chunks of 16 bytes per lane (64 KB), loaded straight into registers.
 //   1. Every lane takes the image of each of its chunks (bf16 images are 16
 //      bits wide and computed two at a time with packed 16-bit integer
 //      operations) and their maximum.
@@ -142,23 +140,25 @@ __device__ __forceinline__ void store_part(uint64_t* part, int item, int kmax, i
 //      wave form KMAX groups; each group's largest lane maximum is a distinct
 //      element, so the least of the KMAX group maxima is at most the KMAX-th
 //      best value.  The bound of the slice is the largest bound of its waves.
-//   3. Chunks whose image reaches tau are listed in LDS (the list holds the
-//      whole slice), then the workgroup examines the listed chunks a thread
-//      per element and appends the elements that reach tau to a candidate
-//      list.  The slice's last partial chunk (fewer than one chunk of
-//      elements) is read with plain loads and checked the same way.
+//   3. Chunks whose image reaches tau are copied with their index to a list
+//      in LDS, then the workgroup examines the listed chunks a thread per
+//      element and appends the elements that reach tau to a candidate list.
+//      The slice's last partial chunk (fewer than one chunk of elements) is
+//      read with plain loads and checked the same way.
 //   4. The candidates are ranked by counting: the list is cut into parts,
 //      each thread counts the keys of one part above one candidate, and the
 //      counts are summed in LDS.  The candidates of rank below k are the
-//      result.  If the list overflows (many values tied at the top), every
-//      lane keeps a sorted list of its best keys among the elements that reach
-//      tau, re-read from memory, and the lists are merged.
-// The kernel's loops stay rolled, which keeps its code small: its
-// instructions are fetched once per CU, cold.
+//      result.  If either list overflows (many values tied at the top), every
+//      lane keeps a sorted list of its best keys among its own elements that
+//      reach tau, and the lists are merged.
+// Only listed chunks pass through LDS, so the slice is read from memory once
+// and LDS carries a few KB.  The kernel's loops stay rolled, which keeps its
+// code small: its instructions are fetched once per CU, cold.
 constexpr int kRowThreads = 1024;
 constexpr int kBatchLoads = 4;                           // chunks per lane
 constexpr int kSliceChunks = kRowThreads * kBatchLoads;  // 64 KB
 constexpr int kCandCap = 256;                            // LDS candidate list
+constexpr int kListCap = 256;                            // LDS chunk list
 
 using s16x2 = short __attribute__((ext_vector_type(2)));
 
@@ -208,6 +208,37 @@ __device__ __forceinline__ uint32_t cmp_bound(uint32_t tau) {
   return (BF16 && tau == kImgPosZeroBf16) ? tau - 1 : tau;
 }
 
+// Cross-lane steps of a wave on the vector ALU, level j pairing lanes that
+// differ in bit j: quad permutes (j = 0, 1), the half-row and row mirrors
+// (j = 2, 3: once the value is uniform over blocks of 2^j lanes, the mirror
+// partner lies in the other block), v_permlane16_swap / v_permlane32_swap
+// (j = 4, 5: with both operands holding the value, the two results are the
+// lane's value and its partner's).
+template <bool MAX, int J>
+__device__ __forceinline__ uint32_t lane_step(uint32_t x) {
+  constexpr int kCtrl[4] = {0xB1, 0x4E, 0x141, 0x140};  // quad_perm 1032, 2301, half-row, row mirror
+  if constexpr (J < 4) {
+    const uint32_t y = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(static_cast<int>(x), static_cast<int>(x), kCtrl[J], 0xF, 0xF, false));
+    return MAX ? max(x, y) : min(x, y);
+  } else {
+    const auto r = J == 4 ? __builtin_amdgcn_permlane16_swap(x, x, false, false)
+                          : __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return MAX ? max(r[0], r[1]) : min(r[0], r[1]);
+  }
+}
+// Maximum over aligned groups of GL lanes, then minimum over the groups.
+template <int GL>
+__device__ __forceinline__ uint32_t group_max_min(uint32_t x) {
+  if constexpr (GL > 1) x = lane_step<true, 0>(x); else x = lane_step<false, 0>(x);
+  if constexpr (GL > 2) x = lane_step<true, 1>(x); else x = lane_step<false, 1>(x);
+  if constexpr (GL > 4) x = lane_step<true, 2>(x); else x = lane_step<false, 2>(x);
+  if constexpr (GL > 8) x = lane_step<true, 3>(x); else x = lane_step<false, 3>(x);
+  if constexpr (GL > 16) x = lane_step<true, 4>(x); else x = lane_step<false, 4>(x);
+  if constexpr (GL > 32) x = lane_step<true, 5>(x); else x = lane_step<false, 5>(x);
+  return x;
+}
+
 template <int KMAX, bool BF16>
 __global__ void __launch_bounds__(kRowThreads)
 k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int slice_len,
@@ -217,12 +248,12 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   constexpr int ES = BF16 ? 2 : 4;
   constexpr int NW = kRowThreads / PTD_WAVE;
   constexpr int GL = PTD_WAVE / KMAX;  // lanes per group
-  __shared__ __attribute__((aligned(16))) uint4 s_buf[kSliceChunks];
+  __shared__ __attribute__((aligned(16))) uint4 s_ldata[kListCap];
   __shared__ uint64_t s_cand[kCandCap];
   __shared__ uint32_t s_bits[kCandCap];
   __shared__ uint32_t s_rank[kCandCap];
-  __shared__ uint16_t s_list[kSliceChunks];
-  __shared__ uint32_t s_tau[NW];
+  __shared__ uint16_t s_list[kListCap];
+  __shared__ __attribute__((aligned(16))) uint32_t s_tau[NW];
   __shared__ int s_nlist, s_cnt;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -235,15 +266,16 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   const int vt = v0 + nfull * E + tid;  // the last partial chunk, one element per lane
   const bool tail = vt < v1;
 
-  // Every lane copies its kBatchLoads chunks (past the end: the slice's last
-  // chunk, never examined); chunk u of a lane is u * kRowThreads + tid.
+  // Chunk u of a lane is u * kRowThreads + tid (past the end: the slice's
+  // last chunk, never examined); all loads are issued before any wait.
+  uint4 cw[kBatchLoads];
   if (nfull > 0) {
-    const uint32_t lds = ptd::lds_addr(s_buf) + wave * PTD_WAVE * 16;
+    const uint4* src = reinterpret_cast<const uint4*>(sb);
 #pragma unroll
-    for (int u = 0; u < kBatchLoads; ++u) {
-      const int j = min(u * kRowThreads + tid, nfull - 1);
-      ptd::dma16_s(sb, static_cast<uint32_t>(j) * 16u, lds + u * kRowThreads * 16);
-    }
+    for (int u = 0; u < kBatchLoads; ++u) cw[u] = src[min(u * kRowThreads + tid, nfull - 1)];
+  } else {
+#pragma unroll
+    for (int u = 0; u < kBatchLoads; ++u) cw[u] = make_uint4(0u, 0u, 0u, 0u);
   }
   const uint32_t bt = tail ? elem_bits<BF16>(rb, vt) : 0u;
   if (tid < kCandCap) s_rank[tid] = 0;
@@ -251,29 +283,25 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
     s_cnt = 0;
     s_nlist = 0;
   }
-  ptd::wait_vmcnt<0>();
-  ptd::lds_barrier();  // the slice landed for every wave
 
   // 1. chunk images and the lane maximum
   uint32_t cm[kBatchLoads];
   uint32_t lm = tail ? elem_img<BF16>(bt) : 0u;
 #pragma unroll
   for (int u = 0; u < kBatchLoads; ++u) {
-    const int c = u * kRowThreads + tid;
-    cm[u] = c < nfull ? chunk_img<BF16>(s_buf[c]) : 0u;
+    cm[u] = u * kRowThreads + tid < nfull ? chunk_img<BF16>(cw[u]) : 0u;
     lm = max(lm, cm[u]);
   }
   // 2. the bound: max over the lane groups, then min over the groups
-  uint32_t g = lm;
-#pragma unroll
-  for (int o = 1; o < GL; o <<= 1) g = max(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
-#pragma unroll
-  for (int o = GL; o < PTD_WAVE; o <<= 1) g = min(g, static_cast<uint32_t>(__shfl_xor(static_cast<int>(g), o, PTD_WAVE)));
+  const uint32_t g = group_max_min<GL>(lm);
   if (lane == 0) s_tau[wave] = g;
   ptd::lds_barrier();
   uint32_t tau = 0;
 #pragma unroll
-  for (int i = 0; i < NW; ++i) tau = max(tau, s_tau[i]);
+  for (int i = 0; i < NW; i += 4) {
+    const uint4 t4 = *reinterpret_cast<const uint4*>(s_tau + i);
+    tau = max(max(tau, max(t4.x, t4.y)), max(t4.z, t4.w));
+  }
   const uint32_t tc = cmp_bound<BF16>(tau);
 
   // 3. list the chunks that reach the bound, then examine them
@@ -288,26 +316,31 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   for (int u = 0; u < kBatchLoads; ++u) {
     if (cm[u] != 0 && cm[u] >= tc) {
       const int pos = atomicAdd(&s_nlist, 1);
-      s_list[pos] = static_cast<uint16_t>(u * kRowThreads + tid);
+      if (pos < kListCap) {
+        s_ldata[pos] = cw[u];
+        s_list[pos] = static_cast<uint16_t>(u * kRowThreads + tid);
+      }
     }
   }
   if (tail && elem_img<BF16>(bt) >= tc) append(bt, vt);
   ptd::lds_barrier();
   const int nl = s_nlist;
-  for (int i0 = 0; i0 < nl; i0 += kRowThreads / E) {
-    const int i = i0 + tid / E;
-    if (i < nl) {
-      const int c = s_list[i], e = tid & (E - 1);
-      const uint32_t bits = BF16 ? static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(s_buf + c)[e]) << 16
-                                 : reinterpret_cast<const uint32_t*>(s_buf + c)[e];
-      if (elem_img<BF16>(bits) >= tc) append(bits, v0 + c * E + e);
+  if (nl <= kListCap) {  // uniform
+    for (int i0 = 0; i0 < nl; i0 += kRowThreads / E) {
+      const int i = i0 + tid / E;
+      if (i < nl) {
+        const int c = s_list[i], e = tid & (E - 1);
+        const uint32_t bits = BF16 ? static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(s_ldata + i)[e]) << 16
+                                   : reinterpret_cast<const uint32_t*>(s_ldata + i)[e];
+        if (elem_img<BF16>(bits) >= tc) append(bits, v0 + c * E + e);
+      }
     }
   }
   __syncthreads();
   const int n = s_cnt;
 
   // 4. selection
-  if (n <= kCandCap) {  // uniform over the workgroup
+  if (nl <= kListCap && n <= kCandCap) {  // uniform over the workgroup
     int n2 = PTD_WAVE;  // candidates per part-set: a power of two >= n
     while (n2 < n) n2 <<= 1;
     const int parts = kRowThreads / n2;
@@ -342,18 +375,21 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
     return;
   }
 
-  // overflow: per-lane sorted lists of the slice's elements that reach tau
+  // overflow: per-lane sorted lists of the lane's own elements that reach tau
   uint64_t l[KMAX];
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) l[j] = 0;
-  for (int c = tid; c < nfull; c += kRowThreads) {
-    const uint4 w = s_buf[c];
-    const int v = v0 + c * E;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const uint32_t bits = chunk_bits<BF16>(w, e);
-      const uint64_t key = make_key(bits, static_cast<uint32_t>(v + e));
-      if (elem_img<BF16>(bits) >= tc && key > l[KMAX - 1]) insert<KMAX>(l, key);
+  for (int u = 0; u < kBatchLoads; ++u) {
+    const int c = u * kRowThreads + tid;
+    if (c < nfull) {
+      const int v = v0 + c * E;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t bits = chunk_bits<BF16>(cw[u], e);
+        const uint64_t key = make_key(bits, static_cast<uint32_t>(v + e));
+        if (elem_img<BF16>(bits) >= tc && key > l[KMAX - 1]) insert<KMAX>(l, key);
+      }
     }
   }
   if (tail) {
