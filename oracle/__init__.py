@@ -34,9 +34,9 @@ def _load():
     lib = ctypes.CDLL(LIB_PATH)
     vp, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
     lib.oracle_tree_mask.argtypes = [vp, vp, i, i, vp, vp]
-    lib.oracle_attention_row.argtypes = [vp, vp, vp, i, vp, vp, i, i, i, i, i, i,
+    lib.oracle_attention_row.argtypes = [vp, vp, vp, i, vp, vp, vp, i, i, i, i, i, i,
                                          d, i, i, i, vp]
-    lib.oracle_tree_attention.argtypes = [vp, vp, vp, i, vp, vp, i, i, i, i, i, i,
+    lib.oracle_tree_attention.argtypes = [vp, vp, vp, i, vp, vp, vp, i, i, i, i, i, i,
                                           d, vp]
     lib.oracle_topk.argtypes = [vp, i, i, i, ctypes.c_longlong, i, vp, vp, vp]
     lib.oracle_verify.argtypes = [vp, vp, vp, vp, i, i, vp, vp, vp]
@@ -114,27 +114,32 @@ def _attn_args(q, k_cache, v_cache, kv_len, parent):
             B, T, Hq, Hkv, D, L_cap)
 
 
-def tree_attention(q, k_cache, v_cache, kv_len, parent, scale: float) -> np.ndarray:
-    """All outputs [B][T][Hq][D] in float64."""
+def tree_attention(q, k_cache, v_cache, kv_len, parent, scale: float,
+                   tree_len=None) -> np.ndarray:
+    """All outputs [B][T][Hq][D] in float64.  tree_len [B] (optional): nodes
+    at index >= tree_len[b] are padding with zero outputs."""
     q, kc, vc, dt, kvl, par, B, T, Hq, Hkv, D, L = _attn_args(
         q, k_cache, v_cache, kv_len, parent)
+    tl = None if tree_len is None else _c(tree_len, np.int32)
     out = np.zeros((B, T, Hq, D), np.float64)
     _check(_load().oracle_tree_attention(_p(q), _p(kc), _p(vc), dt, _p(kvl),
-                                         _p(par), B, T, Hq, Hkv, D, L,
-                                         float(scale), _p(out)))
+                                         _p(par), None if tl is None else _p(tl),
+                                         B, T, Hq, Hkv, D, L, float(scale), _p(out)))
     return out
 
 
-def attention_rows(q, k_cache, v_cache, kv_len, parent, scale: float, rows):
+def attention_rows(q, k_cache, v_cache, kv_len, parent, scale: float, rows,
+                   tree_len=None):
     """Selected outputs: rows is a list of (b, h, i); returns [len(rows)][D]."""
     q, kc, vc, dt, kvl, par, B, T, Hq, Hkv, D, L = _attn_args(
         q, k_cache, v_cache, kv_len, parent)
+    tl = None if tree_len is None else _c(tree_len, np.int32)
     lib = _load()
     out = np.zeros((len(rows), D), np.float64)
     for n, (b, h, i) in enumerate(rows):
         _check(lib.oracle_attention_row(
-            _p(q), _p(kc), _p(vc), dt, _p(kvl), _p(par), B, T, Hq, Hkv, D, L,
-            float(scale), int(b), int(h), int(i),
+            _p(q), _p(kc), _p(vc), dt, _p(kvl), _p(par), None if tl is None else _p(tl),
+            B, T, Hq, Hkv, D, L, float(scale), int(b), int(h), int(i),
             out[n].ctypes.data_as(ctypes.c_void_p)))
     return out
 

@@ -104,18 +104,28 @@ int oracle_tree_mask(const int32_t* parent, const int32_t* tree_len, int B, int 
  *   s_j = scale * <q, k_j>;  m = max_j s_j;  p_j = exp(s_j - m);
  *   out = sum_j p_j v_j / sum_j p_j.
  * Layouts: q [B][T][Hq][D], caches [B][Hkv][L_cap][D], out row of D doubles.
+ * tree_len (NULL: every node live) gives each sequence its own tree size
+ * n_b = clamp(tree_len[b], 0, T) inside the padded batch: nodes at index
+ * >= n_b are padding, whose parents, queries and cache rows are not read,
+ * and whose outputs are zero.  Only n_b cache rows follow the committed ones.
  * ------------------------------------------------------------------------- */
 int oracle_attention_row(const void* q, const void* k_cache, const void* v_cache,
                          int dtype, const int32_t* kv_len, const int32_t* parent,
-                         int B, int T, int Hq, int Hkv, int D, int L_cap,
-                         double scale, int b, int h, int i, double* out) {
+                         const int32_t* tree_len, int B, int T, int Hq, int Hkv, int D,
+                         int L_cap, double scale, int b, int h, int i, double* out) {
   if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= T || Hkv <= 0 ||
       Hq % Hkv)
     return ORC_BAD_SIZE;
+  int nt = T;
+  if (tree_len) nt = tree_len[b] < 0 ? 0 : (tree_len[b] > T ? T : tree_len[b]);
   const int32_t* par = parent + (size_t)b * T;
-  if (!tree_is_valid(par, T)) return ORC_BAD_TREE;
+  if (!tree_is_valid(par, nt)) return ORC_BAD_TREE;
   const int n = kv_len[b];
-  if (n < 0 || n + T > L_cap) return ORC_BAD_SIZE;
+  if (n < 0 || n + nt > L_cap) return ORC_BAD_SIZE;
+  if (i >= nt) {  /* padding node */
+    for (int d = 0; d < D; ++d) out[d] = 0.0;
+    return ORC_OK;
+  }
   const int g = h / (Hq / Hkv);
 
   /* the key rows node i may see */
@@ -159,12 +169,12 @@ int oracle_attention_row(const void* q, const void* k_cache, const void* v_cache
 /* All rows; out is [B][T][Hq][D] doubles. */
 int oracle_tree_attention(const void* q, const void* k_cache, const void* v_cache,
                           int dtype, const int32_t* kv_len, const int32_t* parent,
-                          int B, int T, int Hq, int Hkv, int D, int L_cap,
-                          double scale, double* out) {
+                          const int32_t* tree_len, int B, int T, int Hq, int Hkv, int D,
+                          int L_cap, double scale, double* out) {
   for (int b = 0; b < B; ++b)
     for (int i = 0; i < T; ++i)
       for (int h = 0; h < Hq; ++h) {
-        int st = oracle_attention_row(q, k_cache, v_cache, dtype, kv_len, parent,
+        int st = oracle_attention_row(q, k_cache, v_cache, dtype, kv_len, parent, tree_len,
                                       B, T, Hq, Hkv, D, L_cap, scale, b, h, i,
                                       out + (((size_t)b * T + i) * Hq + h) * D);
         if (st) return st;

@@ -210,6 +210,64 @@ def test_attention_rows_match_full():
         assert np.array_equal(part[n], full[b, i, h])
 
 
+def _ancestor_rows(par, n, i):
+    rows, a = [], i
+    while a != -1:
+        rows.append(n + a)
+        a = int(par[a])
+    return list(range(n)) + sorted(rows)
+
+
+def test_attention_tree_len_live_rows_are_decode_and_padding_is_ignored():
+    # a padded batch of trees of sizes 10, 4, 0 and 7: every live node sees its
+    # prefix and ancestors (plain SDPA over that key set), padding rows are zero,
+    # and garbage in the padding (parents, queries, cache rows) changes nothing
+    T = 10
+    w = W.make_workload(_spec(B=4, Hq=4, Hkv=2, T=T, kv_len=[5, 0, 12, 3]), seed=9)
+    tl = np.array([10, 4, 0, 7], np.int32)
+    q = w.q.copy()
+    kc, vc = w.k_cache.copy(), w.v_cache.copy()
+    par = w.parent.copy()
+    for b in range(w.B):
+        n = int(w.kv_len[b])
+        q[b, tl[b]:] = 1e6
+        kc[b, :, n + tl[b]:] = -1e6
+        vc[b, :, n + tl[b]:] = 1e6
+        par[b, tl[b]:] = [99, -7, 3][b % 3] if tl[b] < T else par[b, tl[b]:]
+    out = O.tree_attention(q, kc, vc, w.kv_len, par, w.scale, tree_len=tl)
+    clean = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    qf, kf, vf = (W.to_f64(x, w.dtype) for x in (w.q, w.k_cache, w.v_cache))
+    G = w.Hq // w.Hkv
+    for b in range(w.B):
+        n = int(w.kv_len[b])
+        assert np.all(out[b, tl[b]:] == 0.0)
+        for i in range(tl[b]):
+            rows = _ancestor_rows(w.parent[b], n, i)
+            for h in range(w.Hq):
+                ref = _sdpa_one(qf[b, i, h], kf[b, h // G, rows], vf[b, h // G, rows], w.scale)
+                np.testing.assert_allclose(out[b, i, h], ref, rtol=0, atol=1e-12)
+            # a live node's result does not depend on the tree's size
+            assert np.array_equal(out[b, i], clean[b, i])
+
+
+def test_attention_tree_len_full_is_no_tree_len_and_cache_may_end_at_the_tree():
+    w = W.make_workload(_spec(B=2, T=8, kv_len=[6, 2]), seed=10)
+    full = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    same = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale,
+                            tree_len=np.array([8, 8], np.int32))
+    assert np.array_equal(full, same)
+    # sizes 3 and 5: the cache needs only kv_len + tree_len rows
+    tl = np.array([3, 5], np.int32)
+    L = int((w.kv_len + tl).max())
+    out = O.tree_attention(w.q, w.k_cache[:, :, :L], w.v_cache[:, :, :L], w.kv_len, w.parent,
+                           w.scale, tree_len=tl)
+    for b in range(2):
+        assert np.array_equal(out[b, :tl[b]], full[b, :tl[b]])
+    with pytest.raises(RuntimeError):
+        O.tree_attention(w.q, w.k_cache[:, :, :L], w.v_cache[:, :, :L], w.kv_len, w.parent,
+                         w.scale)
+
+
 # ---------------------------------------------------------------------------
 # top-k / argmax
 # ---------------------------------------------------------------------------
