@@ -270,10 +270,23 @@ def main():
 
         def attention_paged(i):
             s = sets[i % R]
-            P.ptd_tree_attention_paged(s["q"], kvps[i % R], kv_len, parent, T, out, shape, None,
+            P.ptd_tree_attention_paged(s["q"], kvps[i % R], kv_len, None, parent, T, out, shape, None,
                                        ws_attn, ws_attn.numel(), status, sp)
 
         paged_ms, _ = timed(attention_paged, K)
+
+    # a padded batch of trees of different sizes: per-sequence tree sizes drawn
+    # uniformly from 1..T (seeded), the rest of each sequence's T slots padding
+    gtl = torch.Generator(device="cpu").manual_seed(98)
+    tree_len_r = torch.randint(1, T + 1, (B,), generator=gtl, dtype=torch.int32)
+    tree_len_d = tree_len_r.to(dev)
+
+    def attention_ragged(i):
+        s = sets[i % R]
+        P.ptd_tree_attention_ragged(s["q"], s["k"], s["v"], kv_len, tree_len_d, parent, T, out,
+                                    shape, None, ws_attn, ws_attn.numel(), status, sp)
+
+    ragged_ms, _ = timed(attention_ragged, K)
     sample_ms, _ = timed(sample, K)
     if small_tree:
         prune_ms, _ = timed(prune, K)
@@ -361,6 +374,10 @@ def main():
                                       % (B * (T + 1), K)),
         },
     }
+    line["next_rows"]["ragged_attention"] = next_row(
+        ragged_ms, W.ragged_attention_bytes(w, tree_len_r.numpy()),
+        "ptd_tree_attention_ragged: per-sequence tree sizes %s of T = %d slots, %d back-to-back "
+        "calls" % (tree_len_r.tolist() if B <= 16 else "1..%d" % T, T, K))
     if paged_ms is not None:
         line["next_rows"]["paged_attention"] = next_row(
             paged_ms, alg["attention"], "ptd_tree_attention_paged: the attention call on %d-row "

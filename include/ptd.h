@@ -8,7 +8,9 @@
  *
  *   ptd_build_tree_mask  ancestor-or-self bitmasks and depths of the tree
  *   ptd_tree_attention   tree-masked attention over committed KV + ancestors
- *                        (ptd_tree_attention_paged: the same on paged caches)
+ *                        (ptd_tree_attention_ragged: trees of different sizes
+ *                        in one padded batch; ptd_tree_attention_paged: the
+ *                        same on paged caches)
  *   ptd_topk_argmax      per-row argmax / top-k of the verification logits
  *   ptd_verify           greedy longest accepted path (+ bonus token)
  *   ptd_expand           progressive expansion with top-k children
@@ -121,6 +123,7 @@ int ptd_build_tree_mask(const int32_t* parent, const int32_t* tree_len, int32_t 
  * (split-KV partial results, plus room for the masks when they are read from
  * memory -- fp32 inputs, or T > 128 -- and mask == NULL).  The workspace needs
  * no initialisation; calls sharing one workspace must not overlap.
+ * shape->L_cap may be below T (for ptd_tree_attention_ragged).
  * Returns 0 on invalid arguments.
  */
 size_t ptd_tree_attention_workspace_bytes(const ptd_attn_shape* shape, int32_t T);
@@ -136,6 +139,7 @@ size_t ptd_tree_attention_workspace_bytes(const ptd_attn_shape* shape, int32_t T
  *   k_cache  [B][Hkv][L_cap][D]      in_dtype; tree node i's key is row kv_len[b]+i
  *   v_cache  [B][Hkv][L_cap][D]      in_dtype; likewise
  *   kv_len   int32 [B]               committed length; needs kv_len+T <= L_cap
+ *                                    (L_cap < T is rejected up front)
  *   parent   int32 [B][T]            tree (all T nodes live)
  *   T        nodes per sequence, 1 .. PTD_MAX_T
  *   out      [B][T][Hq][D]           out_dtype (fp32 accumulation inside)
@@ -158,6 +162,27 @@ int ptd_tree_attention(const void* q, const void* k_cache, const void* v_cache,
                        const uint64_t* mask, void* workspace,
                        size_t workspace_bytes, int32_t* dev_status, void* stream);
 
+/*
+ * ptd_tree_attention_ragged -- ptd_tree_attention over a padded batch of
+ * trees of different sizes (the attention of Sec. 3.1, with a batch of
+ * sequences that each carry their own draft tree, as a server holds them):
+ *   tree_len  int32 [B] device, or NULL (all T nodes live).  Sequence b has
+ *             n_b = min(max(tree_len[b], 0), T) live nodes 0 .. n_b-1; the
+ *             slots n_b .. T-1 are padding.
+ * Live node i attends exactly as in ptd_tree_attention (its ancestors are
+ * live nodes); the rows of padding nodes in out are zero.  Parents, queries
+ * and cache rows of padding nodes are not read, and a sequence's cache needs
+ * only kv_len[b] + n_b <= L_cap rows.  mask (if given) must come from
+ * ptd_build_tree_mask with the same tree_len.  Other arguments, workspace,
+ * dev_status and errors as ptd_tree_attention.
+ */
+int ptd_tree_attention_ragged(const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* kv_len, const int32_t* tree_len,
+                              const int32_t* parent, int32_t T, void* out,
+                              const ptd_attn_shape* shape, const uint64_t* mask,
+                              void* workspace, size_t workspace_bytes,
+                              int32_t* dev_status, void* stream);
+
 /* Workspace bytes ptd_topk_argmax needs (0 on invalid arguments). */
 /* Paged key/value caches (host struct, read during the call only). */
 typedef struct {
@@ -172,18 +197,19 @@ typedef struct {
 } ptd_kv_pages;
 
 /*
- * ptd_tree_attention_paged -- ptd_tree_attention on paged caches: the same
- * operation, arguments and workspace, with sequence b's cache row r (committed
- * rows, then tree node i at row kv_len[b] + i) read from page
- * page_table[b][r / page_size].  shape->L_cap must equal
- * max_pages * page_size; bf16 inputs only (the MFMA path).  Entries of the
- * page table past a sequence's kv_len + T rows are not read.  A page id
- * outside [0, num_pages) is reported and page 0 is read in its place.
+ * ptd_tree_attention_paged -- ptd_tree_attention_ragged on paged caches: the
+ * same operation, arguments and workspace (tree_len may be NULL), with
+ * sequence b's cache row r (committed rows, then tree node i at row
+ * kv_len[b] + i) read from page page_table[b][r / page_size].  shape->L_cap
+ * must equal max_pages * page_size; bf16 inputs only (the MFMA path).
+ * Entries of the page table past a sequence's kv_len + n_b rows are not read.
+ * A page id outside [0, num_pages) is reported and page 0 is read in its
+ * place.
  * dev_status: PTD_ERR_BAD_TREE, PTD_ERR_KV_LEN, PTD_ERR_PAGE.
  * Errors: as ptd_tree_attention; PTD_ERR_DTYPE for fp32 inputs.
  */
 int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv, const int32_t* kv_len,
-                             const int32_t* parent, int32_t T, void* out,
+                             const int32_t* tree_len, const int32_t* parent, int32_t T, void* out,
                              const ptd_attn_shape* shape, const uint64_t* mask,
                              void* workspace, size_t workspace_bytes, int32_t* dev_status,
                              void* stream);

@@ -68,7 +68,10 @@ _SIGS = {
     "ptd_tree_attention_workspace_bytes": ([ctypes.POINTER(AttnShape), _i32], _sz),
     "ptd_tree_attention": ([_vp, _vp, _vp, _vp, _vp, _i32, _vp, ctypes.POINTER(AttnShape),
                             _vp, _vp, _sz, _vp, _vp], ctypes.c_int),
-    "ptd_tree_attention_paged": ([_vp, ctypes.POINTER(KVPages), _vp, _vp, _i32, _vp,
+    "ptd_tree_attention_ragged": ([_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp,
+                                   ctypes.POINTER(AttnShape), _vp, _vp, _sz, _vp, _vp],
+                                  ctypes.c_int),
+    "ptd_tree_attention_paged": ([_vp, ctypes.POINTER(KVPages), _vp, _vp, _vp, _i32, _vp,
                                   ctypes.POINTER(AttnShape), _vp, _vp, _sz, _vp, _vp],
                                  ctypes.c_int),
     "ptd_topk_workspace_bytes": ([_i32, _i32, _i32], _sz),
@@ -154,13 +157,23 @@ def ptd_tree_attention(q, k_cache, v_cache, kv_len, parent, T, out, shape: AttnS
            "ptd_tree_attention")
 
 
-def ptd_tree_attention_paged(q, kv: KVPages, kv_len, parent, T, out, shape: AttnShape,
+def ptd_tree_attention_ragged(q, k_cache, v_cache, kv_len, tree_len, parent, T, out,
+                              shape: AttnShape, mask=None, workspace=None, workspace_bytes=0,
+                              dev_status=None, stream=None):
+    _check(_lib.ptd_tree_attention_ragged(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_len),
+                                          _ptr(tree_len), _ptr(parent), T, _ptr(out),
+                                          ctypes.byref(shape), _ptr(mask), _ptr(workspace),
+                                          workspace_bytes, _ptr(dev_status), _stream(stream)),
+           "ptd_tree_attention_ragged")
+
+
+def ptd_tree_attention_paged(q, kv: KVPages, kv_len, tree_len, parent, T, out, shape: AttnShape,
                              mask=None, workspace=None, workspace_bytes=0, dev_status=None,
                              stream=None):
-    _check(_lib.ptd_tree_attention_paged(_ptr(q), ctypes.byref(kv), _ptr(kv_len), _ptr(parent),
-                                         T, _ptr(out), ctypes.byref(shape), _ptr(mask),
-                                         _ptr(workspace), workspace_bytes, _ptr(dev_status),
-                                         _stream(stream)),
+    _check(_lib.ptd_tree_attention_paged(_ptr(q), ctypes.byref(kv), _ptr(kv_len), _ptr(tree_len),
+                                         _ptr(parent), T, _ptr(out), ctypes.byref(shape),
+                                         _ptr(mask), _ptr(workspace), workspace_bytes,
+                                         _ptr(dev_status), _stream(stream)),
            "ptd_tree_attention_paged")
 
 
@@ -322,8 +335,10 @@ def tree_mask(parent: torch.Tensor, tree_len: Optional[torch.Tensor] = None,
 
 def tree_attention(q, k_cache, v_cache, kv_len, parent, mask=None, out=None,
                    out_dtype=None, scale: float = 0.0, workspace=None,
-                   dev_status=None):
-    _need_gpu(q, k_cache, v_cache, kv_len, parent, mask)
+                   dev_status=None, tree_len=None):
+    """tree_len int32 [B] (optional): a padded batch of trees of different
+    sizes (ptd_tree_attention_ragged); nodes >= tree_len[b] get zero rows."""
+    _need_gpu(q, k_cache, v_cache, kv_len, parent, mask, tree_len)
     B, T, Hq, D = q.shape
     shape = attn_shape(q, k_cache, out_dtype, scale)
     if out is None:
@@ -332,17 +347,22 @@ def tree_attention(q, k_cache, v_cache, kv_len, parent, mask=None, out=None,
     nbytes = ptd_tree_attention_workspace_bytes(shape, T)
     if workspace is None and nbytes:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
-    ptd_tree_attention(q, k_cache, v_cache, kv_len, parent, T, out, shape, mask,
-                       workspace, 0 if workspace is None else workspace.numel(),
-                       dev_status)
+    wsb = 0 if workspace is None else workspace.numel()
+    if tree_len is None:
+        ptd_tree_attention(q, k_cache, v_cache, kv_len, parent, T, out, shape, mask,
+                           workspace, wsb, dev_status)
+    else:
+        ptd_tree_attention_ragged(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape,
+                                  mask, workspace, wsb, dev_status)
     return out
 
 
 def tree_attention_paged(q, k_pages, v_pages, page_table, kv_len, parent, out=None,
-                         out_dtype=None, scale: float = 0.0, workspace=None, dev_status=None):
+                         out_dtype=None, scale: float = 0.0, workspace=None, dev_status=None,
+                         tree_len=None):
     """k_pages, v_pages [num_pages][Hkv][page_size][D] (bf16), page_table
     int32 [B][max_pages]; otherwise as tree_attention."""
-    _need_gpu(q, k_pages, v_pages, page_table, kv_len, parent)
+    _need_gpu(q, k_pages, v_pages, page_table, kv_len, parent, tree_len)
     B, T, Hq, D = q.shape
     num_pages, Hkv, ps, _ = k_pages.shape
     max_pages = page_table.shape[1]
@@ -357,7 +377,7 @@ def tree_attention_paged(q, k_pages, v_pages, page_table, kv_len, parent, out=No
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
     kv = KVPages(k_pages.data_ptr(), v_pages.data_ptr(), page_table.data_ptr(), ps, max_pages,
                  num_pages)
-    ptd_tree_attention_paged(q, kv, kv_len, parent, T, out, shape, None, workspace,
+    ptd_tree_attention_paged(q, kv, kv_len, tree_len, parent, T, out, shape, None, workspace,
                              0 if workspace is None else workspace.numel(), dev_status)
     return out
 

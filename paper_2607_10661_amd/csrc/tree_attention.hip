@@ -59,6 +59,7 @@ struct AttnParams {
   const void* v;
   const int32_t* kv_len;
   const int32_t* parent;  // [B][T]
+  const int32_t* tree_len;  // [B] or null: nodes at index >= tree_len[b] are padding
   const uint64_t* mask;   // [B][T][W] ancestor words (trees of more than 128 nodes, fp32 path)
   void* out;
   float* part_o;    // [S][B][Hkv][M][D]
@@ -80,6 +81,11 @@ struct AttnParams {
 __host__ __device__ inline int chunk_size(int N, int splits) {
   const int c = (N + splits - 1) / splits;
   return (c + 31) & ~31;
+}
+
+// Live nodes of sequence b (the rest of the T slots are padding).
+__device__ inline int live_nodes(const AttnParams& p, int b) {
+  return p.tree_len ? min(max(p.tree_len[b], 0), p.T) : p.T;
 }
 
 __device__ inline void logical_block(int nblocks, int& id) {
@@ -190,15 +196,27 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   const int b = rest / p.Hkv;
 
   const int n_kv = p.kv_len[b];
-  if (n_kv < 0 || n_kv + p.T > p.L_cap) {
+  const int tl = live_nodes(p, b);
+  if (n_kv < 0 || n_kv + tl > p.L_cap) {
     if (tid == 0) ptd::report(p.dev_status, PTD_ERR_KV_LEN);
     return;
   }
-  const int N = n_kv + p.T;
+  const int N = n_kv + tl;
   const int csz = chunk_size(N, p.splits);
   const int start = split * csz;
   const int end = min(N, start + csz);
-  if (start >= end) return;  // empty split: the combine skips it
+  if (start >= end) {  // empty split: the combine skips it
+    if (p.splits == 1) {  // no keys at all (every node padding): zero rows
+      const int r0 = pass * p.rows_per_pass, r1 = min(p.M, r0 + p.rows_per_pass);
+      for (int x = tid; x < (r1 - r0) * D; x += kThreads) {
+        const int r = r0 + x / D, d = x % D;
+        const size_t off = ((static_cast<size_t>(b) * p.T + r / p.G) * p.Hq + g * p.G + r % p.G) * D + d;
+        if (p.out_bf16) static_cast<uint16_t*>(p.out)[off] = 0;
+        else static_cast<float*>(p.out)[off] = 0.f;
+      }
+    }
+    return;
+  }
 
   const bool paged = p.page_table != nullptr;  // uniform
   const uint16_t* kbase = static_cast<const uint16_t*>(p.k) +
@@ -420,9 +438,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       mw1[qb] = 0ull;
     }
     if (small_tree && abs0 + R::SUB > n_kv) {
-      int a[QB];
+      int a[QB];  // padding nodes see no tree keys (and their parents are not read)
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) a[qb] = node[qb];
+      for (int qb = 0; qb < QB; ++qb) a[qb] = node[qb] < tl ? node[qb] : -1;
       for (int step = 0; step < 128; ++step) {
         bool live = false;
 #pragma unroll
@@ -734,7 +752,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       const int i = r / p.G, hg = r % p.G;
       const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D +
                          16 * dt + 4 * l4;
-      const f32x4 v = acc * (1.0f / den);
+      const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+      const f32x4 v = i < tl ? acc * (1.0f / den) : zero;
       if (p.out_bf16) {
         const u32x2 w2 = {ptd::cvt_pk_bf16(v[0], v[1]), ptd::cvt_pk_bf16(v[2], v[3])};
         *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.out) + off) = w2;
@@ -823,9 +842,10 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnParams p) {
     }
   };
   const int n_kv = p.kv_len[b];
+  const int tl = live_nodes(p, b);
   load_group(0);
-  const bool valid = n_kv >= 0 && n_kv + p.T <= p.L_cap;  // else reported by the attention kernel
-  const int N = n_kv + p.T;
+  const bool valid = n_kv >= 0 && n_kv + tl <= p.L_cap;  // else reported by the attention kernel
+  const int N = n_kv + tl;
   const int csz = chunk_size(max(N, 1), p.splits);
   const int nsp = (N + csz - 1) / csz;  // non-empty splits
   float mrun = kNegBig, den = 0.f;
@@ -850,8 +870,9 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnParams p) {
     merge_group(s0);
   }
   if (!valid) return;
-  const f32x4 v = acc * (1.0f / den);
   const int i = r / p.G, hg = r % p.G;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  const f32x4 v = i < tl ? acc * (1.0f / den) : zero;  // padding nodes: zero
   const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D + d4 * 4;
   if (p.out_bf16) {
     const u32x2 w = {ptd::cvt_pk_bf16(v[0], v[1]), ptd::cvt_pk_bf16(v[2], v[3])};
@@ -882,11 +903,12 @@ __global__ void __launch_bounds__(kValuThreads) k_attn_valu(AttnParams p) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int pass = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int n_kv = p.kv_len[b];
-  if (n_kv < 0 || n_kv + p.T > p.L_cap) {
+  const int tl = live_nodes(p, b);
+  if (n_kv < 0 || n_kv + tl > p.L_cap) {
     if (tid == 0) ptd::report(p.dev_status, PTD_ERR_KV_LEN);
     return;
   }
-  const int N = n_kv + p.T;
+  const int N = n_kv + tl;
   const int r0 = pass * kValuRows;
   const float* qg = static_cast<const float*>(p.q);
   const float* kg = static_cast<const float*>(p.k);
@@ -961,7 +983,7 @@ __global__ void __launch_bounds__(kValuThreads) k_attn_valu(AttnParams p) {
     if (r >= p.M) continue;
     const int i = r / p.G, hg = r % p.G;
     const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D + d;
-    const float v = acc[rl][d] / sl[rl];
+    const float v = i < tl ? acc[rl][d] / sl[rl] : 0.f;  // padding nodes: zero
     if (p.out_bf16) static_cast<uint16_t*>(p.out)[off] = static_cast<uint16_t>(ptd::f32_to_bf16_rne(v));
     else static_cast<float*>(p.out)[off] = v;
   }
@@ -985,7 +1007,7 @@ constexpr int kTargetBlocks = 256;  // one resident workgroup per CU on MI355X
 bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
   if (!s || s->B < 1 || s->Hq < 1 || s->Hkv < 1 || s->Hq % s->Hkv) return false;
   if (s->D != 64 && s->D != 128) return false;
-  if (T < 1 || T > PTD_MAX_T || s->L_cap < T) return false;
+  if (T < 1 || T > PTD_MAX_T || s->L_cap < 1) return false;  // (L_cap >= T: per entry point)
   if ((s->in_dtype != PTD_F32 && s->in_dtype != PTD_BF16) ||
       (s->out_dtype != PTD_F32 && s->out_dtype != PTD_BF16))
     return false;
@@ -1053,7 +1075,8 @@ namespace {
 
 // The attention call on contiguous caches (page_table null) or paged ones.
 int attention_impl(const void* q, const void* k_cache, const void* v_cache,
-                   const int32_t* kv_len, const int32_t* parent, int32_t T, void* out,
+                   const int32_t* kv_len, const int32_t* tree_len, const int32_t* parent,
+                   int32_t T, void* out,
                    const ptd_attn_shape* shape, const uint64_t* mask, void* workspace,
                    size_t workspace_bytes, int32_t* dev_status, void* stream,
                    const int32_t* page_table, int page_shift, int max_pages, int num_pages) {
@@ -1063,6 +1086,8 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
   if (shape->out_dtype != PTD_F32 && shape->out_dtype != PTD_BF16) return PTD_ERR_DTYPE;
   Plan pl;
   PTD_RETURN_IF(!make_plan(shape, T, &pl), PTD_ERR_SHAPE);
+  // every tree row must fit unless tree sizes come with the call
+  PTD_RETURN_IF(!tree_len && shape->L_cap < T, PTD_ERR_SHAPE);
   PTD_RETURN_IF(!ptd_aligned(q, 16) || !ptd_aligned(k_cache, 16) || !ptd_aligned(v_cache, 16) ||
                     !ptd_aligned(out, 16) || (mask && !ptd_aligned(mask, 8)),
                 PTD_ERR_ALIGN);
@@ -1077,7 +1102,7 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   if (build_mask) {
     uint64_t* mws = reinterpret_cast<uint64_t*>(ws + pl.partial_bytes);
-    const int rc = ptd_launch_tree_mask(parent, nullptr, shape->B, T, mws, nullptr, dev_status, st);
+    const int rc = ptd_launch_tree_mask(parent, tree_len, shape->B, T, mws, nullptr, dev_status, st);
     if (rc != PTD_OK) return rc;
     mask = mws;
   }
@@ -1087,6 +1112,7 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
   prm.v = v_cache;
   prm.kv_len = kv_len;
   prm.parent = parent;
+  prm.tree_len = tree_len;
   prm.mask = pl.needs_mask ? mask : nullptr;
   prm.out = out;
   prm.part_o = pl.splits > 1 ? reinterpret_cast<float*>(ws) : nullptr;
@@ -1145,12 +1171,23 @@ extern "C" int ptd_tree_attention(const void* q, const void* k_cache, const void
                                   const uint64_t* mask, void* workspace,
                                   size_t workspace_bytes, int32_t* dev_status,
                                   void* stream) {
-  return attention_impl(q, k_cache, v_cache, kv_len, parent, T, out, shape, mask, workspace,
-                        workspace_bytes, dev_status, stream, nullptr, 0, 0, 0);
+  return attention_impl(q, k_cache, v_cache, kv_len, nullptr, parent, T, out, shape, mask,
+                        workspace, workspace_bytes, dev_status, stream, nullptr, 0, 0, 0);
+}
+
+extern "C" int ptd_tree_attention_ragged(const void* q, const void* k_cache, const void* v_cache,
+                                         const int32_t* kv_len, const int32_t* tree_len,
+                                         const int32_t* parent, int32_t T, void* out,
+                                         const ptd_attn_shape* shape, const uint64_t* mask,
+                                         void* workspace, size_t workspace_bytes,
+                                         int32_t* dev_status, void* stream) {
+  return attention_impl(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape, mask,
+                        workspace, workspace_bytes, dev_status, stream, nullptr, 0, 0, 0);
 }
 
 extern "C" int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv,
-                                        const int32_t* kv_len, const int32_t* parent, int32_t T,
+                                        const int32_t* kv_len, const int32_t* tree_len,
+                                        const int32_t* parent, int32_t T,
                                         void* out, const ptd_attn_shape* shape,
                                         const uint64_t* mask, void* workspace,
                                         size_t workspace_bytes, int32_t* dev_status,
@@ -1164,7 +1201,7 @@ extern "C" int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv,
   PTD_RETURN_IF(static_cast<long long>(kv->max_pages) * ps != shape->L_cap, PTD_ERR_SHAPE);
   int shift = 0;
   while ((1 << shift) < ps) ++shift;
-  return attention_impl(q, kv->k_pages, kv->v_pages, kv_len, parent, T, out, shape, mask,
+  return attention_impl(q, kv->k_pages, kv->v_pages, kv_len, tree_len, parent, T, out, shape, mask,
                         workspace, workspace_bytes, dev_status, stream, kv->page_table, shift,
                         kv->max_pages, kv->num_pages);
 }

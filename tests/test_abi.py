@@ -49,7 +49,10 @@ def test_attention_workspace_sizes():
     assert P.ptd_tree_attention_workspace_bytes(_shape(D=96), 64) == 0
     assert P.ptd_tree_attention_workspace_bytes(_shape(), 0) == 0
     assert P.ptd_tree_attention_workspace_bytes(_shape(), P.PTD_MAX_T + 1) == 0
-    assert P.ptd_tree_attention_workspace_bytes(_shape(L=32), 64) == 0  # L_cap < T
+    # a cache shorter than T is valid for trees of fewer live nodes (ragged calls)
+    assert P.ptd_tree_attention_workspace_bytes(_shape(dt=P.PTD_F32, D=64, Hq=2, Hkv=2, L=8),
+                                                16) == 256
+    assert P.ptd_tree_attention_workspace_bytes(_shape(L=0), 64) == 0
 
 
 def test_topk_workspace_sizes():
@@ -76,6 +79,8 @@ def test_attention_validation():
     assert _err(P.ptd_tree_attention, None, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 1
     assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE, s) == 2
     assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE,
+                _shape(L=32)) == 2                                      # L_cap < T
+    assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE,
                 _shape(Hq=3, Hkv=2)) == 2
     bad = _shape()
     bad.in_dtype = 7
@@ -85,6 +90,16 @@ def test_attention_validation():
     assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 5
     assert _err(P.ptd_tree_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s,
                 workspace=FAKE, workspace_bytes=16) == 5
+
+
+def test_ragged_attention_validation():
+    s = _shape()
+    A = P.ptd_tree_attention_ragged
+    assert _err(A, None, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 1
+    assert _err(A, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE, s) == 2
+    assert _err(A, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, _shape(Hq=3, Hkv=2)) == 2
+    assert _err(A, FAKE + 2, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 4
+    assert _err(A, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 5  # no workspace
 
 
 def test_topk_verify_expand_mask_validation():
@@ -185,11 +200,11 @@ def test_paged_attention_validation():
     kv = P.KVPages(FAKE, FAKE, FAKE, 64, 32, 64)
     A = P.ptd_tree_attention_paged
     bad_null = P.KVPages(FAKE, None, FAKE, 64, 32, 64)
-    assert _err(A, FAKE, bad_null, FAKE, FAKE, 64, FAKE, s) == 1
+    assert _err(A, FAKE, bad_null, FAKE, None, FAKE, 64, FAKE, s) == 1
     f32 = _shape(L=2048, dt=P.PTD_F32, od=P.PTD_F32)
-    assert _err(A, FAKE, kv, FAKE, FAKE, 64, FAKE, f32) == 3            # bf16 only
+    assert _err(A, FAKE, kv, FAKE, None, FAKE, 64, FAKE, f32) == 3            # bf16 only
     for ps in (16, 48, 96):                                              # power of two >= 32
-        assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, ps, 2048 // ps, 64), FAKE, FAKE, 64,
+        assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, ps, 2048 // ps, 64), FAKE, None, FAKE, 64,
                     FAKE, s) == 2
-    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 64, 31, 64), FAKE, FAKE, 64, FAKE, s) == 2
-    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 64, 32, 0), FAKE, FAKE, 64, FAKE, s) == 2
+    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 64, 31, 64), FAKE, None, FAKE, 64, FAKE, s) == 2
+    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 64, 32, 0), FAKE, None, FAKE, 64, FAKE, s) == 2

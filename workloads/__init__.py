@@ -342,6 +342,15 @@ def algorithmic_bytes(w: Workload) -> Dict[str, int]:
                 attention=attn, logits=logits, step=attn + logits)
 
 
+def ragged_attention_bytes(w: Workload, tree_len: np.ndarray) -> int:
+    """Algorithmic bytes of the attention over trees of tree_len[b] live
+    nodes: committed K/V, the live tree rows' K/V, q and out of live rows."""
+    es = 2 if w.dtype == "bf16" else 4
+    live = int(np.clip(np.asarray(tree_len), 0, w.T).sum())
+    return (int(w.kv_len.sum()) * w.Hkv * w.D * 2 * es + live * w.Hkv * w.D * 2 * es
+            + 2 * live * w.Hq * w.D * es)
+
+
 def rope_bytes(w: Workload) -> int:
     """Bytes the rotary embedding of the tree rows moves: every query head
     and tree key row of every node read and written once."""
