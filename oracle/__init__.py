@@ -39,6 +39,7 @@ def _load():
     lib.oracle_tree_attention.argtypes = [vp, vp, vp, i, vp, vp, vp, i, i, i, i, i, i,
                                           d, vp]
     lib.oracle_topk.argtypes = [vp, i, i, i, ctypes.c_longlong, i, vp, vp, vp]
+    lib.oracle_e4m3_decode.argtypes = [vp, ctypes.c_longlong, vp]
     lib.oracle_verify.argtypes = [vp, vp, vp, vp, i, i, vp, vp, vp]
     lib.oracle_expand.argtypes = [vp, vp, vp, i, i, vp, i, vp, i, i, vp, vp, vp]
     lib.oracle_tree_rope.argtypes = [vp, vp, i, vp, vp, i, i, i, i, i, i, vp, i, vp, vp,
@@ -57,7 +58,7 @@ def _load():
     for f in ("oracle_gather_pages", "oracle_step_prune", "oracle_pool_merge", "oracle_pool_retrieve",
               "oracle_verify_sample", "oracle_tree_mask", "oracle_attention_row", "oracle_tree_attention",
               "oracle_topk", "oracle_verify", "oracle_expand", "oracle_tree_rope",
-              "oracle_kv_commit"):
+              "oracle_kv_commit", "oracle_e4m3_decode"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -86,7 +87,9 @@ def _dtype_code(arr: np.ndarray) -> int:
         return 1
     if arr.dtype == np.float32:
         return 0
-    raise TypeError("oracle inputs are bf16 bits (uint16) or float32")
+    if arr.dtype == np.float64:
+        return 2
+    raise TypeError("oracle inputs are bf16 bits (uint16), float32 or float64")
 
 
 def tree_mask(parent: np.ndarray, tree_len: Optional[np.ndarray] = None):
@@ -142,6 +145,31 @@ def attention_rows(q, k_cache, v_cache, kv_len, parent, scale: float, rows,
             B, T, Hq, Hkv, D, L, float(scale), int(b), int(h), int(i),
             out[n].ctypes.data_as(ctypes.c_void_p)))
     return out
+
+
+def e4m3_decode(codes) -> np.ndarray:
+    """OCP FP8 E4M3 codes (uint8) -> their values, float64, same shape."""
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    out = np.empty(c.shape, np.float64)
+    _check(_load().oracle_e4m3_decode(_p(c), c.size, _p(out)))
+    return out
+
+
+def tree_attention_fp8kv(q, k_codes, v_codes, k_scale, v_scale, kv_len, parent,
+                         scale: float, tree_len=None, rows=None):
+    """Tree attention on E4M3 key/value caches [B][Hkv][L][D] with per-KV-head
+    scales: key = value(code) * k_scale[g], likewise for values.  All outputs
+    [B][T][Hq][D] (float64), or the selected (b, h, i) rows if given."""
+    ks = np.asarray(k_scale, np.float64)[None, :, None, None]
+    vs = np.asarray(v_scale, np.float64)[None, :, None, None]
+    kc = e4m3_decode(k_codes) * ks   # exact: 4 significant bits times a float32
+    vc = e4m3_decode(v_codes) * vs
+    qd = np.ascontiguousarray(q)
+    if qd.dtype == np.uint16:  # bf16 bits, widened exactly
+        qd = (qd.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if rows is None:
+        return tree_attention(qd, kc, vc, kv_len, parent, scale, tree_len=tree_len)
+    return attention_rows(qd, kc, vc, kv_len, parent, scale, rows, tree_len=tree_len)
 
 
 def topk(logits: np.ndarray, k: int):

@@ -25,6 +25,8 @@
  *                          query and key at that position (RoFormer rotation).
  *   oracle_kv_commit       Sec. 3.2 accepted sequence X': the accepted nodes'
  *                          keys and values become the next committed rows.
+ *   oracle_e4m3_decode     value of an OCP FP8 E4M3 code (keys and values
+ *                          cached in 8 bits, a serving format: not in the paper).
  *   oracle_verify_sample   Sec. 3.2 sampling decoding strategy; App. B
  *                          recursive candidate-tree sampling, normalized as in
  *                          the proof of App. C.
@@ -44,8 +46,10 @@
 #define ORC_BAD_KV_LEN 8
 #define ORC_BAD_PATH 9
 
-/* element widening: dtype 0 = fp32, 1 = bf16 (upper half of an fp32) */
+/* element widening: dtype 0 = fp32, 1 = bf16 (upper half of an fp32),
+ * 2 = fp64 */
 static double load_elem(const void* base, int dtype, size_t idx) {
+  if (dtype == 2) return ((const double*)base)[idx];
   if (dtype == 1) {
     uint16_t h = ((const uint16_t*)base)[idx];
     uint32_t u = ((uint32_t)h) << 16;
@@ -179,6 +183,27 @@ int oracle_tree_attention(const void* q, const void* k_cache, const void* v_cach
                                       out + (((size_t)b * T + i) * Hq + h) * D);
         if (st) return st;
       }
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * OCP 8-bit floating point E4M3 ("e4m3fn"): bit 7 sign, bits 6..3 exponent e
+ * (bias 7), bits 2..0 mantissa m.  e > 0: (1 + m/8) * 2^(e-7); e = 0:
+ * (m/8) * 2^-6 (subnormals, and +-0); e = 15 with m = 7 is NaN (the format
+ * has no infinities, so e = 15 with m < 7 is a normal number, up to 448).
+ * ------------------------------------------------------------------------- */
+static double e4m3_value(uint8_t c) {
+  const int sgn = c >> 7, e = (c >> 3) & 15, m = c & 7;
+  double v;
+  if (e == 15 && m == 7) return NAN;
+  if (e == 0) v = ldexp((double)m / 8.0, -6);
+  else v = ldexp(1.0 + (double)m / 8.0, e - 7);
+  return sgn ? -v : v;
+}
+
+int oracle_e4m3_decode(const uint8_t* codes, long long n, double* out) {
+  if (n < 0) return ORC_BAD_SIZE;
+  for (long long i = 0; i < n; ++i) out[i] = e4m3_value(codes[i]);
   return ORC_OK;
 }
 

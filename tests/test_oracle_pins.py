@@ -269,6 +269,72 @@ def test_attention_tree_len_full_is_no_tree_len_and_cache_may_end_at_the_tree():
 
 
 # ---------------------------------------------------------------------------
+# 8-bit (OCP E4M3) key/value caches
+# ---------------------------------------------------------------------------
+def test_e4m3_decode_matches_torch_float8_e4m3fn():
+    codes = np.arange(256, dtype=np.uint8)
+    got = O.e4m3_decode(codes)
+    ref = torch.from_numpy(codes.copy()).view(torch.float8_e4m3fn).double().numpy()
+    assert np.array_equal(np.isnan(got), np.isnan(ref)) and np.isnan(got).sum() == 2
+    ok = ~np.isnan(ref)
+    assert np.array_equal(got[ok], ref[ok])
+    assert np.array_equal(np.signbit(got[ok]), np.signbit(ref[ok]))
+
+
+def test_e4m3_decode_closed_forms():
+    pairs = {0x38: 1.0, 0x40: 2.0, 0x30: 0.5, 0x3C: 1.5, 0x7E: 448.0, 0xFE: -448.0,
+             0x78: 256.0, 0x08: 2.0 ** -6, 0x01: 2.0 ** -9, 0x07: 7 * 2.0 ** -9,
+             0x00: 0.0, 0xB8: -1.0}
+    got = O.e4m3_decode(np.array(list(pairs), np.uint8))
+    assert got.tolist() == list(pairs.values())
+    z = O.e4m3_decode(np.array([0x80], np.uint8))[0]
+    assert z == 0.0 and np.signbit(z)
+    assert np.isnan(O.e4m3_decode(np.array([0x7F, 0xFF], np.uint8))).all()
+
+
+def _e4m3_codes(rng, shape):
+    # random finite codes (no NaN)
+    c = rng.integers(0, 256, shape).astype(np.uint8)
+    c[(c & 0x7F) == 0x7F] = 0x3F
+    return c
+
+
+def test_e4m3_input_encoder_rounds_like_torch():
+    # the seeded generator's quantizer (input side, not the oracle)
+    rng = np.random.default_rng(12)
+    x = (rng.standard_normal(50000) * np.exp(rng.uniform(-12, 7, 50000))).astype(np.float32)
+    x = np.clip(x, -448, 448)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(W.f32_to_e4m3_bits(x), ref)
+
+
+def test_fp8kv_attention_is_the_attention_of_the_decoded_caches():
+    # every E4M3 value is a bf16 value: with unit scales the fp8 path equals
+    # the bf16 oracle on caches holding the same values
+    rng = np.random.default_rng(11)
+    w = W.make_workload(_spec(B=2, Hq=4, Hkv=2, T=7, kv_len=[9, 3], dtype="bf16"), seed=11)
+    kq = _e4m3_codes(rng, w.k_cache.shape)
+    vq = _e4m3_codes(rng, w.v_cache.shape)
+    one = np.ones(w.Hkv, np.float32)
+    out8 = O.tree_attention_fp8kv(w.q, kq, vq, one, one, w.kv_len, w.parent, w.scale)
+    as_bf16 = lambda c: W.f32_to_bf16_bits(O.e4m3_decode(c).astype(np.float32))
+    ref = O.tree_attention(w.q, as_bf16(kq), as_bf16(vq), w.kv_len, w.parent, w.scale)
+    assert np.array_equal(out8, ref)
+    # a key scale multiplies every score (= a larger softmax scale); a value
+    # scale multiplies the output
+    ks = np.array([2.0, 0.25], np.float32)
+    vs = np.array([0.5, 3.0], np.float32)
+    out_s = O.tree_attention_fp8kv(w.q, kq, vq, ks, vs, w.kv_len, w.parent, w.scale)
+    G = w.Hq // w.Hkv
+    for g in range(w.Hkv):
+        ref_g = O.tree_attention(w.q, as_bf16(kq), as_bf16(vq), w.kv_len, w.parent,
+                                 w.scale * float(ks[g]))
+        np.testing.assert_allclose(out_s[:, :, g * G:(g + 1) * G],
+                                   float(vs[g]) * ref_g[:, :, g * G:(g + 1) * G],
+                                   rtol=1e-13, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
 # top-k / argmax
 # ---------------------------------------------------------------------------
 def test_topk_golden_ties():

@@ -79,6 +79,36 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
             << np.uint32(16)).view(np.float32)
 
 
+# The 127 non-negative finite OCP E4M3 values, indexed by their code (0x00 ..
+# 0x7E): (1 + m/8) * 2^(e-7), subnormals (m/8) * 2^-6 at e = 0.
+_E4M3_POS = np.array([(m / 8.0) * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7)
+                      for e in range(16) for m in range(8)][:127], np.float64)
+
+
+def f32_to_e4m3_bits(x: np.ndarray) -> np.ndarray:
+    """Round to the nearest OCP E4M3 value (ties to the even code, i.e. even
+    mantissa), saturating at +-448; returns uint8 codes.  Inputs are finite."""
+    a = np.abs(np.asarray(x, np.float64))
+    a = np.minimum(a, 448.0)
+    hi = np.clip(np.searchsorted(_E4M3_POS, a, side="left"), 0, 126)
+    lo = np.clip(hi - 1, 0, 126)
+    d_hi = _E4M3_POS[hi] - a
+    d_lo = a - _E4M3_POS[lo]
+    pick_lo = (d_lo < d_hi) | ((d_lo == d_hi) & (lo % 2 == 0))
+    code = np.where(pick_lo, lo, hi).astype(np.uint8)
+    return code | np.where(np.signbit(np.asarray(x, np.float64)), 0x80, 0).astype(np.uint8)
+
+
+def quantize_kv_e4m3(cache: np.ndarray):
+    """A float cache [B][Hkv][L][D] -> (E4M3 codes, float32 scale per KV head):
+    scale_g = max |x| over the head / 448, codes = e4m3(x / scale_g)."""
+    x = np.asarray(cache, np.float64)
+    amax = np.abs(x).max(axis=(0, 2, 3))
+    scale = np.where(amax > 0, amax / 448.0, 1.0).astype(np.float32)
+    codes = f32_to_e4m3_bits(x / scale.astype(np.float64)[None, :, None, None])
+    return codes, scale
+
+
 def to_f64(arr: np.ndarray, dtype: str) -> np.ndarray:
     """Exact widening of a workload array ("bf16" bits or "f32") to float64."""
     if dtype == "bf16":
