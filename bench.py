@@ -287,6 +287,30 @@ def main():
                                     shape, None, ws_attn, ws_attn.numel(), status, sp)
 
     ragged_ms, _ = timed(attention_ragged, K)
+
+    # 8-bit (E4M3) key/value caches with one scale per KV head, quantized on
+    # the GPU from each rotated set before timing (D = 128, bf16 queries)
+    fp8_ms = None
+    if w.dtype == "bf16" and w.D == 128:
+        def quant(c):
+            amax = c.float().abs().amax(dim=(0, 2, 3)).clamp_min(1e-30)
+            sc = (amax / 448.0).contiguous()
+            codes = (c.float() / sc[None, :, None, None]).to(torch.float8_e4m3fn)
+            return codes.view(torch.uint8).contiguous(), sc
+
+        fp8_sets = []
+        for st_ in sets:
+            kq, ksc = quant(st_["k"])
+            vq, vsc = quant(st_["v"])
+            fp8_sets.append((kq, vq, ksc, vsc))
+
+        def attention_fp8(i):
+            s = sets[i % R]
+            kq, vq, ksc, vsc = fp8_sets[i % R]
+            P.ptd_tree_attention_fp8kv(s["q"], kq, vq, ksc, vsc, kv_len, None, parent, T, out,
+                                       shape, ws_attn, ws_attn.numel(), status, sp)
+
+        fp8_ms, _ = timed(attention_fp8, K)
     sample_ms, _ = timed(sample, K)
     if small_tree:
         prune_ms, _ = timed(prune, K)
@@ -378,6 +402,11 @@ def main():
         ragged_ms, W.ragged_attention_bytes(w, tree_len_r.numpy()),
         "ptd_tree_attention_ragged: per-sequence tree sizes %s of T = %d slots, %d back-to-back "
         "calls" % (tree_len_r.tolist() if B <= 16 else "1..%d" % T, T, K))
+    if fp8_ms is not None:
+        line["next_rows"]["fp8kv_attention"] = next_row(
+            fp8_ms, W.fp8kv_attention_bytes(w), "ptd_tree_attention_fp8kv: the attention call "
+            "on E4M3 key/value caches (one scale per KV head), %d back-to-back calls; bf16 "
+            "caches: %.3f us" % (K, att_avg_s * 1e6))
     if paged_ms is not None:
         line["next_rows"]["paged_attention"] = next_row(
             paged_ms, alg["attention"], "ptd_tree_attention_paged: the attention call on %d-row "

@@ -10,7 +10,8 @@
  *   ptd_tree_attention   tree-masked attention over committed KV + ancestors
  *                        (ptd_tree_attention_ragged: trees of different sizes
  *                        in one padded batch; ptd_tree_attention_paged: the
- *                        same on paged caches)
+ *                        same on paged caches; ptd_tree_attention_fp8kv: on
+ *                        8-bit E4M3 key/value caches)
  *   ptd_topk_argmax      per-row argmax / top-k of the verification logits
  *   ptd_verify           greedy longest accepted path (+ bonus token)
  *   ptd_expand           progressive expansion with top-k children
@@ -182,6 +183,29 @@ int ptd_tree_attention_ragged(const void* q, const void* k_cache, const void* v_
                               const ptd_attn_shape* shape, const uint64_t* mask,
                               void* workspace, size_t workspace_bytes,
                               int32_t* dev_status, void* stream);
+
+/*
+ * ptd_tree_attention_fp8kv -- ptd_tree_attention_ragged on key/value caches
+ * stored as OCP FP8 E4M3 codes (1 byte per element, half the bytes of bf16;
+ * a serving format, not in the paper) with one fp32 scale per KV head:
+ *   key row j of head g = e4m3(k_cache[b][g][j][:]) * k_scale[g], values likewise
+ *   k_cache, v_cache  uint8 [B][Hkv][L_cap][D] E4M3 codes (no NaN codes)
+ *   k_scale, v_scale  fp32 [Hkv] device, or NULL for 1
+ *   q                 bf16 [B][T][Hq][D]: shape->in_dtype must be PTD_BF16
+ * D = 128 only.  Codes are widened to bf16 exactly inside the kernel, the key
+ * scale joins the softmax scale and the value scale the output, so the
+ * arithmetic is that of the bf16 path on the decoded caches.  tree_len may be
+ * NULL; masks are derived or built as for ptd_tree_attention (no mask
+ * argument).  Workspace: ptd_tree_attention_workspace_bytes(shape, T).
+ * dev_status and errors as ptd_tree_attention; PTD_ERR_DTYPE for non-bf16
+ * queries, PTD_ERR_SHAPE for D != 128.
+ */
+int ptd_tree_attention_fp8kv(const void* q, const void* k_cache, const void* v_cache,
+                             const float* k_scale, const float* v_scale,
+                             const int32_t* kv_len, const int32_t* tree_len,
+                             const int32_t* parent, int32_t T, void* out,
+                             const ptd_attn_shape* shape, void* workspace,
+                             size_t workspace_bytes, int32_t* dev_status, void* stream);
 
 /* Workspace bytes ptd_topk_argmax needs (0 on invalid arguments). */
 /* Paged key/value caches (host struct, read during the call only). */

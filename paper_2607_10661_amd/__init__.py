@@ -71,6 +71,8 @@ _SIGS = {
     "ptd_tree_attention_ragged": ([_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp,
                                    ctypes.POINTER(AttnShape), _vp, _vp, _sz, _vp, _vp],
                                   ctypes.c_int),
+    "ptd_tree_attention_fp8kv": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp,
+                                  ctypes.POINTER(AttnShape), _vp, _sz, _vp, _vp], ctypes.c_int),
     "ptd_tree_attention_paged": ([_vp, ctypes.POINTER(KVPages), _vp, _vp, _vp, _i32, _vp,
                                   ctypes.POINTER(AttnShape), _vp, _vp, _sz, _vp, _vp],
                                  ctypes.c_int),
@@ -165,6 +167,17 @@ def ptd_tree_attention_ragged(q, k_cache, v_cache, kv_len, tree_len, parent, T, 
                                           ctypes.byref(shape), _ptr(mask), _ptr(workspace),
                                           workspace_bytes, _ptr(dev_status), _stream(stream)),
            "ptd_tree_attention_ragged")
+
+
+def ptd_tree_attention_fp8kv(q, k_cache, v_cache, k_scale, v_scale, kv_len, tree_len, parent, T,
+                             out, shape: AttnShape, workspace=None, workspace_bytes=0,
+                             dev_status=None, stream=None):
+    _check(_lib.ptd_tree_attention_fp8kv(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_scale),
+                                         _ptr(v_scale), _ptr(kv_len), _ptr(tree_len),
+                                         _ptr(parent), T, _ptr(out), ctypes.byref(shape),
+                                         _ptr(workspace), workspace_bytes, _ptr(dev_status),
+                                         _stream(stream)),
+           "ptd_tree_attention_fp8kv")
 
 
 def ptd_tree_attention_paged(q, kv: KVPages, kv_len, tree_len, parent, T, out, shape: AttnShape,
@@ -354,6 +367,31 @@ def tree_attention(q, k_cache, v_cache, kv_len, parent, mask=None, out=None,
     else:
         ptd_tree_attention_ragged(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape,
                                   mask, workspace, wsb, dev_status)
+    return out
+
+
+def tree_attention_fp8kv(q, k_cache, v_cache, k_scale, v_scale, kv_len, parent, out=None,
+                         out_dtype=None, scale: float = 0.0, workspace=None, dev_status=None,
+                         tree_len=None):
+    """k_cache, v_cache uint8 [B][Hkv][L_cap][D] E4M3 codes; k_scale, v_scale
+    float32 [Hkv] (or None); q bf16; otherwise as tree_attention."""
+    _need_gpu(q, k_cache, v_cache, k_scale, v_scale, kv_len, parent, tree_len)
+    if k_cache.dtype != torch.uint8 or v_cache.dtype != torch.uint8:
+        raise ValueError("expected uint8 E4M3 caches")
+    B, T, Hq, D = q.shape
+    _, Hkv, L, _ = k_cache.shape
+    shape = AttnShape(B, Hq, Hkv, D, L, _dtype_code(q),
+                      _dtype_code(q) if out_dtype is None else
+                      (PTD_BF16 if out_dtype == torch.bfloat16 else PTD_F32), float(scale))
+    if out is None:
+        od = torch.bfloat16 if shape.out_dtype == PTD_BF16 else torch.float32
+        out = torch.empty((B, T, Hq, D), dtype=od, device=q.device)
+    nbytes = ptd_tree_attention_workspace_bytes(shape, T)
+    if workspace is None and nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    ptd_tree_attention_fp8kv(q, k_cache, v_cache, k_scale, v_scale, kv_len, tree_len, parent, T,
+                             out, shape, workspace, 0 if workspace is None else workspace.numel(),
+                             dev_status)
     return out
 
 

@@ -60,6 +60,8 @@ struct AttnParams {
   const int32_t* kv_len;
   const int32_t* parent;  // [B][T]
   const int32_t* tree_len;  // [B] or null: nodes at index >= tree_len[b] are padding
+  const float* k_scale;     // [Hkv] or null (8-bit caches): key = code value * k_scale[g]
+  const float* v_scale;     // [Hkv] or null: value = code value * v_scale[g]
   const uint64_t* mask;   // [B][T][W] ancestor words (trees of more than 128 nodes, fp32 path)
   void* out;
   float* part_o;    // [S][B][Hkv][M][D]
@@ -129,19 +131,39 @@ __device__ __forceinline__ i16x4 lds_read_tr16(const unsigned char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((PTD_LDS i16x4*)p);
 }
 
-// LDS layout of one 32-key sub-tile: K rows then V rows, each [32][D] bf16,
-// row-major with the 16-byte chunks of row r stored XOR-permuted by f(r)
-// (CH = D/8 chunks per row).  For D = 128, f(r) = ((r mod 8) << 1) | bit 3
-// of r: a bijection on 16 rows, so the K-operand reads (16 rows x one chunk
-// per 16 lanes) hit distinct banks, and f >> 1 is distinct over rows 0..7 and
-// over rows 8..15, so each half-wave of a V transpose read (8 rows x 2
-// adjacent chunks) covers all 16 chunk positions once.  For D = 64,
-// f(r) = r mod 8.
-template <int D>
+using i32x2 = int __attribute__((ext_vector_type(2)));
+// Transpose read of bytes (ds_read_b64_tr_b8): in each 16-lane group, lane i
+// receives byte i mod 8 of the 8 bytes read by the group's lanes 2j + i / 8,
+// j = 0..7, as its bytes j.
+__device__ __forceinline__ u32x2 lds_read_tr8(const unsigned char* p) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr8_b64_v2i32((PTD_LDS i32x2*)p));
+}
+// Eight OCP E4M3 values (bytes 0..7 of w) as eight bf16, exactly (every E4M3
+// value is a bf16 value): gfx950 v_cvt_scalef32_pk_bf16_fp8 with scale 1.
+__device__ __forceinline__ bf16x8 e4m3x8_to_bf16(u32x2 w) {
+  const u32x4 r = {
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, false)),
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, true)),
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, false)),
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, true))};
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+// LDS layout of one 32-key sub-tile: K rows then V rows, each [32][D] of
+// ES-byte elements (bf16, or E4M3 for 8-bit caches), row-major with the
+// 16-byte chunks of row r stored XOR-permuted by f(r) (CH = D*ES/16 chunks
+// per row).  bf16, D = 128: f(r) = ((r mod 8) << 1) | bit 3 of r, a bijection
+// on 16 rows, so the K-operand reads (16 rows x one chunk per 16 lanes) hit
+// distinct banks, and f >> 1 is distinct over rows 0..7 and over rows 8..15,
+// so each half-wave of a V transpose read (8 rows x 2 adjacent chunks) covers
+// all 16 chunk positions once.  Otherwise (bf16 D = 64, E4M3 D = 128: 8
+// chunks) f(r) = r mod 8.
+template <int D, int ES>
 struct Ring {
-  static constexpr int CH = D / 8;                   // 16-byte chunks per row
+  static constexpr int RB = D * ES;                  // bytes per row
+  static constexpr int CH = RB / 16;                 // 16-byte chunks per row
   static constexpr int SUB = 32;                     // keys per sub-tile
-  static constexpr int PART = SUB * D * 2;           // bytes of K (or V) per sub-tile
+  static constexpr int PART = SUB * RB;              // bytes of K (or V) per sub-tile
   static constexpr int SLOT = 2 * PART;              // K + V
   static constexpr int NS = (160 * 1024) / SLOT;     // sub-tiles in the ring (all of LDS)
   static constexpr int DPS = 2 * SUB * CH / kThreads;  // copies per thread per sub-tile
@@ -165,9 +187,13 @@ __device__ __forceinline__ u32x4 gload16(const void* p) {
 // Orders every later use of v after the preceding (volatile) wait.
 __device__ __forceinline__ void reg_fence(u32x4& v) { asm volatile("" : "+v"(v)); }
 
-template <int D, int QB, int WR>
+template <int D, int QB, int WR, bool F8>
 __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
-  using R = Ring<D>;
+  // F8: keys and values are OCP E4M3 codes (scaled per KV head), widened to
+  // bf16 exactly after the LDS reads; everything else is the bf16 kernel
+  using KV = std::conditional_t<F8, uint8_t, uint16_t>;
+  constexpr int ES = F8 ? 1 : 2;
+  using R = Ring<D, ES>;
   constexpr int WK = (kThreads / PTD_WAVE) / WR;  // key groups: sub-tiles per round
   constexpr int DB = D / 32;                      // 32-wide d blocks (QK^T k-dim)
   constexpr int DT = D / 16;                      // 16-wide d tiles (PV output rows)
@@ -219,10 +245,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   }
 
   const bool paged = p.page_table != nullptr;  // uniform
-  const uint16_t* kbase = static_cast<const uint16_t*>(p.k) +
-                          (paged ? 0 : (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D);
-  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) +
-                          (paged ? 0 : (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D);
+  const KV* kbase = static_cast<const KV*>(p.k) +
+                    (paged ? 0 : (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D);
+  const KV* vbase = static_cast<const KV*>(p.v) +
+                    (paged ? 0 : (static_cast<size_t>(b) * p.Hkv + g) * p.L_cap * D);
   // paged: the split's first 256 page ids, one per lane and register, loaded
   // untracked ahead of the query rows
   const int first_page = paged ? (start >> p.page_shift) : 0;
@@ -277,8 +303,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     cp_v[u] = (u * kThreads + wave * PTD_WAVE) / (R::SUB * R::CH) != 0;
     const int local = c % (R::SUB * R::CH);
     cp_row[u] = local / R::CH;
-    cp_off[u] = R::swz(cp_row[u], local % R::CH) * 8;
-    cp_voff[u] = static_cast<uint32_t>((cp_row[u] * D + cp_off[u]) * 2);
+    cp_off[u] = R::swz(cp_row[u], local % R::CH) * (16 / ES);  // elements
+    cp_voff[u] = static_cast<uint32_t>((cp_row[u] * D + cp_off[u]) * ES);
     cp_lds[u] = static_cast<uint32_t>((u * kThreads + wave * PTD_WAVE) * 16);
   }
   // element offset of key row `row0` (a multiple of 32): contiguous, or in
@@ -352,14 +378,28 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   // per-lane LDS byte offsets inside a sub-tile (the row's swizzle is the
   // same for both 16-row halves, which therefore differ by a constant)
   int koff[DB], voff[DT];
+  if constexpr (F8) {
+    // K: lane (l16, l4) reads the 8 bytes d = 32*db + 8*l4 .. of key l16.
+    // V: source lane l16 = 2j + h of group l4 points at key slot j's row
+    // (keys 4*l4 + j, j < 4, and 16 + 4*l4 + j - 4), bytes 16*dt + 8h ..;
+    // the transpose read gives lane l16 the 8 keys' values at d = 16*dt + l16.
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
-    koff[db] = l16 * (D * 2) + R::swz(l16, db * 4 + l4) * 16;
-  const int tj = l16 >> 2, tq = l16 & 3;
-  const int key0 = 4 * l4 + tj;  // this lane's source key for the transpose reads
+    for (int db = 0; db < DB; ++db)
+      koff[db] = l16 * R::RB + R::swz(l16, 2 * db + (l4 >> 1)) * 16 + (l4 & 1) * 8;
+    const int j = l16 >> 1, h = l16 & 1;
+    const int key0 = j < 4 ? 4 * l4 + j : 16 + 4 * l4 + (j - 4);
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-    voff[dt] = key0 * (D * 2) + R::swz(key0, 2 * dt + (tq >> 1)) * 16 + (tq & 1) * 8;
+    for (int dt = 0; dt < DT; ++dt) voff[dt] = key0 * R::RB + R::swz(key0, dt) * 16 + h * 8;
+  } else {
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      koff[db] = l16 * R::RB + R::swz(l16, db * 4 + l4) * 16;
+    const int tj = l16 >> 2, tq = l16 & 3;
+    const int key0 = 4 * l4 + tj;  // this lane's source key for the transpose reads
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      voff[dt] = key0 * R::RB + R::swz(key0, 2 * dt + (tq >> 1)) * 16 + (tq & 1) * 8;
+  }
 
   struct Tile {
     f32x4 s[2][QB];
@@ -374,9 +414,13 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        f.k[db][kb] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(ks + kb * 16 * (D * 2) + koff[db]));
+      for (int kb = 0; kb < 2; ++kb) {
+        if constexpr (F8)
+          f.k[db][kb] = e4m3x8_to_bf16(*reinterpret_cast<const u32x2*>(ks + kb * 16 * R::RB + koff[db]));
+        else
+          f.k[db][kb] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(ks + kb * 16 * R::RB + koff[db]));
+      }
     return f;
   };
   // S^T (keys x queries) = K Q^T; lane: query l16, keys 16*kb + 4*l4 + e
@@ -405,10 +449,15 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   auto read_v = [&](int slot) __attribute__((always_inline)) -> VFrag {
     VFrag f;
     const unsigned char* vs = smem + slot * R::SLOT + R::PART;
+    if constexpr (F8) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) f.v[dt] = e4m3x8_to_bf16(lds_read_tr8(vs + voff[dt]));
+      return f;
+    }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       const i16x4 lo = lds_read_tr16(vs + voff[dt]);
-      const i16x4 hi = lds_read_tr16(vs + 16 * (D * 2) + voff[dt]);
+      const i16x4 hi = lds_read_tr16(vs + 16 * R::RB + voff[dt]);
       const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
       const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
       const u32x4 vv = {l2[0], l2[1], h2[0], h2[1]};
@@ -510,7 +559,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   //      sub-tile's p are recomputed.
   f32x4 o[QB][DT];
   float m[QB], nmc[QB], lsum[QB];
-  const float c = p.c;
+  // score scale in the exp2 domain; 8-bit keys carry their head's scale
+  const float c = F8 && p.k_scale ? p.c * p.k_scale[g] : p.c;
+  const float vsc = F8 && p.v_scale ? p.v_scale[g] : 1.0f;  // value scale
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     m[qb] = kNegBig;
@@ -753,7 +804,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       const size_t off = ((static_cast<size_t>(b) * p.T + i) * p.Hq + g * p.G + hg) * D +
                          16 * dt + 4 * l4;
       const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-      const f32x4 v = i < tl ? acc * (1.0f / den) : zero;
+      const f32x4 v = i < tl ? acc * (vsc / den) : zero;
       if (p.out_bf16) {
         const u32x2 w2 = {ptd::cvt_pk_bf16(v[0], v[1]), ptd::cvt_pk_bf16(v[2], v[3])};
         *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.out) + off) = w2;
@@ -762,7 +813,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       }
     } else {
       const size_t prow = ((static_cast<size_t>(split) * p.B + b) * p.Hkv + g) * p.M + r;
-      *reinterpret_cast<f32x4*>(p.part_o + prow * D + 16 * dt + 4 * l4) = acc;
+      *reinterpret_cast<f32x4*>(p.part_o + prow * D + 16 * dt + 4 * l4) = F8 ? acc * vsc : acc;
       if (dt == 0 && l4 == 0) p.part_ml[prow] = make_float2(mc, den);
     }
   };
@@ -771,7 +822,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) store_tile(qb, dt, o[qb][dt], m[qb] * p.c, lsum[qb]);
+      for (int dt = 0; dt < DT; ++dt) store_tile(qb, dt, o[qb][dt], m[qb] * c, lsum[qb]);
   } else {
     f32x4* so = reinterpret_cast<f32x4*>(smem);  // [WR][WK][QB][DT][64]
     float2* sml = reinterpret_cast<float2*>(smem + PARK_O);  // [WR][WK][QB][64]
@@ -794,7 +845,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       }
 #pragma unroll
       for (int k2 = 0; k2 < WK; ++k2) {
-        w[k2] = __builtin_amdgcn_exp2f((mk[k2] - mm) * p.c);
+        w[k2] = __builtin_amdgcn_exp2f((mk[k2] - mm) * c);
         den += w[k2] * sml[((wr * WK + k2) * QB + qb) * 64 + lane].y;
       }
 #pragma unroll
@@ -803,7 +854,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int k2 = 0; k2 < WK; ++k2) acc += so[(((wr * WK + k2) * QB + qb) * DT + dt) * 64 + lane] * w[k2];
-        store_tile(qb, dt, acc, mm * p.c, den);
+        store_tile(qb, dt, acc, mm * c, den);
       }
     }
   }
@@ -1051,12 +1102,12 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
   return true;
 }
 
-template <int D>
+template <int D, bool F8>
 void launch_mfma(const Plan& pl, const AttnParams& prm, hipStream_t st) {
   const dim3 grid(prm.B * prm.Hkv * pl.passes * pl.splits);
   const dim3 block(kThreads);
 #define PTD_MFMA_CASE(qb_, wr_) \
-  if (pl.QB == qb_ && pl.WR == wr_) { hipLaunchKernelGGL((k_attn_mfma<D, qb_, wr_>), grid, block, 0, st, prm); return; }
+  if (pl.QB == qb_ && pl.WR == wr_) { hipLaunchKernelGGL((k_attn_mfma<D, qb_, wr_, F8>), grid, block, 0, st, prm); return; }
   PTD_MFMA_CASE(1, 2) PTD_MFMA_CASE(2, 2)
   PTD_MFMA_CASE(1, 4) PTD_MFMA_CASE(2, 4)
   PTD_MFMA_CASE(1, 8) PTD_MFMA_CASE(2, 8)
@@ -1079,7 +1130,9 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
                    int32_t T, void* out,
                    const ptd_attn_shape* shape, const uint64_t* mask, void* workspace,
                    size_t workspace_bytes, int32_t* dev_status, void* stream,
-                   const int32_t* page_table, int page_shift, int max_pages, int num_pages) {
+                   const int32_t* page_table, int page_shift, int max_pages, int num_pages,
+                   bool f8 = false, const float* k_scale = nullptr,
+                   const float* v_scale = nullptr) {
   PTD_RETURN_IF(!q || !k_cache || !v_cache || !kv_len || !parent || !out || !shape,
                 PTD_ERR_NULL);
   if (shape->in_dtype != PTD_F32 && shape->in_dtype != PTD_BF16) return PTD_ERR_DTYPE;
@@ -1113,6 +1166,8 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
   prm.kv_len = kv_len;
   prm.parent = parent;
   prm.tree_len = tree_len;
+  prm.k_scale = k_scale;
+  prm.v_scale = v_scale;
   prm.mask = pl.needs_mask ? mask : nullptr;
   prm.out = out;
   prm.part_o = pl.splits > 1 ? reinterpret_cast<float*>(ws) : nullptr;
@@ -1141,8 +1196,9 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
     prm.part_ml = reinterpret_cast<float2*>(prm.part_o + rows * shape->D);
   }
   if (pl.mfma) {
-    if (shape->D == 128) launch_mfma<128>(pl, prm, st);
-    else launch_mfma<64>(pl, prm, st);
+    if (f8) launch_mfma<128, true>(pl, prm, st);  // (D = 128 checked by the entry point)
+    else if (shape->D == 128) launch_mfma<128, false>(pl, prm, st);
+    else launch_mfma<64, false>(pl, prm, st);
     if (pl.splits > 1) {
       const size_t total = static_cast<size_t>(prm.B) * prm.Hkv * prm.M * (shape->D / 4);
       const dim3 grid(static_cast<unsigned>((total + 255) / 256));
@@ -1183,6 +1239,21 @@ extern "C" int ptd_tree_attention_ragged(const void* q, const void* k_cache, con
                                          int32_t* dev_status, void* stream) {
   return attention_impl(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape, mask,
                         workspace, workspace_bytes, dev_status, stream, nullptr, 0, 0, 0);
+}
+
+extern "C" int ptd_tree_attention_fp8kv(const void* q, const void* k_cache, const void* v_cache,
+                                        const float* k_scale, const float* v_scale,
+                                        const int32_t* kv_len, const int32_t* tree_len,
+                                        const int32_t* parent, int32_t T, void* out,
+                                        const ptd_attn_shape* shape, void* workspace,
+                                        size_t workspace_bytes, int32_t* dev_status,
+                                        void* stream) {
+  PTD_RETURN_IF(!shape, PTD_ERR_NULL);
+  PTD_RETURN_IF(shape->in_dtype != PTD_BF16, PTD_ERR_DTYPE);  // bf16 queries (the MFMA path)
+  PTD_RETURN_IF(shape->D != 128, PTD_ERR_SHAPE);
+  return attention_impl(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape, nullptr,
+                        workspace, workspace_bytes, dev_status, stream, nullptr, 0, 0, 0, true,
+                        k_scale, v_scale);
 }
 
 extern "C" int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv,

@@ -102,6 +102,16 @@ def test_ragged_attention_validation():
     assert _err(A, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 5  # no workspace
 
 
+def test_fp8kv_attention_validation():
+    s = _shape()
+    A = P.ptd_tree_attention_fp8kv
+    assert _err(A, None, FAKE, FAKE, None, None, FAKE, None, FAKE, 64, FAKE, s) == 1
+    assert _err(A, FAKE, FAKE, FAKE, None, None, FAKE, None, FAKE, 64, FAKE,
+                _shape(dt=P.PTD_F32, od=P.PTD_F32)) == 3               # bf16 queries only
+    assert _err(A, FAKE, FAKE, FAKE, None, None, FAKE, None, FAKE, 64, FAKE, _shape(D=64)) == 2
+    assert _err(A, FAKE, FAKE, FAKE, None, None, FAKE, None, FAKE, 64, FAKE, s) == 5
+
+
 def test_topk_verify_expand_mask_validation():
     assert _err(P.ptd_topk_argmax, None, P.PTD_BF16, 4, 100, 100, 4, FAKE) == 1
     assert _err(P.ptd_topk_argmax, FAKE, 5, 4, 100, 100, 4, FAKE) == 3

@@ -381,6 +381,14 @@ def ragged_attention_bytes(w: Workload, tree_len: np.ndarray) -> int:
             + 2 * live * w.Hq * w.D * es)
 
 
+def fp8kv_attention_bytes(w: Workload) -> int:
+    """Algorithmic bytes of the attention on 8-bit key/value caches: committed
+    and tree K/V at one byte per element, q and out at the workload's width."""
+    es = 2 if w.dtype == "bf16" else 4
+    kv = (int(w.kv_len.sum()) + w.B * w.T) * w.Hkv * w.D * 2
+    return kv + 2 * w.B * w.T * w.Hq * w.D * es
+
+
 def rope_bytes(w: Workload) -> int:
     """Bytes the rotary embedding of the tree rows moves: every query head
     and tree key row of every node read and written once."""
