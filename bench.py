@@ -356,6 +356,35 @@ def main():
                          f"{w.Hq} heads, single thread), {el:.1f} s",
                "us_per_step": round(el / done * 1e6, 1)}
 
+        # the same oracle on the host's cores (at most 16, the box's share): a
+        # step's attention rows spread over a thread pool (the oracle's C calls
+        # release the GIL); mask, top-k, verify and expand as above
+        import concurrent.futures as cf
+        nth = max(1, min(16, os.cpu_count() or 1))
+        rows_all = [(b, h, i) for b in range(B) for h in range(w.Hq) for i in range(T)]
+        chunks = [rows_all[j::nth] for j in range(nth)]
+
+        def rows_of(ch):
+            return O.attention_rows(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale, ch)
+
+        with cf.ThreadPoolExecutor(nth) as ex:
+            done_m, t_start = 0, time.perf_counter()
+            while True:
+                O.tree_mask(w.parent)
+                list(ex.map(rows_of, chunks))
+                r_am, r_idx, _ = O.topk(w.logits, k)
+                O.verify(r_am.reshape(B, -1), w.tokens, w.parent)
+                O.expand(w.parent, w.tokens, r_idx.reshape(B, T + 1, k), w.width, w.d_max,
+                         w.T_max)
+                done_m += 1
+                el_m = time.perf_counter() - t_start
+                if el_m >= args.cpu_seconds or el_m * (done_m + 1) / done_m > 3 * args.cpu_seconds:
+                    break
+        cpu["all_cores"] = {"value": round(B * T * done_m / el_m, 3), "unit": "tree tokens/s",
+                            "cores": nth,
+                            "sample": f"{done_m} whole step(s), attention rows over {nth} "
+                                      f"threads, {el_m:.1f} s"}
+
     line = {
         "metric": "tree tokens/s (tree-attn + top-k + verify + expand step)",
         "value": round(tokens_per_s, 1),
