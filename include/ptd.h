@@ -198,7 +198,8 @@ int ptd_tree_attention_ragged(const void* q, const void* k_cache, const void* v_
  * NULL; masks are derived or built as for ptd_tree_attention (no mask
  * argument).  Workspace: ptd_tree_attention_workspace_bytes(shape, T).
  * dev_status and errors as ptd_tree_attention; PTD_ERR_DTYPE for non-bf16
- * queries, PTD_ERR_SHAPE for D != 128.
+ * queries, PTD_ERR_SHAPE for D != 128, PTD_ERR_ALIGN for scales that are not
+ * 4-byte aligned.
  */
 int ptd_tree_attention_fp8kv(const void* q, const void* k_cache, const void* v_cache,
                              const float* k_scale, const float* v_scale,

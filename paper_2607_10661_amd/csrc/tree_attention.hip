@@ -1251,6 +1251,8 @@ extern "C" int ptd_tree_attention_fp8kv(const void* q, const void* k_cache, cons
   PTD_RETURN_IF(!shape, PTD_ERR_NULL);
   PTD_RETURN_IF(shape->in_dtype != PTD_BF16, PTD_ERR_DTYPE);  // bf16 queries (the MFMA path)
   PTD_RETURN_IF(shape->D != 128, PTD_ERR_SHAPE);
+  PTD_RETURN_IF((k_scale && !ptd_aligned(k_scale, 4)) || (v_scale && !ptd_aligned(v_scale, 4)),
+                PTD_ERR_ALIGN);
   return attention_impl(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape, nullptr,
                         workspace, workspace_bytes, dev_status, stream, nullptr, 0, 0, 0, true,
                         k_scale, v_scale);

@@ -110,6 +110,7 @@ def test_fp8kv_attention_validation():
                 _shape(dt=P.PTD_F32, od=P.PTD_F32)) == 3               # bf16 queries only
     assert _err(A, FAKE, FAKE, FAKE, None, None, FAKE, None, FAKE, 64, FAKE, _shape(D=64)) == 2
     assert _err(A, FAKE, FAKE, FAKE, None, None, FAKE, None, FAKE, 64, FAKE, s) == 5
+    assert _err(A, FAKE, FAKE, FAKE, FAKE + 2, None, FAKE, None, FAKE, 64, FAKE, s) == 4
 
 
 def test_topk_verify_expand_mask_validation():
