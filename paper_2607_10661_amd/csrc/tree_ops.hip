@@ -538,9 +538,13 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
     const int key = wave_max_i32(accepted ? dep * 128 + (127 - lane) : -1);
     const int klen = key < 0 ? 0 : key / 128;
     const int best = key < 0 ? -1 : 127 - key % 128;
-    const uint64_t path = shfl64(anc, best < 0 ? 0 : best);
+    // best is uniform over the wave (a wave maximum): read its lane directly
+    const int bsrc = __builtin_amdgcn_readfirstlane(best < 0 ? 0 : best);
+    const uint64_t path =
+        (static_cast<uint64_t>(__builtin_amdgcn_readlane(static_cast<uint32_t>(anc >> 32), bsrc)) << 32) |
+        __builtin_amdgcn_readlane(static_cast<uint32_t>(anc), bsrc);
     const int bt = best + 1;  // the terminal's argmax row: the bonus token
-    const int bonus_lo = __shfl(am_lo, bt & 63, PTD_WAVE);
+    const int bonus_lo = __builtin_amdgcn_readlane(am_lo, __builtin_amdgcn_readfirstlane(bt & 63));
     const int bonus = bt < kWaveNodes ? bonus_lo : am_hi;
     int32_t* an = accept_nodes + static_cast<size_t>(b) * T;
     int32_t* ot = out_tokens + static_cast<size_t>(b) * (T + 1);
