@@ -28,6 +28,7 @@
 // block-wide exclusive scans of child counts.
 //
 // One workgroup per sequence; the tree is staged in LDS once.
+#include "ptd_async.hpp"
 #include "ptd_common.hpp"
 
 namespace {
@@ -424,7 +425,7 @@ k_verify_expand(const int32_t* __restrict__ argmax, const int32_t* __restrict__ 
 //   - expansion: children masks by LDS atomic OR; a node's added candidates
 //     as a bit set over its top-k row; breadth-first positions level by
 //     level: the nodes of a level write their child counts at their
-//     positions, a scan over the wave (7 ballots: counts stay below 128)
+//     positions, a scan over the wave (DPP row shifts and broadcasts)
 //     gives every node its first child's position, and old children add
 //     their rank among their siblings to their parent's
 // Wave reductions use DPP and the gfx950 lane swaps (VALU only); gathers
@@ -453,20 +454,21 @@ __device__ __forceinline__ int wave_max_i32(int x) {
   return max(static_cast<int>(r32[0]), static_cast<int>(r32[1]));
 }
 
-// Exclusive prefix sum over the lanes of c in [0, 128), and the total: one
-// ballot per bit, counted below the lane with mbcnt.
-__device__ __forceinline__ int wave_excl_scan7(int c, int* total) {
-  int x = 0, t = 0;
-#pragma unroll
-  for (int bit = 0; bit < 7; ++bit) {
-    const uint64_t m = __ballot((c >> bit) & 1);
-    const int below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
-                                                __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0));
-    x += below << bit;
-    t += __popcll(m) << bit;
-  }
-  *total = t;
-  return x;
+// Exclusive prefix sum over the lanes, and the total, on the vector ALU:
+// an inclusive scan within each row of 16 lanes by row_shr 1, 2, 4, 8 (lanes
+// shifted in from outside the row add 0), then the rows' totals carried by
+// row_bcast:15 (lane 15 of a row into the next row: rows 1 and 3) and
+// row_bcast:31 (lane 31 into rows 2 and 3).
+__device__ __forceinline__ int wave_excl_scan(int c, int* total) {
+  int x = c;
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  *total = __builtin_amdgcn_readlane(x, 63);
+  return x - c;
 }
 
 template <bool VERIFY, bool EXPAND, int KM>
@@ -563,7 +565,7 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
 
   if (EXPAND) {
     if (live && par >= 0) atomicOr(reinterpret_cast<unsigned long long*>(&s_cm[par]), 1ull << lane);
-    __syncthreads();
+    ptd::lds_barrier();  // LDS only: the global stores need no wait
     const uint64_t cm = s_cm[lane];
     const int ncld = __popcll(cm);
     // candidates added under this node (bit r: topk row entry r)
@@ -610,10 +612,10 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
       // positions [lo, hi) hold this level; lane p of the scan is position lo + p
       const bool here = pos >= 0 && dep == level;
       if (here) s_cnt[pos] = ncld + nnew;
-      __syncthreads();
+      ptd::lds_barrier();  // LDS only: the global stores need no wait
       const int p = lo + lane;
       int total;
-      const int first = hi + wave_excl_scan7(p < hi ? s_cnt[p] : 0, &total);
+      const int first = hi + wave_excl_scan(p < hi ? s_cnt[p] : 0, &total);
       const int start = __shfl(first, here ? pos - lo : 0, PTD_WAVE);  // valid where here
       if (here) {  // added children: after the old ones, in candidate order
         int q = start + ncld;
@@ -628,9 +630,12 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
           }
         }
       }
+      // the parent's first-child position and its own position in one
+      // gather (start < 2^16 and -1 <= pos < 2^15)
       const int src = par >= 0 ? par : lane;
-      const int pstart = __shfl(start, src, PTD_WAVE);
-      const int ppos = __shfl(pos, src, PTD_WAVE);
+      const int pk = __shfl((start & 0xFFFF) | ((pos + 1) << 16), src, PTD_WAVE);
+      const int pstart = pk & 0xFFFF;
+      const int ppos = (pk >> 16) - 1;
       if (live && par >= 0 && dep == level + 1 && ppos >= 0) {  // the parent is on this level
         const int q = pstart + srank;
         if (q < T_max) {
