@@ -11,7 +11,7 @@
  *                        (ptd_tree_attention_ragged: trees of different sizes
  *                        in one padded batch; ptd_tree_attention_paged: the
  *                        same on paged caches; ptd_tree_attention_fp8kv: on
- *                        8-bit E4M3 key/value caches)
+ *                        8-bit E4M3 key/value caches; _paged_fp8kv: both)
  *   ptd_topk_argmax      per-row argmax / top-k of the verification logits
  *   ptd_verify           greedy longest accepted path (+ bonus token)
  *   ptd_expand           progressive expansion with top-k children
@@ -238,6 +238,19 @@ int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv, const int32_
                              const ptd_attn_shape* shape, const uint64_t* mask,
                              void* workspace, size_t workspace_bytes, int32_t* dev_status,
                              void* stream);
+
+/*
+ * ptd_tree_attention_paged_fp8kv -- ptd_tree_attention_fp8kv on paged caches:
+ * kv->k_pages / v_pages hold E4M3 codes, [num_pages][Hkv][page_size][D]
+ * bytes, addressed through the page table as in ptd_tree_attention_paged;
+ * k_scale / v_scale as in ptd_tree_attention_fp8kv.  Errors: the union of the
+ * two calls' checks.
+ */
+int ptd_tree_attention_paged_fp8kv(const void* q, const ptd_kv_pages* kv, const float* k_scale,
+                                   const float* v_scale, const int32_t* kv_len,
+                                   const int32_t* tree_len, const int32_t* parent, int32_t T,
+                                   void* out, const ptd_attn_shape* shape, void* workspace,
+                                   size_t workspace_bytes, int32_t* dev_status, void* stream);
 
 size_t ptd_topk_workspace_bytes(int32_t R, int32_t V, int32_t k);
 

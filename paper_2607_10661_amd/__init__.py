@@ -73,6 +73,9 @@ _SIGS = {
                                   ctypes.c_int),
     "ptd_tree_attention_fp8kv": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp,
                                   ctypes.POINTER(AttnShape), _vp, _sz, _vp, _vp], ctypes.c_int),
+    "ptd_tree_attention_paged_fp8kv": ([_vp, ctypes.POINTER(KVPages), _vp, _vp, _vp, _vp, _vp,
+                                        _i32, _vp, ctypes.POINTER(AttnShape), _vp, _sz, _vp,
+                                        _vp], ctypes.c_int),
     "ptd_tree_attention_paged": ([_vp, ctypes.POINTER(KVPages), _vp, _vp, _vp, _i32, _vp,
                                   ctypes.POINTER(AttnShape), _vp, _vp, _sz, _vp, _vp],
                                  ctypes.c_int),
@@ -178,6 +181,17 @@ def ptd_tree_attention_fp8kv(q, k_cache, v_cache, k_scale, v_scale, kv_len, tree
                                          _ptr(workspace), workspace_bytes, _ptr(dev_status),
                                          _stream(stream)),
            "ptd_tree_attention_fp8kv")
+
+
+def ptd_tree_attention_paged_fp8kv(q, kv: KVPages, k_scale, v_scale, kv_len, tree_len, parent, T,
+                                   out, shape: AttnShape, workspace=None, workspace_bytes=0,
+                                   dev_status=None, stream=None):
+    _check(_lib.ptd_tree_attention_paged_fp8kv(_ptr(q), ctypes.byref(kv), _ptr(k_scale),
+                                               _ptr(v_scale), _ptr(kv_len), _ptr(tree_len),
+                                               _ptr(parent), T, _ptr(out), ctypes.byref(shape),
+                                               _ptr(workspace), workspace_bytes, _ptr(dev_status),
+                                               _stream(stream)),
+           "ptd_tree_attention_paged_fp8kv")
 
 
 def ptd_tree_attention_paged(q, kv: KVPages, kv_len, tree_len, parent, T, out, shape: AttnShape,
@@ -397,10 +411,11 @@ def tree_attention_fp8kv(q, k_cache, v_cache, k_scale, v_scale, kv_len, parent, 
 
 def tree_attention_paged(q, k_pages, v_pages, page_table, kv_len, parent, out=None,
                          out_dtype=None, scale: float = 0.0, workspace=None, dev_status=None,
-                         tree_len=None):
-    """k_pages, v_pages [num_pages][Hkv][page_size][D] (bf16), page_table
-    int32 [B][max_pages]; otherwise as tree_attention."""
-    _need_gpu(q, k_pages, v_pages, page_table, kv_len, parent, tree_len)
+                         tree_len=None, k_scale=None, v_scale=None):
+    """k_pages, v_pages [num_pages][Hkv][page_size][D] (bf16, or uint8 E4M3
+    codes with optional k_scale / v_scale [Hkv]), page_table int32
+    [B][max_pages]; otherwise as tree_attention."""
+    _need_gpu(q, k_pages, v_pages, page_table, kv_len, parent, tree_len, k_scale, v_scale)
     B, T, Hq, D = q.shape
     num_pages, Hkv, ps, _ = k_pages.shape
     max_pages = page_table.shape[1]
@@ -415,8 +430,13 @@ def tree_attention_paged(q, k_pages, v_pages, page_table, kv_len, parent, out=No
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
     kv = KVPages(k_pages.data_ptr(), v_pages.data_ptr(), page_table.data_ptr(), ps, max_pages,
                  num_pages)
-    ptd_tree_attention_paged(q, kv, kv_len, tree_len, parent, T, out, shape, None, workspace,
-                             0 if workspace is None else workspace.numel(), dev_status)
+    wsb = 0 if workspace is None else workspace.numel()
+    if k_pages.dtype == torch.uint8:
+        ptd_tree_attention_paged_fp8kv(q, kv, k_scale, v_scale, kv_len, tree_len, parent, T, out,
+                                       shape, workspace, wsb, dev_status)
+    else:
+        ptd_tree_attention_paged(q, kv, kv_len, tree_len, parent, T, out, shape, None, workspace,
+                                 wsb, dev_status)
     return out
 
 

@@ -1267,13 +1267,10 @@ extern "C" int ptd_tree_attention_fp8kv(const void* q, const void* k_cache, cons
                         k_scale, v_scale);
 }
 
-extern "C" int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv,
-                                        const int32_t* kv_len, const int32_t* tree_len,
-                                        const int32_t* parent, int32_t T,
-                                        void* out, const ptd_attn_shape* shape,
-                                        const uint64_t* mask, void* workspace,
-                                        size_t workspace_bytes, int32_t* dev_status,
-                                        void* stream) {
+namespace {
+
+// Checks of a page description; the page-size shift on success.
+int paged_args(const ptd_kv_pages* kv, const ptd_attn_shape* shape, int* shift) {
   PTD_RETURN_IF(!kv || !shape, PTD_ERR_NULL);
   PTD_RETURN_IF(!kv->k_pages || !kv->v_pages || !kv->page_table, PTD_ERR_NULL);
   PTD_RETURN_IF(shape->in_dtype != PTD_BF16, PTD_ERR_DTYPE);  // the MFMA path only
@@ -1281,9 +1278,43 @@ extern "C" int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv,
   PTD_RETURN_IF(ps < 32 || ps > (1 << 20) || (ps & (ps - 1)) != 0, PTD_ERR_SHAPE);
   PTD_RETURN_IF(kv->max_pages < 1 || kv->num_pages < 1, PTD_ERR_SHAPE);
   PTD_RETURN_IF(static_cast<long long>(kv->max_pages) * ps != shape->L_cap, PTD_ERR_SHAPE);
+  int sh = 0;
+  while ((1 << sh) < ps) ++sh;
+  *shift = sh;
+  return PTD_OK;
+}
+
+}  // namespace
+
+extern "C" int ptd_tree_attention_paged(const void* q, const ptd_kv_pages* kv,
+                                        const int32_t* kv_len, const int32_t* tree_len,
+                                        const int32_t* parent, int32_t T,
+                                        void* out, const ptd_attn_shape* shape,
+                                        const uint64_t* mask, void* workspace,
+                                        size_t workspace_bytes, int32_t* dev_status,
+                                        void* stream) {
   int shift = 0;
-  while ((1 << shift) < ps) ++shift;
+  const int rc = paged_args(kv, shape, &shift);
+  if (rc != PTD_OK) return rc;
   return attention_impl(q, kv->k_pages, kv->v_pages, kv_len, tree_len, parent, T, out, shape, mask,
                         workspace, workspace_bytes, dev_status, stream, kv->page_table, shift,
                         kv->max_pages, kv->num_pages);
+}
+
+extern "C" int ptd_tree_attention_paged_fp8kv(const void* q, const ptd_kv_pages* kv,
+                                              const float* k_scale, const float* v_scale,
+                                              const int32_t* kv_len, const int32_t* tree_len,
+                                              const int32_t* parent, int32_t T, void* out,
+                                              const ptd_attn_shape* shape, void* workspace,
+                                              size_t workspace_bytes, int32_t* dev_status,
+                                              void* stream) {
+  int shift = 0;
+  const int rc = paged_args(kv, shape, &shift);
+  if (rc != PTD_OK) return rc;
+  PTD_RETURN_IF(shape->D != 128, PTD_ERR_SHAPE);
+  PTD_RETURN_IF((k_scale && !ptd_aligned(k_scale, 4)) || (v_scale && !ptd_aligned(v_scale, 4)),
+                PTD_ERR_ALIGN);
+  return attention_impl(q, kv->k_pages, kv->v_pages, kv_len, tree_len, parent, T, out, shape,
+                        nullptr, workspace, workspace_bytes, dev_status, stream, kv->page_table,
+                        shift, kv->max_pages, kv->num_pages, true, k_scale, v_scale);
 }

@@ -113,6 +113,22 @@ def test_fp8kv_attention_validation():
     assert _err(A, FAKE, FAKE, FAKE, FAKE + 2, None, FAKE, None, FAKE, 64, FAKE, s) == 4
 
 
+def test_paged_fp8kv_attention_validation():
+    s = _shape(L=2048)
+    kv = P.KVPages(FAKE, FAKE, FAKE, 64, 32, 64)
+    A = P.ptd_tree_attention_paged_fp8kv
+    assert _err(A, FAKE, P.KVPages(FAKE, None, FAKE, 64, 32, 64), None, None, FAKE, None, FAKE,
+                64, FAKE, s) == 1
+    assert _err(A, FAKE, kv, None, None, FAKE, None, FAKE, 64, FAKE,
+                _shape(L=2048, dt=P.PTD_F32, od=P.PTD_F32)) == 3
+    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 48, 2048 // 48, 64), None, None, FAKE, None,
+                FAKE, 64, FAKE, s) == 2
+    assert _err(A, FAKE, P.KVPages(FAKE, FAKE, FAKE, 64, 16, 64), None, None, FAKE, None, FAKE,
+                64, FAKE, _shape(L=1024, D=64)) == 2
+    assert _err(A, FAKE, kv, FAKE + 2, None, FAKE, None, FAKE, 64, FAKE, s) == 4
+    assert _err(A, FAKE, kv, None, None, FAKE, None, FAKE, 64, FAKE, s) == 5
+
+
 def test_topk_verify_expand_mask_validation():
     assert _err(P.ptd_topk_argmax, None, P.PTD_BF16, 4, 100, 100, 4, FAKE) == 1
     assert _err(P.ptd_topk_argmax, FAKE, 5, 4, 100, 100, 4, FAKE) == 3

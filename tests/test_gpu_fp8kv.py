@@ -122,3 +122,34 @@ def test_fp8kv_gqa_long_context_sampled(P):
     ref = O.tree_attention_fp8kv(w.q, kq, vq, ks, vs, w.kv_len, w.parent, w.scale, rows=rows)
     for n, (b, h, i) in enumerate(rows):
         assert np.abs(got[b, i, h] - ref[n]).max() <= TOL, (b, h, i)
+
+
+@pytest.mark.parametrize("ps", [32, 128])
+def test_fp8kv_paged_matches_contiguous(P, ps):
+    # E4M3 caches scattered over pages through a random table: bit for bit the
+    # contiguous 8-bit call (same arithmetic), and within the bound of the oracle
+    rng = np.random.default_rng(30 + ps)
+    B, T, Hkv, L = 3, 24, 4, 1024
+    q, kq, ks, vq, vs = make(rng, B, T, 16, Hkv, L)
+    kv_len = np.array([0, 500, L - T], np.int32)
+    tl = np.array([24, 9, 17], np.int32)
+    parent = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    maxp = L // ps
+    table = rng.permutation(B * maxp + 3)[:B * maxp].reshape(B, maxp).astype(np.int32)
+    kp = rng.integers(0, 0x7E, (B * maxp + 3, Hkv, ps, 128)).astype(np.uint8)  # noise pages
+    vp = kp.copy()
+    for b in range(B):
+        for j in range(maxp):
+            kp[table[b, j]] = kq[b, :, j * ps:(j + 1) * ps]
+            vp[table[b, j]] = vq[b, :, j * ps:(j + 1) * ps]
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    paged = P.tree_attention_paged(cu(q), cu(kp), cu(vp), cu(table), cu(kv_len), cu(parent),
+                                   out_dtype=torch.float32, dev_status=st, tree_len=cu(tl),
+                                   k_scale=cu(ks), v_scale=cu(vs))
+    contig = run(P, q, kq, ks, vq, vs, kv_len, parent, tree_len=tl)
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    assert torch.equal(paged, contig)
+    ref = O.tree_attention_fp8kv(q, kq, vq, ks, vs, kv_len, parent, 1.0 / np.sqrt(128),
+                                 tree_len=tl)
+    assert np.abs(paged.cpu().numpy() - ref).max() <= TOL
