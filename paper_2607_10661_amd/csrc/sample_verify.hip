@@ -56,6 +56,29 @@ __device__ __forceinline__ double shfl_up_f64(double x, int d) {
   const uint32_t hi = __shfl_up(static_cast<uint32_t>(u >> 32), d, PTD_WAVE);
   return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
 }
+// One DPP step of a wave scan on an fp64 value (both halves moved with the
+// same control; lanes outside the row or the row mask receive +0.0).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = __double_as_longlong(x);
+  const uint32_t lo = static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u)), CTRL, ROWS, 0xF, false));
+  const uint32_t hi = static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(u >> 32)), CTRL, ROWS, 0xF, false));
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+// Inclusive prefix sum over the wave on the vector ALU: row_shr 1, 2, 4, 8
+// within rows of 16 lanes, then row_bcast:15 (into rows 1 and 3) and
+// row_bcast:31 (into rows 2 and 3).
+__device__ __forceinline__ double wave_incl_scan_f64(double x) {
+  x += dpp_f64<0x111, 0xF>(x);
+  x += dpp_f64<0x112, 0xF>(x);
+  x += dpp_f64<0x114, 0xF>(x);
+  x += dpp_f64<0x118, 0xF>(x);
+  x += dpp_f64<0x142, 0xA>(x);
+  x += dpp_f64<0x143, 0xC>(x);
+  return x;
+}
 __device__ __forceinline__ double readlane_f64(double x, int lane) {
   const uint64_t u = __double_as_longlong(x);
   const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(u), lane);
@@ -399,12 +422,7 @@ __global__ void __launch_bounds__(kWalkThreads) k_verify_sample(SampleArgs a) {
     const bool in_b = yb < V && !((L.bits[yb >> 5] >> (yb & 31)) & 1u);
     const double ea = in_a ? term(ya) : 0.0, eb = in_b ? term(yb) : 0.0;
     const double own = ea + eb;
-    double incl = own;
-#pragma unroll
-    for (int d = 1; d < PTD_WAVE; d <<= 1) {
-      const double o = shfl_up_f64(incl, d);
-      if (lane >= d) incl += o;
-    }
+    const double incl = wave_incl_scan_f64(own);
     double excl = shfl_up_f64(incl, 1);
     if (lane == 0) excl = 0.0;
     if (lane == 63) L.wsum[wave] = incl;
