@@ -153,3 +153,20 @@ def test_fp8kv_paged_matches_contiguous(P, ps):
     ref = O.tree_attention_fp8kv(q, kq, vq, ks, vs, kv_len, parent, 1.0 / np.sqrt(128),
                                  tree_len=tl)
     assert np.abs(paged.cpu().numpy() - ref).max() <= TOL
+
+
+def test_fp8kv_tree_over_128_nodes_with_tree_len(P):
+    rng = np.random.default_rng(40)
+    B, T, L = 2, 144, 700
+    q, kq, ks, vq, vs = make(rng, B, T, 8, 2, L)
+    kv_len = np.array([300, 0], np.int32)
+    tl = np.array([144, 100], np.int32)
+    parent = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    parent[1, 100:] = 500  # padding parents: never read
+    got = run(P, q, kq, ks, vq, vs, kv_len, parent, tree_len=tl).cpu().numpy()
+    assert np.all(got[1, 100:] == 0.0)
+    rows = [(0, 7, 143), (0, 2, 129), (1, 5, 99), (1, 0, 1)]
+    ref = O.tree_attention_fp8kv(q, kq, vq, ks, vs, kv_len, parent, 1.0 / np.sqrt(128),
+                                 tree_len=tl, rows=rows)
+    for n, (b, h, i) in enumerate(rows):
+        assert np.abs(got[b, i, h] - ref[n]).max() <= TOL, (b, h, i)

@@ -204,3 +204,40 @@ def test_ragged_paged_matches_contiguous(P):
     got = contig.float().cpu().numpy()
     ref = O.tree_attention(q, kc, vc, kvl, par, 1.0 / np.sqrt(D), tree_len=tl)
     assert np.abs(got - ref).max() <= 8e-3  # bf16 outputs: half an ulp at |x| < 2
+
+
+def test_ragged_fp32_tree_over_128_nodes(P):
+    # vector-ALU path with masks built from tree_len
+    rng = np.random.default_rng(11)
+    q, kc, vc, kvl, tl, par = make_case(rng, 2, 140, 2, 2, 64, [30, 5], [140, 66], dtype="f32")
+    rows = [(0, 1, 139), (0, 0, 70), (1, 1, 65), (1, 0, 0)]
+    check(P, q, kc, vc, kvl, tl, par, rows=rows, tol=TOL_F32)
+
+
+def test_ragged_paged_tree_over_128_nodes(P):
+    # paged caches, masks built from tree_len, padding pages never read
+    rng = np.random.default_rng(12)
+    B, T, Hkv, D, ps = 2, 160, 2, 128, 32
+    q, kc, vc, kvl, tl, par = make_case(rng, B, T, 4, Hkv, D, [64, 300], [160, 90])
+    L = (kc.shape[2] + ps - 1) // ps * ps
+    pad = ((0, 0), (0, 0), (0, L - kc.shape[2]), (0, 0))
+    kc, vc = np.pad(kc, pad), np.pad(vc, pad)
+    maxp = L // ps
+    table = rng.permutation(B * maxp)[:B * maxp].reshape(B, maxp).astype(np.int32)
+    kp = np.zeros((B * maxp, Hkv, ps, D), np.uint16)
+    vp = np.zeros_like(kp)
+    for b in range(B):
+        for j in range(maxp):
+            kp[table[b, j]] = kc[b, :, j * ps:(j + 1) * ps]
+            vp[table[b, j]] = vc[b, :, j * ps:(j + 1) * ps]
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    paged = P.tree_attention_paged(cu(q), cu(kp), cu(vp), cu(table), cu(kvl), cu(par),
+                                   out_dtype=torch.float32, dev_status=st, tree_len=cu(tl))
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    got = paged.cpu().numpy()
+    assert np.all(got[1, 90:] == 0.0)
+    rows = [(0, 3, 159), (0, 1, 128), (1, 2, 89), (1, 0, 3)]
+    ref = O.attention_rows(q, kc, vc, kvl, par, 1.0 / np.sqrt(D), rows, tree_len=tl)
+    for n, (b, h, i) in enumerate(rows):
+        assert np.abs(got[b, i, h] - ref[n]).max() <= TOL_BF16, (b, h, i)
