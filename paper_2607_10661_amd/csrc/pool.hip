@@ -111,6 +111,7 @@ k_step_prune(const int32_t* __restrict__ parent, const int32_t* __restrict__ tok
              int32_t* __restrict__ tree_len_next, int32_t* dev_status) {
   __shared__ int s_h[kMaxNodes], s_fc[kMaxNodes], s_rootof[kMaxNodes];
   __shared__ unsigned long long s_cm[kMaxNodes];
+  __shared__ unsigned long long s_U[kMaxNodes + 1];
   __shared__ unsigned long long s_nr;
   const int lane = threadIdx.x, b = blockIdx.x;
   int n = T;
@@ -148,12 +149,20 @@ k_step_prune(const int32_t* __restrict__ parent, const int32_t* __restrict__ tok
   }
   const int dep = __popcll(anc);
   // depth of the sub-tree under each node: max over its descendants w of
-  // dep(w) - dep(v) + 1
-  int h = live ? 1 : 0;
-  for (int w = 0; w < n; ++w) {
-    const uint64_t aw = rl64(anc, w);
-    const int dw = rl(dep, w);
-    if (live && ((aw >> lane) & 1ull)) h = max(h, dw - dep + 1);
+  // dep(w) - dep(v) + 1.  U[d], the union of the ancestor-or-self sets of the
+  // nodes at depth d, holds exactly the nodes with a descendant at depth d;
+  // v's descendants fill every level from dep(v) down to its deepest one,
+  // so h(v) counts the consecutive levels d >= dep(v) with v in U[d].
+  s_U[lane] = 0ull;
+  if (lane == 0) s_U[kMaxNodes] = 0ull;
+  __syncthreads();
+  if (live) atomicOr(&s_U[dep], static_cast<unsigned long long>(anc));
+  __syncthreads();
+  int h = 0;
+  if (live) {
+    int d = dep;  // v itself is in U[dep]
+    while (d < kMaxNodes && ((s_U[d + 1] >> lane) & 1ull)) ++d;
+    h = d - dep + 1;
   }
   s_h[lane] = h;
   s_cm[lane] = 0ull;
