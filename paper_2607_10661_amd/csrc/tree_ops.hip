@@ -480,8 +480,9 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
             int32_t* __restrict__ out_tokens, int32_t* __restrict__ parent_next,
             int32_t* __restrict__ tokens_next, int32_t* __restrict__ tree_len_next,
             int32_t* dev_status) {
-  __shared__ int s_tok[kWaveNodes], s_cnt[kWaveNodes];
+  __shared__ int s_cnt[kWaveNodes];
   __shared__ uint64_t s_cm[kWaveNodes];
+  __shared__ uint32_t s_dup[kWaveNodes];
   __shared__ int s_width[PTD_MAX_DEPTH];
   const int lane = threadIdx.x, b = blockIdx.x;
   const int n = live_nodes(tree_len, b, T);
@@ -506,9 +507,9 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
   }
   const int par = live ? par_in : -1;
   const int tok = live ? tok_in : 0;
-  s_tok[lane] = tok;
   s_cm[lane] = 0ull;
   s_cnt[lane] = 0;
+  s_dup[lane] = 0u;
 
   if (__any(live && (par < -1 || par >= lane))) {  // not topological
     if (lane == 0) ptd::report(dev_status, PTD_ERR_BAD_TREE);
@@ -564,7 +565,18 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
   }
 
   if (EXPAND) {
-    if (live && par >= 0) atomicOr(reinterpret_cast<unsigned long long*>(&s_cm[par]), 1ull << lane);
+    // children masks, and each child marks the entries of its parent's top-k
+    // row that repeat its own token (the parent's row gathered by shuffles)
+    uint32_t mydup = 0;
+#pragma unroll
+    for (int r = 0; r < KM; ++r) {
+      const int pc = __shfl(cand[r], par >= 0 ? par : lane, PTD_WAVE);
+      mydup |= (pc == tok) ? (1u << r) : 0u;
+    }
+    if (live && par >= 0) {
+      atomicOr(reinterpret_cast<unsigned long long*>(&s_cm[par]), 1ull << lane);
+      atomicOr(&s_dup[par], mydup);
+    }
     ptd::lds_barrier();  // LDS only: the global stores need no wait
     const uint64_t cm = s_cm[lane];
     const int ncld = __popcll(cm);
@@ -572,12 +584,7 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
     uint32_t sel = 0;
     if (live && dep + 1 <= d_max) {
       const int cap = s_width[dep];
-      uint32_t dup = 0;
-      for (uint64_t m = cm; m; m &= m - 1ull) {  // existing children's tokens
-        const int t = s_tok[__ffsll(static_cast<long long>(m)) - 1];
-#pragma unroll
-        for (int r = 0; r < KM; ++r) dup |= (cand[r] == t) ? (1u << r) : 0u;
-      }
+      const uint32_t dup = s_dup[lane];  // entries equal to an existing child's token
       int have = ncld;
 #pragma unroll
       for (int r = 0; r < KM; ++r) {
