@@ -427,7 +427,7 @@ size_t ptd_verify_sample_workspace_bytes(int32_t B, int32_t T, int32_t V);
 
 /*
  * ptd_verify_sample -- sampling verification of the tree (Sec. 3.2 "sampling
- * decoding strategy"; App. B recursive candidate-tree sampling; App. C proof
+ * decoding strategy"; App. E recursive candidate-tree sampling; App. F proof
  * of distributional consistency).  P_v = softmax(row of v / temperature),
  * row 0 being the last committed token n_0 and row v+1 node v.  From n_0 the
  * children of the current node v are examined in index order; child n with

@@ -27,9 +27,9 @@
  *                          keys and values become the next committed rows.
  *   oracle_e4m3_decode     value of an OCP FP8 E4M3 code (keys and values
  *                          cached in 8 bits, a serving format: not in the paper).
- *   oracle_verify_sample   Sec. 3.2 sampling decoding strategy; App. B
+ *   oracle_verify_sample   Sec. 3.2 sampling decoding strategy; App. E
  *                          recursive candidate-tree sampling, normalized as in
- *                          the proof of App. C.
+ *                          the proof of App. F.
  *
  * Error returns: 0 = ok, 7 = malformed tree (parent[i] outside [-1, i)),
  * 2 = bad sizes, 8 = kv_len outside [0, L_cap - T], 9 = accepted path not
@@ -528,15 +528,15 @@ int oracle_kv_commit(void* k_cache, void* v_cache, int dtype, const int32_t* kv_
 }
 
 /* ---------------------------------------------------------------------------
- * Sampling verification (Sec. 3.2 "sampling decoding strategy"; App. B,
- * recursive candidate-tree sampling; App. C, distributional consistency).
+ * Sampling verification (Sec. 3.2 "sampling decoding strategy"; App. E,
+ * recursive candidate-tree sampling; App. F, distributional consistency).
  * P_v = softmax(logits row of v / temperature) over the vocabulary; row 0 is
  * the last committed token n_0 (the parent of every root), row v + 1 is
  * node v.  Starting at n_0, the children of the current node v are examined
  * in index order.  Child n (token t_n) is accepted iff
  *     u_node[n] < P_v[t_n] / S,
  * where S is the mass of P_v not yet rejected at v (S = 1 before the first
- * child; App. C divides by it).  A rejected child's token gets probability 0
+ * child; App. F divides by it).  A rejected child's token gets probability 0
  * (S drops by its old value), so a later sibling with the same token is never
  * accepted.  On acceptance the walk moves to n; when every child of v is
  * rejected, v is the terminal and the bonus token is drawn from the residual

@@ -1,12 +1,12 @@
 // Sampling verification of a draft tree (Sec. 3.2 "sampling decoding
-// strategy"; App. B recursive candidate-tree sampling; App. C proof of
+// strategy"; App. E recursive candidate-tree sampling; App. F proof of
 // distributional consistency).
 //
 // P_v = softmax(logits row of v / temperature); row 0 is the last committed
 // token n_0 (the parent of every root), row v + 1 is node v.  From n_0 the
 // children of the current node are examined in index order; child n (token
 // t_n) is accepted iff u_node[n] < P_v[t_n] / S, S being the mass of P_v not
-// yet rejected at this node (App. C divides by it).  A rejected token's
+// yet rejected at this node (App. F divides by it).  A rejected token's
 // probability becomes 0, so a later sibling with the same token is rejected.
 // On acceptance the walk moves to n; when every child is rejected the node is
 // the terminal and the bonus token is drawn by inverse CDF (index order) from

@@ -796,7 +796,7 @@ def test_kv_commit_rejects_bad_paths(al, nodes, kv):
 
 
 # ---------------------------------------------------------------------------
-# sampling verification (App. B / App. C)
+# sampling verification (App. E / App. F)
 # ---------------------------------------------------------------------------
 def _chi2_ok(counts, probs, n):
     """Pearson chi-square of observed counts against n * probs; accepts at a
@@ -819,7 +819,7 @@ def _replicate(parent, tokens, rows, n):
 
 
 def test_sample_first_token_follows_the_model_distribution():
-    # App. C: every candidate is selected with its own probability, and the
+    # App. F: every candidate is selected with its own probability, and the
     # fallback draw covers the rest, so the first emitted token ~ P_root.
     # Logits are logs of chosen probabilities (temperature 1).
     P0 = np.array([0.30, 0.25, 0.20, 0.10, 0.10, 0.05])
