@@ -72,7 +72,9 @@ typedef enum {
   PTD_ERR_KV_LEN = 8,    /* device-detected: kv_len < 0 or kv_len + T > L_cap */
   PTD_ERR_BAD_PATH = 9,  /* device-detected: accepted path not strictly increasing
                             node ids in [0, T), or its length outside [0, T] */
-  PTD_ERR_PAGE = 10      /* device-detected: a page id outside [0, num_pages) */
+  PTD_ERR_PAGE = 10,     /* device-detected: a page id outside [0, num_pages) */
+  PTD_ERR_SCRATCH = 11   /* the problem needs more scratch than the fixed array of
+                            ptd_tree_attention_noalloc (PTD_NOALLOC_SCRATCH_BYTES) */
 } ptd_status;
 
 /* Dimension pairs turned together by the rotary embedding. */
@@ -84,6 +86,7 @@ typedef enum {
 #define PTD_MAX_T 1024   /* tree nodes per sequence */
 #define PTD_MAX_K 16     /* top-k */
 #define PTD_MAX_DEPTH 64 /* entries of a width schedule */
+#define PTD_NOALLOC_SCRATCH_BYTES (64u << 20) /* device scratch of ptd_tree_attention_noalloc */
 
 /* Attention problem description (host struct, read during the call only). */
 typedef struct {
@@ -208,7 +211,31 @@ int ptd_tree_attention_fp8kv(const void* q, const void* k_cache, const void* v_c
                              const ptd_attn_shape* shape, void* workspace,
                              size_t workspace_bytes, int32_t* dev_status, void* stream);
 
-/* Workspace bytes ptd_topk_argmax needs (0 on invalid arguments). */
+/*
+ * ptd_tree_attention_noalloc -- ptd_tree_attention_ragged for callers that
+ * cannot allocate device memory or pass a workspace (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).  Same
+ * operation, arguments (tree_len may be NULL), results and dev_status codes
+ * as ptd_tree_attention_ragged, without the workspace arguments: the split
+ * partials and, when needed, the ancestor masks go to a fixed device array of
+ * PTD_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds on each GPU it
+ * runs on until the process ends.  The call allocates nothing and clears
+ * nothing (the scratch needs no initialisation).  Every call on one GPU
+ * shares that GPU's array: calls that overlap on one GPU (several streams or
+ * host threads) race and their outputs are unspecified; calls ordered on one
+ * stream are safe.  ptd_tree_attention_workspace_bytes(shape, T) is the
+ * scratch a problem needs (the masks' share only with T > 128 or fp32
+ * inputs, when mask is NULL).
+ * Errors: those of ptd_tree_attention_ragged except PTD_ERR_WORKSPACE;
+ * PTD_ERR_SCRATCH if the problem needs more than PTD_NOALLOC_SCRATCH_BYTES;
+ * PTD_ERR_HIP if the array's device address cannot be obtained.
+ */
+int ptd_tree_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                               const int32_t* kv_len, const int32_t* tree_len,
+                               const int32_t* parent, int32_t T, void* out,
+                               const ptd_attn_shape* shape, const uint64_t* mask,
+                               int32_t* dev_status, void* stream);
+
 /* Paged key/value caches (host struct, read during the call only). */
 typedef struct {
   const void* k_pages;        /* [num_pages][Hkv][page_size][D] in_dtype */
@@ -252,6 +279,7 @@ int ptd_tree_attention_paged_fp8kv(const void* q, const ptd_kv_pages* kv, const 
                                    void* out, const ptd_attn_shape* shape, void* workspace,
                                    size_t workspace_bytes, int32_t* dev_status, void* stream);
 
+/* Workspace bytes ptd_topk_argmax needs (0 on invalid arguments). */
 size_t ptd_topk_workspace_bytes(int32_t R, int32_t V, int32_t k);
 
 /*

@@ -30,7 +30,8 @@ PTD_MAX_T, PTD_MAX_K, PTD_MAX_DEPTH = 1024, 16, 64
 STATUS = {0: "PTD_OK", 1: "PTD_ERR_NULL", 2: "PTD_ERR_SHAPE", 3: "PTD_ERR_DTYPE",
           4: "PTD_ERR_ALIGN", 5: "PTD_ERR_WORKSPACE", 6: "PTD_ERR_HIP",
           7: "PTD_ERR_BAD_TREE", 8: "PTD_ERR_KV_LEN", 9: "PTD_ERR_BAD_PATH",
-          10: "PTD_ERR_PAGE"}
+          10: "PTD_ERR_PAGE", 11: "PTD_ERR_SCRATCH"}
+PTD_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class PTDError(RuntimeError):
@@ -71,6 +72,8 @@ _SIGS = {
     "ptd_tree_attention_ragged": ([_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp,
                                    ctypes.POINTER(AttnShape), _vp, _vp, _sz, _vp, _vp],
                                   ctypes.c_int),
+    "ptd_tree_attention_noalloc": ([_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp,
+                                    ctypes.POINTER(AttnShape), _vp, _vp, _vp], ctypes.c_int),
     "ptd_tree_attention_fp8kv": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp,
                                   ctypes.POINTER(AttnShape), _vp, _sz, _vp, _vp], ctypes.c_int),
     "ptd_tree_attention_paged_fp8kv": ([_vp, ctypes.POINTER(KVPages), _vp, _vp, _vp, _vp, _vp,
@@ -170,6 +173,15 @@ def ptd_tree_attention_ragged(q, k_cache, v_cache, kv_len, tree_len, parent, T, 
                                           ctypes.byref(shape), _ptr(mask), _ptr(workspace),
                                           workspace_bytes, _ptr(dev_status), _stream(stream)),
            "ptd_tree_attention_ragged")
+
+
+def ptd_tree_attention_noalloc(q, k_cache, v_cache, kv_len, tree_len, parent, T, out,
+                               shape: AttnShape, mask=None, dev_status=None, stream=None):
+    _check(_lib.ptd_tree_attention_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_len),
+                                           _ptr(tree_len), _ptr(parent), T, _ptr(out),
+                                           ctypes.byref(shape), _ptr(mask), _ptr(dev_status),
+                                           _stream(stream)),
+           "ptd_tree_attention_noalloc")
 
 
 def ptd_tree_attention_fp8kv(q, k_cache, v_cache, k_scale, v_scale, kv_len, tree_len, parent, T,

@@ -14,6 +14,7 @@ extern "C" const char* ptd_status_string(int status) {
     case PTD_ERR_KV_LEN: return "kv_len < 0 or kv_len + T > L_cap";
     case PTD_ERR_BAD_PATH: return "accepted path: length outside [0, T] or node ids not strictly increasing in [0, T)";
     case PTD_ERR_PAGE: return "page id outside [0, num_pages)";
+    case PTD_ERR_SCRATCH: return "problem needs more than the 64 MiB scratch of ptd_tree_attention_noalloc";
     default: return "unknown status";
   }
 }

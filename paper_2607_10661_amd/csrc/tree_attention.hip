@@ -25,6 +25,7 @@
 //   k_attn_valu    fp32 (or bf16) inputs on the vector ALUs, fp32 throughout.
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "ptd_async.hpp"
@@ -1136,6 +1137,38 @@ extern "C" size_t ptd_tree_attention_workspace_bytes(const ptd_attn_shape* shape
   return pl.total_bytes;
 }
 
+// ---------------------------------------------------------------------------
+// Allocation-free variant: the scratch is a fixed device array.  In host code
+// `scratch` names a host-side stand-in, never the device memory: its device
+// address is looked up once per GPU (hipGetSymbolAddress with that GPU
+// current) and only that address is handed to kernels.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[PTD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of the current GPU's scratch array (null on failure).
+void* scratch_device_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+      (void)hipGetLastError();  // clear the sticky error of the failed lookup
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
 namespace {
 
 // The attention call on contiguous caches (page_table null) or paged ones.
@@ -1146,7 +1179,7 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
                    size_t workspace_bytes, int32_t* dev_status, void* stream,
                    const int32_t* page_table, int page_shift, int max_pages, int num_pages,
                    bool f8 = false, const float* k_scale = nullptr,
-                   const float* v_scale = nullptr) {
+                   const float* v_scale = nullptr, bool noalloc = false) {
   PTD_RETURN_IF(!q || !k_cache || !v_cache || !kv_len || !parent || !out || !shape,
                 PTD_ERR_NULL);
   if (shape->in_dtype != PTD_F32 && shape->in_dtype != PTD_BF16) return PTD_ERR_DTYPE;
@@ -1160,6 +1193,12 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
                 PTD_ERR_ALIGN);
   const bool build_mask = pl.needs_mask && !mask;
   const size_t need = pl.partial_bytes + (build_mask ? pl.mask_bytes : 0);
+  if (noalloc && need > 0) {  // the fixed scratch array stands in for the workspace
+    PTD_RETURN_IF(need > PTD_NOALLOC_SCRATCH_BYTES, PTD_ERR_SCRATCH);
+    workspace = scratch_device_ptr();
+    PTD_RETURN_IF(!workspace, PTD_ERR_HIP);
+    workspace_bytes = PTD_NOALLOC_SCRATCH_BYTES;
+  }
   if (need > 0) {
     PTD_RETURN_IF(!workspace, PTD_ERR_WORKSPACE);
     PTD_RETURN_IF(workspace_bytes < need, PTD_ERR_WORKSPACE);
@@ -1253,6 +1292,16 @@ extern "C" int ptd_tree_attention_ragged(const void* q, const void* k_cache, con
                                          int32_t* dev_status, void* stream) {
   return attention_impl(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape, mask,
                         workspace, workspace_bytes, dev_status, stream, nullptr, 0, 0, 0);
+}
+
+extern "C" int ptd_tree_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                          const int32_t* kv_len, const int32_t* tree_len,
+                                          const int32_t* parent, int32_t T, void* out,
+                                          const ptd_attn_shape* shape, const uint64_t* mask,
+                                          int32_t* dev_status, void* stream) {
+  return attention_impl(q, k_cache, v_cache, kv_len, tree_len, parent, T, out, shape, mask,
+                        nullptr, 0, dev_status, stream, nullptr, 0, 0, 0, false, nullptr, nullptr,
+                        true);
 }
 
 extern "C" int ptd_tree_attention_fp8kv(const void* q, const void* k_cache, const void* v_cache,

@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(0, 11):
+    for code in range(0, 12):
         assert P.ptd_status_string(code) != "unknown status"
     assert P.ptd_status_string(99) == "unknown status"
     assert P.ptd_version() >= 100
@@ -100,6 +100,24 @@ def test_ragged_attention_validation():
     assert _err(A, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, _shape(Hq=3, Hkv=2)) == 2
     assert _err(A, FAKE + 2, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 4
     assert _err(A, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, s) == 5  # no workspace
+
+
+def test_noalloc_attention_validation():
+    s = _shape()
+    A = P.ptd_tree_attention_noalloc
+    assert _err(A, None, FAKE, FAKE, FAKE, None, FAKE, 64, FAKE, s) == 1
+    assert _err(A, FAKE, FAKE, FAKE, FAKE, None, FAKE, 0, FAKE, s) == 2
+    assert _err(A, FAKE, FAKE, FAKE, FAKE, None, FAKE, 64, FAKE, _shape(Hq=3, Hkv=2)) == 2
+    assert _err(A, FAKE + 2, FAKE, FAKE, FAKE, None, FAKE, 64, FAKE, s) == 4
+    # 600 trees of 1024 nodes: their ancestor masks alone (78.6 MB) exceed the
+    # fixed scratch; rejected before anything is looked up or launched
+    big = _shape(B=600, Hq=1, Hkv=1, D=64, L=2048)
+    assert P.ptd_tree_attention_workspace_bytes(big, 1024) > P.PTD_NOALLOC_SCRATCH_BYTES
+    assert _err(A, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1024, FAKE, big) == 11
+    # the workloads' own problems fit (ragged-16's split partials: 34 MB)
+    for shp, T in ((_shape(), 64), (_shape(B=16, Hkv=8, L=8256), 64),
+                   (_shape(Hkv=8, L=32832), 64), (_shape(Hq=40, Hkv=40, L=4192), 96)):
+        assert 0 < P.ptd_tree_attention_workspace_bytes(shp, T) <= P.PTD_NOALLOC_SCRATCH_BYTES
 
 
 def test_fp8kv_attention_validation():
