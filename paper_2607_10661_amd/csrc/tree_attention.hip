@@ -50,9 +50,10 @@ using u32x2 = uint32_t __attribute__((ext_vector_type(2)));
 constexpr int kThreads = 512;   // 8 waves: two per SIMD
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;  // running-max start: finite, below any score
-// Sequences with at least this many keys carry the softmax weights p as
-// bf16 into the PV product; shorter ones as bf16 hi + lo (see k_attn_mfma).
-constexpr int kPlainKeys = 512;
+// A query block of a tile in which some softmax weight p exceeds this
+// fraction of its query row's sum so far carries p into the PV product as
+// bf16 hi + lo rather than bf16 (see k_attn_mfma).
+constexpr float kPreciseFrac = 1.0f / 16.0f;
 
 struct AttnParams {
   const void* q;
@@ -574,7 +575,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[qb][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  auto exp_tile = [&](const Tile& x, float (&pv)[QB][8], float (&ps)[QB]) __attribute__((always_inline)) {
+  // exponentials of a tile, and the largest of each lane's eight
+  auto exp_tile = [&](const Tile& x, float (&pv)[QB][8], float (&pm)[QB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
@@ -582,9 +584,21 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         pv[qb][e] = __builtin_amdgcn_exp2f(fmaf(x.s[0][qb][e], c, nmc[qb]));
         pv[qb][4 + e] = __builtin_amdgcn_exp2f(fmaf(x.s[1][qb][e], c, nmc[qb]));
       }
-      ps[qb] = ((pv[qb][0] + pv[qb][1]) + (pv[qb][2] + pv[qb][3])) +
-               ((pv[qb][4] + pv[qb][5]) + (pv[qb][6] + pv[qb][7]));
+      pm[qb] = fmaxf(fmaxf(fmaxf(pv[qb][0], pv[qb][1]), fmaxf(pv[qb][2], pv[qb][3])),
+                     fmaxf(fmaxf(pv[qb][4], pv[qb][5]), fmaxf(pv[qb][6], pv[qb][7])));
     }
+  };
+  // sum of the eight bf16 values of f added to acc (v_dot2 with ones; each
+  // pair taken by an explicit shuffle: element extraction through a bit cast
+  // of the packed vector fed the same dword to every v_dot2)
+  using bf16x2 = __bf16 __attribute__((ext_vector_type(2)));
+  const bf16x2 one2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+  auto rowsum = [&](float acc, bf16x8 f) __attribute__((always_inline)) -> float {
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 0, 1), one2, acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 2, 3), one2, acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 4, 5), one2, acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 6, 7), one2, acc, false);
+    return acc;
   };
   // rare: move the reference of rows whose maximum passed it (uniform over
   // the row's four lanes)
@@ -613,51 +627,24 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     }
   };
   // p of a tile as bf16 MFMA operands (B of O^T += V^T P^T: lane holds its
-  // query column's 8 keys); with `precise` also the rounding residue p - bf16(p)
+  // query column's 8 keys); for precise query blocks also the rounding
+  // residue p - bf16(p)
   struct PFrag {
     bf16x8 hi[QB], lo[QB];
   };
-  auto softmax = [&](const Tile& x, bool precise) __attribute__((always_inline)) -> PFrag {
-    float pv[QB][8], ps[QB];
-    exp_tile(x, pv, ps);
-    bool over = false;
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) over |= !(ps[qb] <= 65536.0f);
-    if (__any(over)) {
-      move_ref(x);
-      exp_tile(x, pv, ps);
-    }
-    PFrag f;
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      u32x4 ph, pl;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[qb][2 * w], pv[qb][2 * w + 1]);
-      if (precise) {
-#pragma unroll
-        for (int w = 0; w < 4; ++w)
-          pl[w] = ptd::cvt_pk_bf16(pv[qb][2 * w] - ptd::bf16_lo(ph[w]),
-                                   pv[qb][2 * w + 1] - ptd::bf16_hi(ph[w]));
-        f.lo[qb] = __builtin_bit_cast(bf16x8, pl);
-      }
-      lsum[qb] += ps[qb];
-      f.hi[qb] = __builtin_bit_cast(bf16x8, ph);
-    }
-    return f;
-  };
-  auto pv_acc = [&](const VFrag& v, const PFrag& f, bool precise) __attribute__((always_inline)) {
+  auto pv_acc = [&](const VFrag& v, const PFrag& f, unsigned precise) __attribute__((always_inline)) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
         o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v.v[dt], f.hi[qb], o[qb][dt], 0, 0, 0);
-    if (precise) {
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+    for (int qb = 0; qb < QB; ++qb)
+      if (precise & (1u << qb)) {
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
+        for (int dt = 0; dt < DT; ++dt)
           o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v.v[dt], f.lo[qb], o[qb][dt], 0, 0, 0);
-    }
+      }
   };
 
   // ---- rounds.  Round rd holds sub-tiles rd*WK .. rd*WK + WK - 1 (wave kg
@@ -670,40 +657,49 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   //      rd - 1 are free there and refilled right away.  Round rd + 1's data
   //      is then issued by round rd - 1, which needs 3*WK ring slots; with
   //      more key groups a round computes its own sub-tile start to end.
-  //      P is carried as bf16 when the sequence has at least kPlainKeys keys
-  //      (the softmax weight is then spread over many keys and bf16 rounding
-  //      of p moves the output by well under 1e-3); shorter sequences, where
-  //      a few keys can hold all the weight, carry p as bf16 hi + lo.
+  //      The denominator adds the same bf16 p that enter O, so that O is
+  //      the exact average of V under the rounded weights.  A query block
+  //      of a tile in which some p exceeds kPreciseFrac of its row's sum so
+  //      far (this wave's keys, the four lanes of the query column added)
+  //      carries p as bf16 hi + lo (residue at most 2^-16 p instead of
+  //      2^-8 p): every key carried as plain bf16 then weighs at most
+  //      kPreciseFrac of its row's final sum, so the 2^-8 relative rounding
+  //      of a dominant key, or of a few large ones, never reaches O.
   constexpr bool PIPE = 3 * WK <= R::NS;
   static_assert((2 + (PIPE ? 1 : 0)) * WK <= R::NS, "round data issued one round ahead");
-  const bool precise = N < kPlainKeys;  // uniform over the workgroup
-  // bf16 p of scores x (exponentials pv and their lane sums ps computed)
-  auto to_p = [&](const Tile& x, float (&pv)[QB][8], float (&ps)[QB]) __attribute__((always_inline))
-      -> PFrag {
+  // bf16 p of scores x (exponentials pv and lane maxima pm computed);
+  // returns the mask of precise query blocks (residues in f.lo)
+  auto to_p = [&](const Tile& x, float (&pv)[QB][8], float (&pm)[QB], PFrag& f)
+      __attribute__((always_inline)) -> unsigned {
     bool over = false;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) over |= !(ps[qb] <= 65536.0f);
+    for (int qb = 0; qb < QB; ++qb) over |= !(pm[qb] <= 65536.0f);
     if (__any(over)) {
       move_ref(x);
-      exp_tile(x, pv, ps);
+      exp_tile(x, pv, pm);
     }
-    PFrag f;
+    unsigned pmask = 0;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+      pmask |= __any(!(pm[qb] <= kPreciseFrac * sum_xor32(sum_xor16(lsum[qb])))) ? (1u << qb) : 0u;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
+      const bool precise = pmask & (1u << qb);
       u32x4 ph, pl;
 #pragma unroll
       for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[qb][2 * w], pv[qb][2 * w + 1]);
+      f.hi[qb] = __builtin_bit_cast(bf16x8, ph);
+      lsum[qb] = rowsum(lsum[qb], f.hi[qb]);
       if (precise) {
 #pragma unroll
         for (int w = 0; w < 4; ++w)
-          pl[w] = ptd::cvt_pk_bf16(pv[qb][2 * w] - ptd::bf16_lo(ph[w]),
-                                   pv[qb][2 * w + 1] - ptd::bf16_hi(ph[w]));
+          pl[w] = ptd::cvt_pk_bf16(pv[qb][2 * w] - static_cast<float>(f.hi[qb][2 * w]),
+                                   pv[qb][2 * w + 1] - static_cast<float>(f.hi[qb][2 * w + 1]));
         f.lo[qb] = __builtin_bit_cast(bf16x8, pl);
+        lsum[qb] = rowsum(lsum[qb], f.lo[qb]);
       }
-      lsum[qb] += ps[qb];
-      f.hi[qb] = __builtin_bit_cast(bf16x8, ph);
     }
-    return f;
+    return pmask;
   };
 
   for (int t = 0; t < ninit; ++t) issue(t, t);
@@ -754,7 +750,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     if (ns >= R::NS) ns -= R::NS;
     const int j = rd * WK + kg;
     if (wave_live && j < ntiles) {
-      float pv[QB][8], ps[QB];
+      float pv[QB][8], pm[QB];
       if constexpr (PIPE) {
         // next K reads in flight while this sub-tile's exponentials run (they
         // overlap the previous round's PV MFMAs, still executing); then the
@@ -763,8 +759,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         // holds and its result is dropped: one code path keeps the register
         // allocation of this loop within the two-waves-per-SIMD budget.
         const KFrag kf = read_k(ns);
-        exp_tile(sc, pv, ps);
-        const PFrag pf = to_p(sc, pv, ps);
+        exp_tile(sc, pv, pm);
+        PFrag pf;
+        const unsigned precise = to_p(sc, pv, pm, pf);
         Tile sn = qk(kf);
         const VFrag vf = read_v(cs);
         pv_acc(vf, pf, precise);
@@ -774,8 +771,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         sc = qk(read_k(cs));
         mask_tile(sc, j);
         const VFrag vf = read_v(cs);
-        exp_tile(sc, pv, ps);
-        const PFrag pf = to_p(sc, pv, ps);
+        exp_tile(sc, pv, pm);
+        PFrag pf;
+        const unsigned precise = to_p(sc, pv, pm, pf);
         pv_acc(vf, pf, precise);
       }
     }

@@ -410,6 +410,53 @@ def test_attention_configs_sampled(P, name):
     assert np.isfinite(got).all()
 
 
+def _dominant_case(seed, B, kvl, Hq, Hkv, T, n_dom, extra):
+    """Inputs where n_dom keys per KV head hold much of the softmax weight of
+    the head's query rows: the keys point along the mean query direction,
+    scaled so that for the median row their scores lead the unit-variance
+    scores of the other keys by log(1.65 kv_len) + extra (a lead of
+    log(1.65 kv_len) alone gives one such key about half the weight)."""
+    rng = np.random.default_rng(seed)
+    D, G = 128, Hq // Hkv
+    par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)]).astype(np.int32)
+    q = rng.standard_normal((B, T, Hq, D)).astype(np.float32)
+    kc = rng.standard_normal((B, Hkv, kvl + T, D)).astype(np.float32)
+    vc = (rng.standard_normal((B, Hkv, kvl + T, D)) * 2.0).astype(np.float32)
+    lead = np.log(1.65 * kvl) + extra
+    for b in range(B):
+        for g in range(Hkv):
+            rows = q[b, :, g * G:(g + 1) * G].reshape(-1, D)
+            qs = rows.sum(0)
+            qs /= np.linalg.norm(qs)
+            alpha = lead / np.median(rows @ qs / np.sqrt(D))
+            for d in range(n_dom):
+                j = int(rng.integers(40, kvl))
+                kc[b, g, j] = qs * alpha * (1.0 + 0.02 * d)
+    return (W.f32_to_bf16_bits(q), W.f32_to_bf16_bits(kc), W.f32_to_bf16_bits(vc),
+            np.full(B, kvl, np.int32), par)
+
+
+# (seed, B, kv_len, Hq, Hkv, T, keys holding the weight, extra lead).  Some
+# run through several KV splits (long sequences, few heads).
+DOMINANT = [(1, 1, 1024, 8, 8, 16, 1, 0.0), (3, 2, 1024, 8, 8, 16, 2, 1.0),
+            (5, 3, 700, 8, 8, 32, 2, 0.0), (2, 1, 2000, 32, 8, 64, 1, 1.0),
+            (6, 1, 1024, 4, 4, 4, 4, 2.0), (4, 2, 4096, 32, 8, 64, 2, 0.5),
+            (7, 1, 20000, 8, 8, 16, 1, 0.0), (8, 1, 30000, 8, 1, 1, 2, 1.0)]
+
+
+@pytest.mark.parametrize("case", DOMINANT)
+def test_attention_dominant_keys(P, case):
+    q, kc, vc, kvl, par = _dominant_case(*case)
+    ref = O.tree_attention(q, kc, vc, kvl, par, 1 / np.sqrt(128))
+    st = status_buf()
+    out = P.tree_attention(cu(q), cu(kc), cu(vc), cu(kvl), cu(par), out_dtype=torch.float32,
+                           dev_status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 0
+    err = np.abs(out.cpu().numpy().astype(np.float64) - ref).max()
+    assert err <= TOL["bf16"], (case, err)
+
+
 def test_attention_deterministic(P):
     w = W.make_workload(_spec(Hq=32, Hkv=8, T=64, kv_len=3000), seed=9, logits=False)
     a = _attn_gpu(P, w, out_dtype=torch.float32)
