@@ -228,15 +228,14 @@ def main():
     sp_pn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
     sp_tn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
     sp_ln = torch.empty(B, dtype=torch.int32, device=dev)
-    pool_e, pool_n = 2048, 64
+    pool_e, pool_n = 2048, w.T_max + 1  # a retrieved tree can fill the draft
     pool_bytes = P.ptd_pool_bytes(B, pool_e, pool_n)
     pool = torch.empty(pool_bytes, dtype=torch.uint8, device=dev)
     P.ptd_pool_init(pool, pool_bytes, B, pool_e, pool_n, stream=sp)
     bonus = torch.gather(ot, 1, al.long().view(B, 1)).view(B).contiguous()
-    rt_pn = torch.empty((B, 64), dtype=torch.int32, device=dev)
-    rt_tn = torch.empty((B, 64), dtype=torch.int32, device=dev)
+    rt_pn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
+    rt_tn = torch.empty((B, w.T_max), dtype=torch.int32, device=dev)
     rt_ln = torch.empty(B, dtype=torch.int32, device=dev)
-    small_tree = w.T_max <= 64
 
     def prune(i):
         P.ptd_step_prune(pn, tn, ln, B, w.T_max, d_prune, w.T_max, sp_pn, sp_tn, sp_ln, status, sp)
@@ -245,8 +244,8 @@ def main():
         P.ptd_pool_merge(pool, pool_bytes, B, pool_e, pool_n, pn, tn, ln, w.T_max, status, sp)
 
     def retrieve(i):
-        P.ptd_pool_retrieve(pool, pool_bytes, B, pool_e, pool_n, bonus, 64, rt_pn, rt_tn, rt_ln,
-                            sp)
+        P.ptd_pool_retrieve(pool, pool_bytes, B, pool_e, pool_n, bonus, w.T_max, rt_pn, rt_tn,
+                            rt_ln, sp)
 
     # attention on paged caches: 64-row pages scattered through a random page
     # table (one table for all rotated sets), same inputs otherwise
@@ -312,10 +311,9 @@ def main():
 
         fp8_ms, _ = timed(attention_fp8, K)
     sample_ms, _ = timed(sample, K)
-    if small_tree:
-        prune_ms, _ = timed(prune, K)
-        merge_ms, _ = timed(merge, K)
-        retrieve_ms, _ = timed(retrieve, K)
+    prune_ms, _ = timed(prune, K)
+    merge_ms, _ = timed(merge, K)
+    retrieve_ms, _ = timed(retrieve, K)
     rope_ms, _ = timed(rope, K)
     commit_ms, _ = timed(commit, K)
     torch.cuda.synchronize()
@@ -441,19 +439,18 @@ def main():
             paged_ms, alg["attention"], "ptd_tree_attention_paged: the attention call on %d-row "
             "pages through a random page table (%d pages), %d back-to-back calls; contiguous: "
             "%.3f us" % (PS, num_pages, K, att_avg_s * 1e6))
-    if small_tree:
-        tree_b = B * w.T_max * 4 * 2
-        line["next_rows"].update({
-            "step_prune": next_row(prune_ms, 2 * tree_b, "ptd_step_prune of the expanded trees "
-                                   "(T_max %d) at d_max %d, %d back-to-back calls"
-                                   % (w.T_max, d_prune, K)),
-            "pool_merge": next_row(merge_ms, tree_b, "ptd_pool_merge of the expanded trees into "
-                                   "a pool of %d trees x %d nodes per sequence (first call grows "
-                                   "it, later calls find every node), %d back-to-back calls"
-                                   % (pool_e, pool_n, K)),
-            "pool_retrieve": next_row(retrieve_ms, tree_b, "ptd_pool_retrieve of the candidate "
-                                      "trees keyed by the bonus tokens, %d back-to-back calls" % K),
-        })
+    tree_b = B * w.T_max * 4 * 2
+    line["next_rows"].update({
+        "step_prune": next_row(prune_ms, 2 * tree_b, "ptd_step_prune of the expanded trees "
+                               "(T_max %d) at d_max %d, %d back-to-back calls"
+                               % (w.T_max, d_prune, K)),
+        "pool_merge": next_row(merge_ms, tree_b, "ptd_pool_merge of the expanded trees into "
+                               "a pool of %d trees x %d nodes per sequence (first call grows "
+                               "it, later calls find every node), %d back-to-back calls"
+                               % (pool_e, pool_n, K)),
+        "pool_retrieve": next_row(retrieve_ms, tree_b, "ptd_pool_retrieve of the candidate "
+                                  "trees keyed by the bonus tokens, %d back-to-back calls" % K),
+    })
     print(json.dumps(line), flush=True)
 
 

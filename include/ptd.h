@@ -505,7 +505,7 @@ int ptd_verify_sample(const void* logits, ptd_dtype dtype, int32_t V, int64_t ld
  * is renumbered breadth first (by depth; by the parent's new index; siblings
  * in old index order; roots in the order of the roots they replace) and cut
  * to T_max nodes; slots from tree_len_next on hold -1.
- *   parent, tokens  int32 [B][T], T 1 .. 64;  tree_len int32 [B] or NULL
+ *   parent, tokens  int32 [B][T], T 1 .. 128;  tree_len int32 [B] or NULL
  *   d_max           >= 1;  T_max 1 .. PTD_MAX_T
  *   parent_next, tokens_next  int32 [B][T_max];  tree_len_next int32 [B]
  * dev_status: PTD_ERR_BAD_TREE (that sequence's output is empty).
@@ -519,8 +519,8 @@ int ptd_step_prune(const int32_t* parent, const int32_t* tokens, const int32_t* 
 /*
  * Candidate pool (Sec. 3.1 "Draft Extraction via Merging"; Alg. 1 steps 1
  * and 4): per sequence, trees of tokens keyed by the token of their root, at
- * most e_max trees (1 .. 2048) of at most n_cap nodes (1 .. 64, root
- * included).  The pool is a caller-owned device buffer of ptd_pool_bytes
+ * most e_max trees (1 .. 2048) of at most n_cap nodes (1 .. 129, root
+ * included, so that a retrieved tree can fill 128 draft slots).  The pool is a caller-owned device buffer of ptd_pool_bytes
  * bytes, 256-byte aligned, set up once by ptd_pool_init; every call that
  * names it must pass the same B, e_max and n_cap.  Calls on one pool must not
  * overlap.  Returns 0 from ptd_pool_bytes on invalid arguments.
@@ -538,7 +538,7 @@ int ptd_pool_init(void* pool, size_t pool_bytes, int32_t B, int32_t e_max, int32
  * sub-tree's nodes are taken in index order (each after its parent), which
  * fixes the insertion order.  An insertion beyond n_cap nodes, or a new tree
  * beyond e_max trees, is skipped together with what it would carry.
- *   parent, tokens  int32 [B][T], T 1 .. 64;  tree_len int32 [B] or NULL
+ *   parent, tokens  int32 [B][T], T 1 .. 128;  tree_len int32 [B] or NULL
  * dev_status: PTD_ERR_BAD_TREE (that sequence's pool is left unchanged).
  * Errors: PTD_ERR_NULL, PTD_ERR_SHAPE, PTD_ERR_WORKSPACE (pool_bytes too
  * small), PTD_ERR_ALIGN, PTD_ERR_HIP.

@@ -224,20 +224,20 @@ def test_verify_sample_validation():
 
 def test_step_prune_and_pool_validation():
     assert P.ptd_pool_bytes(1, 0, 8) == 0 and P.ptd_pool_bytes(1, 2049, 8) == 0
-    assert P.ptd_pool_bytes(1, 8, 65) == 0 and P.ptd_pool_bytes(0, 8, 8) == 0
+    assert P.ptd_pool_bytes(1, 8, 130) == 0 and P.ptd_pool_bytes(0, 8, 8) == 0
     # 16-byte header, 64 hash slots (key + tree), 8 counts, 8 x 8 nodes, 256-rounded
     assert P.ptd_pool_bytes(1, 8, 8) == 1280 and P.ptd_pool_bytes(3, 8, 8) == 3 * 1280
     assert _err(P.ptd_step_prune, None, FAKE, None, 1, 8, 2, 8, FAKE, FAKE, FAKE) == 1
-    assert _err(P.ptd_step_prune, FAKE, FAKE, None, 1, 65, 2, 8, FAKE, FAKE, FAKE) == 2
+    assert _err(P.ptd_step_prune, FAKE, FAKE, None, 1, 129, 2, 8, FAKE, FAKE, FAKE) == 2
     assert _err(P.ptd_step_prune, FAKE, FAKE, None, 1, 8, 0, 8, FAKE, FAKE, FAKE) == 2
     nb = P.ptd_pool_bytes(2, 16, 8)
     assert _err(P.ptd_pool_init, None, nb, 2, 16, 8) == 1
     assert _err(P.ptd_pool_init, FAKE, nb - 1, 2, 16, 8) == 5
     assert _err(P.ptd_pool_init, FAKE + 16, nb, 2, 16, 8) == 4
-    assert _err(P.ptd_pool_merge, FAKE, nb, 2, 16, 8, FAKE, FAKE, None, 65) == 2
+    assert _err(P.ptd_pool_merge, FAKE, nb, 2, 16, 8, FAKE, FAKE, None, 129) == 2
     assert _err(P.ptd_pool_merge, FAKE, nb, 2, 16, 8, None, FAKE, None, 8) == 1
     assert _err(P.ptd_pool_retrieve, FAKE, nb, 2, 16, 8, FAKE, 0, FAKE, FAKE, FAKE) == 2
-    assert _err(P.ptd_pool_retrieve, FAKE, nb, 2, 16, 100, FAKE, 8, FAKE, FAKE, FAKE) == 2
+    assert _err(P.ptd_pool_retrieve, FAKE, nb, 2, 16, 130, FAKE, 8, FAKE, FAKE, FAKE) == 2
 
 
 def test_paged_attention_validation():

@@ -39,7 +39,7 @@ def trees(rng, B, T, kind):
     return np.stack(out)
 
 
-@pytest.mark.parametrize("T", [1, 7, 33, 64])
+@pytest.mark.parametrize("T", [1, 7, 33, 64, 65, 96, 128])
 @pytest.mark.parametrize("d_max", [1, 2, 3, 5])
 def test_step_prune_random(P, T, d_max):
     rng = np.random.default_rng(T * 10 + d_max)
@@ -103,6 +103,53 @@ def test_pool_bounds_drop_deterministically(P):
 
 def test_pool_many_tokens_full_trees(P):
     pool_case(P, np.random.default_rng(3), B=2, T=64, V=500, e_max=2048, n_cap=64, steps=3)
+
+
+@pytest.mark.parametrize("T,n_cap,V", [(65, 66, 30), (96, 97, 300), (128, 129, 40)])
+def test_pool_large_trees(P, T, n_cap, V):
+    # drafts of more than 64 nodes into trees of more than 64 nodes
+    pool_case(P, np.random.default_rng(T), B=3, T=T, V=V, e_max=2048, n_cap=n_cap, steps=3,
+              T_max=n_cap - 1)
+
+
+def test_pool_more_touched_trees_than_staged(P):
+    # about 120 distinct tokens per draft: the touched trees are staged in
+    # two batches
+    pool_case(P, np.random.default_rng(6), B=2, T=128, V=5000, e_max=2048, n_cap=129, steps=2,
+              T_max=128)
+
+
+def test_step_and_pool_13b_expanded_tree(P):
+    # the 96-node trees that expansion builds for the 13B workload: stepped,
+    # merged into a pool and retrieved by every token they hold
+    w = W.make_workload("llama2-13b")
+    B = w.B
+    _, idx, _ = O.topk(w.logits, w.k)
+    pn, tn, ln = O.expand(w.parent, w.tokens, idx.reshape(B, w.T + 1, w.k), w.width, w.d_max,
+                          w.T_max)
+    assert w.T_max == 96 and ln.max() > 64
+    for d_max in (1, 2, 3, w.d_max - 1):
+        ref = O.step_prune(pn, tn, d_max, w.T_max, ln)
+        st = torch.zeros(1, dtype=torch.int32, device="cuda")
+        got = P.step_prune(cu(pn), cu(tn), d_max, w.T_max, cu(ln), st)
+        torch.cuda.synchronize()
+        assert st.item() == 0
+        for r, g in zip(ref, got):
+            assert np.array_equal(g.cpu().numpy(), r), d_max
+    ref = O.Pool(B, 2048, w.T_max + 1)
+    gpu = P.Pool(B, 2048, w.T_max + 1)
+    for step in range(2):
+        ref.merge(pn, tn, ln)
+        st = torch.zeros(1, dtype=torch.int32, device="cuda")
+        gpu.merge(cu(pn), cu(tn), cu(ln), st)
+        torch.cuda.synchronize()
+        assert st.item() == 0
+        for key in np.unique(tn[tn >= 0])[:64]:
+            last = np.full(B, key, np.int32)
+            r = ref.retrieve(last, w.T_max)
+            g = gpu.retrieve(cu(last), w.T_max)
+            for a, c in zip(r, g):
+                assert np.array_equal(c.cpu().numpy(), a), (step, key)
 
 
 def test_pool_bad_tree_leaves_pool(P):
