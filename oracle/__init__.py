@@ -132,18 +132,30 @@ def tree_attention(q, k_cache, v_cache, kv_len, parent, scale: float,
 
 
 def attention_rows(q, k_cache, v_cache, kv_len, parent, scale: float, rows,
-                   tree_len=None):
-    """Selected outputs: rows is a list of (b, h, i); returns [len(rows)][D]."""
+                   tree_len=None, threads: int = 1):
+    """Selected outputs: rows is a list of (b, h, i); returns [len(rows)][D].
+    threads > 1 spreads the rows over a thread pool (each row is computed
+    alone, so the results do not depend on it)."""
     q, kc, vc, dt, kvl, par, B, T, Hq, Hkv, D, L = _attn_args(
         q, k_cache, v_cache, kv_len, parent)
     tl = None if tree_len is None else _c(tree_len, np.int32)
     lib = _load()
     out = np.zeros((len(rows), D), np.float64)
-    for n, (b, h, i) in enumerate(rows):
-        _check(lib.oracle_attention_row(
-            _p(q), _p(kc), _p(vc), dt, _p(kvl), _p(par), None if tl is None else _p(tl),
-            B, T, Hq, Hkv, D, L, float(scale), int(b), int(h), int(i),
-            out[n].ctypes.data_as(ctypes.c_void_p)))
+
+    def run(ns):
+        for n in ns:
+            b, h, i = rows[n]
+            _check(lib.oracle_attention_row(
+                _p(q), _p(kc), _p(vc), dt, _p(kvl), _p(par), None if tl is None else _p(tl),
+                B, T, Hq, Hkv, D, L, float(scale), int(b), int(h), int(i),
+                out[n].ctypes.data_as(ctypes.c_void_p)))
+
+    if threads <= 1 or len(rows) < 2:
+        run(range(len(rows)))
+    else:
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(threads) as ex:
+            list(ex.map(run, [range(j, len(rows), threads) for j in range(threads)]))
     return out
 
 
@@ -156,7 +168,7 @@ def e4m3_decode(codes) -> np.ndarray:
 
 
 def tree_attention_fp8kv(q, k_codes, v_codes, k_scale, v_scale, kv_len, parent,
-                         scale: float, tree_len=None, rows=None):
+                         scale: float, tree_len=None, rows=None, threads: int = 1):
     """Tree attention on E4M3 key/value caches [B][Hkv][L][D] with per-KV-head
     scales: key = value(code) * k_scale[g], likewise for values.  All outputs
     [B][T][Hq][D] (float64), or the selected (b, h, i) rows if given."""
@@ -169,7 +181,8 @@ def tree_attention_fp8kv(q, k_codes, v_codes, k_scale, v_scale, kv_len, parent,
         qd = (qd.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     if rows is None:
         return tree_attention(qd, kc, vc, kv_len, parent, scale, tree_len=tree_len)
-    return attention_rows(qd, kc, vc, kv_len, parent, scale, rows, tree_len=tree_len)
+    return attention_rows(qd, kc, vc, kv_len, parent, scale, rows, tree_len=tree_len,
+                          threads=threads)
 
 
 def topk(logits: np.ndarray, k: int):

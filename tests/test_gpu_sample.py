@@ -7,10 +7,12 @@ CDF from fp32 exponentials taken per block of 2048 entries and rescaled to
 the row maximum (each factor within ~1.2e-7 relative: one ulp of the hardware
 exp2, argument rounding compensated) summed in fp64, the oracle in fp64
 throughout, so a probability or cumulative probability may differ by ~5e-7
-at most.  Every sequence must therefore equal the oracle's result for
-the given uniforms, or for the same uniforms all shifted by +DELTA or -DELTA
-(a decision within rounding of its boundary going either way); the exact
-match must hold for nearly all of them.
+at most.  The oracle reports, per sequence, the smallest distance of a
+uniform from a boundary it was compared with (its margin).  A sequence whose
+margin exceeds DELTA must equal the oracle's result exactly; one with a
+smaller margin must equal it for the given uniforms, or for the same
+uniforms all shifted by +DELTA or -DELTA (a decision within rounding of its
+boundary going either way).
 """
 import numpy as np
 import pytest
@@ -53,9 +55,9 @@ def likely_tokens(rng, logits_f32, parent, top=3, p_random=0.2):
     return tok
 
 
-def sample_case(P, lg, tok, par, temp, u1, u2, tree_len=None, ld=None, min_exact=0.9):
+def sample_case(P, lg, tok, par, temp, u1, u2, tree_len=None, ld=None):
     B, T = par.shape
-    al_r, an_r, ot_r, _ = O.verify_sample(lg, tok, par, temp, u1, u2, tree_len)
+    al_r, an_r, ot_r, mg_r = O.verify_sample(lg, tok, par, temp, u1, u2, tree_len)
     V = lg.shape[-1]
     flat = lg.reshape(B * (T + 1), V)
     if ld is not None and ld > V:
@@ -70,12 +72,12 @@ def sample_case(P, lg, tok, par, temp, u1, u2, tree_len=None, ld=None, min_exact
     torch.cuda.synchronize()
     assert st.item() == 0
     al, an, ot = al.cpu().numpy(), an.cpu().numpy(), ot.cpu().numpy()
-    exact = 0
     lgb = lg.reshape(B, T + 1, V)
     for b in range(B):
         if al[b] == al_r[b] and np.array_equal(an[b], an_r[b]) and np.array_equal(ot[b], ot_r[b]):
-            exact += 1
             continue
+        assert mg_r[b] <= DELTA, (b, "differs although every decision is %.3g from its boundary"
+                                  % mg_r[b])
         ok = False
         for sgn in (1.0, -1.0):
             sl = slice(b, b + 1)
@@ -86,7 +88,6 @@ def sample_case(P, lg, tok, par, temp, u1, u2, tree_len=None, ld=None, min_exact
             if r[0][0] == al[b] and np.array_equal(r[1][0], an[b]) and np.array_equal(r[2][0], ot[b]):
                 ok = True
         assert ok, (b, al[b], al_r[b], ot[b][:al[b] + 2], ot_r[b][:al_r[b] + 2])
-    assert exact >= min_exact * B, f"{exact} of {B} sequences match the unshifted uniforms"
     return al_r, ot_r
 
 
@@ -107,15 +108,16 @@ def test_sample_random_trees(P, dtype, temp):
     assert al.max() >= 2  # the walks do go below the roots
 
 
-@pytest.mark.parametrize("name", ["llama2-7b", "llama3-8b-long", "ragged-16"])
+@pytest.mark.parametrize("name", ["llama2-7b", "llama2-13b", "llama3-8b-long", "ragged-16"])
 def test_sample_configs(P, name):
     w = W.make_workload(name)
     rng = np.random.default_rng(5)
     B, T = w.B, w.T
     lf = W.bf16_bits_to_f32(w.logits).reshape(B, T + 1, w.V)
     tok = likely_tokens(rng, lf, w.parent, top=2, p_random=0.1)
-    sample_case(P, w.logits.reshape(B, T + 1, w.V), tok, w.parent, 1.0, rng.random((B, T)),
-                rng.random((B, T + 1)), min_exact=0.0 if B == 1 else 0.8)
+    for draw in range(4):  # several draws of the uniforms
+        sample_case(P, w.logits.reshape(B, T + 1, w.V), tok, w.parent, 1.0, rng.random((B, T)),
+                    rng.random((B, T + 1)))
 
 
 def test_sample_wide_star_with_duplicates(P):
@@ -128,7 +130,7 @@ def test_sample_wide_star_with_duplicates(P):
     top = np.argsort(-x[:, 0], axis=-1)[:, :50]
     tok = np.stack([top[b, rng.integers(0, 50, T)] for b in range(B)]).astype(np.int32)
     u1 = rng.uniform(0.3, 1.0, (B, T))   # mostly rejections
-    sample_case(P, x, tok, par, 1.0, u1, rng.random((B, T + 1)), min_exact=0.5)
+    sample_case(P, x, tok, par, 1.0, u1, rng.random((B, T + 1)))
 
 
 def test_sample_chain_padding_and_strided_rows(P):
