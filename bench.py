@@ -29,7 +29,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-DEFAULT_WORKLOAD = "llama2-7b"
+DEFAULT_WORKLOAD = "ragged-16"
+# measured in the same run and reported as fields of the same line
+COMPANION_WORKLOADS = "llama3-8b-long"
 
 
 def parse():
@@ -38,6 +40,15 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--also", default=COMPANION_WORKLOADS,
+                    help="comma-separated workloads whose step and attention figures are "
+                         "measured after the main one and added to the line ('' for none)")
+    ap.add_argument("--plain", action="store_true",
+                    help="time only the step and the plain attention call of --workload (no "
+                         "next rows, companion workloads, decode shapes or CPU baseline): the "
+                         "run that kernel traces and counters are taken on")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the decode-shaped attention calls")
     ap.add_argument("--rotate-bytes", type=float, default=1.0 * 2**30,
                     help="total bytes of rotated input sets (cold-cache timing)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -85,6 +96,193 @@ def load_traffic(workload, per_launch_alg):
     return d.get("bytes_per_launch")
 
 
+def host_cpu():
+    """CPU model and the CPUs this process may run on (Linux)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        cpus = sorted(os.sched_getaffinity(0))
+    except AttributeError:
+        cpus = list(range(os.cpu_count() or 1))
+    ranges, start = [], None
+    for i, c in enumerate(cpus):
+        if start is None:
+            start = c
+        if i + 1 == len(cpus) or cpus[i + 1] != c + 1:
+            ranges.append(f"{start}-{c}" if c != start else f"{start}")
+            start = None
+    return model, ",".join(ranges), len(cpus)
+
+
+def cpu_baseline(args, name, w):
+    """The oracle timed on this host: whole steps (ancestor masks, attention
+    rows over a thread pool, top-k, verification, expansion) for at least
+    --cpu-seconds; and a one-thread rate estimated from a sample of the
+    attention rows (every 16th) plus the rest of a step."""
+    import concurrent.futures as cf
+
+    import numpy as np
+
+    import oracle as O
+    B, T, k = w.B, w.T, w.k
+    model, affinity, ncpu = host_cpu()
+    nth = max(1, min(16, ncpu))
+    rows_all = [(b, h, i) for b in range(B) for h in range(w.Hq) for i in range(T)]
+    chunks = [rows_all[j::nth] for j in range(nth)]
+
+    def rows_of(ch):
+        return O.attention_rows(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale, ch)
+
+    lg_rows = w.logits.reshape(-1, w.V)
+    lg_chunks = [lg_rows[j::nth] for j in range(nth)]
+
+    def rest(ex=None):
+        if ex is None:
+            r_am, r_idx, _ = O.topk(lg_rows, k)
+        else:  # logits rows over the pool, reassembled in row order
+            parts = list(ex.map(lambda c: O.topk(c, k), lg_chunks))
+            r_am = np.empty(lg_rows.shape[0], np.int32)
+            r_idx = np.empty((lg_rows.shape[0], k), np.int32)
+            for j, (a, ix, _) in enumerate(parts):
+                r_am[j::nth] = a
+                r_idx[j::nth] = ix
+        O.verify(r_am.reshape(B, -1), w.tokens, w.parent)
+        O.expand(w.parent, w.tokens, r_idx.reshape(B, T + 1, k), w.width, w.d_max, w.T_max)
+
+    with cf.ThreadPoolExecutor(nth) as ex:
+        done, t0 = 0, time.perf_counter()
+        while True:
+            O.tree_mask(w.parent)
+            list(ex.map(rows_of, chunks))
+            rest(ex)
+            done += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds or el * (done + 1) / done > 3 * args.cpu_seconds:
+                break
+    sample = rows_all[::16]
+    t0 = time.perf_counter()
+    O.tree_mask(w.parent)
+    rows_of(sample)
+    t_rows = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    rest()
+    t_rest = time.perf_counter() - t0
+    est = t_rows * len(rows_all) / len(sample) + t_rest
+    return {"value": round(B * T * done / el, 3), "unit": "tree tokens/s", "cores": nth,
+            "kind": "oracle",
+            "sample": f"{done} whole {name} step(s) (all {B * T} nodes x {w.Hq} heads; "
+                      f"attention rows and top-k rows over {nth} threads), {el:.1f} s",
+            "us_per_step": round(el / done * 1e6, 1),
+            "cpu_model": model, "affinity": affinity, "cpus_available": ncpu,
+            "single_thread": {"value": round(B * T / est, 3), "unit": "tree tokens/s",
+                              "cores": 1,
+                              "sample": f"every 16th attention row ({len(sample)} of "
+                                        f"{len(rows_all)}, {t_rows:.1f} s, scaled) + top-k, "
+                                        f"verify and expand ({t_rest:.2f} s)"}}
+
+
+def load_mfma(workload):
+    """MFMA busy share of the attention kernel from a committed rocprofv3
+    counter summary (None if absent or taken on another kernel source)."""
+    path = os.path.join(ROOT, "profiles", f"mfma_tree_attention_{workload}.json")
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except OSError:
+        return None
+    if d.get("kernel_source_sha") != kernel_source_hash():
+        return None
+    return {k: d[k] for k in ("mfma_util_pct", "kernel", "counters", "file") if k in d}
+
+
+# Decode-shaped attention calls: (name, B, T, Hq, Hkv, kv_len)
+DECODE_SHAPES = [("T1_mha_4096", 1, 1, 32, 32, 4096), ("T1_gqa_32768", 1, 1, 32, 8, 32768),
+                 ("T3_gqa_32768", 1, 3, 32, 8, 32768), ("T1_gqa_B16_8192", 16, 1, 32, 8, 8192)]
+
+
+def decode_calls(args):
+    """ptd_tree_attention on decode-sized calls (T = 1 to 3, fewer than 16 query
+    rows per KV head), against a device copy of the same key/value bytes
+    (each cold: input sets rotated).  The copy moves the bytes twice (read
+    and write); its rate is read + write bytes per second."""
+    import numpy as np
+    import torch
+
+    import paper_2607_10661_amd as P
+    import workloads as W
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    out = {}
+    for nm, B, T, Hq, Hkv, kvl in DECODE_SHAPES:
+        w = W.make_workload(dict(B=B, Hq=Hq, Hkv=Hkv, D=128, kv_len=kvl, T=T, tree="uniform",
+                                 V=16, dtype="bf16", plant=None, k=2), seed=3, logits=False)
+        def cu(a):
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(
+                torch.bfloat16)
+        q0, k0, v0 = cu(w.q), cu(w.k_cache), cu(w.v_cache)
+        set_b = (q0.numel() + k0.numel() + v0.numel()) * 2
+        R = max(2, min(64, math.ceil(args.rotate_bytes / set_b)))
+        sets = [(q0, k0, v0)] + [(q0.clone(), k0.clone(), v0.clone()) for _ in range(R - 1)]
+        kv_len, parent = cu_i(w.kv_len, dev), cu_i(w.parent, dev)
+        shape = P.attn_shape(q0, k0, out_dtype=q0.dtype)
+        ws = torch.empty(max(1, P.ptd_tree_attention_workspace_bytes(shape, T)),
+                         dtype=torch.uint8, device=dev)
+        o = torch.empty_like(q0)
+        st = torch.zeros(1, dtype=torch.int32, device=dev)
+        n = max(20, args.steps)
+
+        def att(i):
+            q, kc, vc = sets[i % R]
+            P.ptd_tree_attention(q, kc, vc, kv_len, parent, T, o, shape, None, ws, ws.numel(), st,
+                                 sp)
+        kv_bytes = 2 * B * Hkv * (kvl + T) * 128 * 2
+        dsts = [torch.empty(kv_bytes // 2, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+        srcs = [torch.cat([s[1].view(-1)[:kv_bytes // 4], s[2].view(-1)[:kv_bytes // 4]])
+                for s in sets[:R]]
+
+        def cp(i):
+            dsts[i % 2].copy_(srcs[i % R])
+        res = {}
+        for fn, key in ((att, "attention"), (cp, "copy")):
+            for i in range(5):
+                fn(i)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(20_000_000)
+            e0.record(stream)
+            for i in range(n):
+                fn(i)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            res[key] = e0.elapsed_time(e1) * 1e-3 / n
+        assert st.item() == 0, P.ptd_status_string(st.item())
+        alg = W.algorithmic_bytes(w)["attention"]
+        out[nm] = {"B": B, "T": T, "Hq": Hq, "Hkv": Hkv, "kv_len": kvl,
+                   "attention_us": round(res["attention"] * 1e6, 3), "alg_bytes": alg,
+                   "attention_GBps": round(alg / res["attention"] / 1e9, 1),
+                   "copy_us": round(res["copy"] * 1e6, 3),
+                   "copy_GBps": round(2 * kv_bytes / res["copy"] / 1e9, 1)}
+        del sets, srcs, dsts
+        torch.cuda.empty_cache()
+    return out
+
+
+def cu_i(a, dev):
+    import numpy as np
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
@@ -95,6 +293,20 @@ def main():
               "multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
+    line = run(args, args.workload, "plain" if args.plain else "full")
+    if not args.plain:
+        for wl in [x for x in args.also.split(",") if x and x != args.workload]:
+            line[wl] = run(args, wl, "companion")
+        if not args.no_decode:
+            line["decode"] = decode_calls(args)
+    print(json.dumps(line), flush=True)
+
+
+def run(args, name, mode):
+    """Measure one workload.  mode "full": the step, the attention call, every
+    next row and the CPU baseline; "plain": the step and the attention call
+    only; "companion": the same, returned as a field of the main line."""
+
     import numpy as np
     import torch
 
@@ -103,7 +315,7 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = W.make_workload(args.workload)
+    w = W.make_workload(name)
     B, T, k = w.B, w.T, w.k
 
     def cu(a):
@@ -185,6 +397,31 @@ def main():
     # the roofline's kernel: ptd_tree_attention alone, back to back, same inputs
     att_ms, _ = timed(attention, K)
     att_avg_s = att_ms * 1e-3
+    alg = W.algorithmic_bytes(w)
+    achieved = alg["attention"] / att_avg_s / 1e9
+    flops = W.attention_flops(w)
+    tokens_per_s = B * T / (ms_step * 1e-3)
+    traffic = load_traffic(name, alg["attention"])
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "kernel": "ptd_tree_attention (k_attn_mfma + k_attn_combine)",
+                "alg_bytes_per_launch": alg["attention"],
+                "basis": "algorithmic bytes of one call / average duration of %d back-to-back "
+                         "calls (HIP events on the launch stream); the kernel trace of "
+                         "bench.py --plain gives the two kernels' average durations, whose "
+                         "sum is this duration" % K}
+    config = {"workload": name, "B": B, "T": T, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D,
+              "kv_len": int(w.kv_len.max()) if B == 1 else w.kv_len.tolist(), "V": w.V, "k": k}
+    if mode != "full":
+        torch.cuda.synchronize()
+        res = {"config": config, "us_per_step": round(ms_step * 1e3, 3),
+               "tree_tokens_per_s": round(tokens_per_s, 1),
+               "attention_us": round(att_avg_s * 1e6, 3),
+               "attention_TBps": round(achieved / 1000, 3), "roofline": roofline,
+               "mfma_counters": load_mfma(name)}
+        del sets, base
+        torch.cuda.empty_cache()
+        return res
 
     # ptd_tree_rope and ptd_kv_commit on their own, after the step timings:
     # the rope turns q and the tree key rows of the rotated sets in place, the
@@ -326,62 +563,10 @@ def main():
         return {"us": round(ms * 1e3, 3), "alg_bytes": nbytes, "GBps": round(gbps, 1),
                 "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4), "what": what}
 
-    alg = W.algorithmic_bytes(w)
-    achieved = alg["attention"] / att_avg_s / 1e9
-    flops = W.attention_flops(w)
-    tokens_per_s = B * T / (ms_step * 1e-3)
-    traffic = load_traffic(args.workload, alg["attention"])
-
     # CPU oracle on a bounded sample of the same workload: whole steps
     cpu = None
     if args.cpu_seconds > 0:
-        import oracle as O
-        done, t_start = 0, time.perf_counter()
-        while True:
-            O.tree_mask(w.parent)
-            O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
-            r_am, r_idx, _ = O.topk(w.logits, k)
-            O.verify(r_am.reshape(B, -1), w.tokens, w.parent)
-            O.expand(w.parent, w.tokens, r_idx.reshape(B, T + 1, k), w.width, w.d_max,
-                     w.T_max)
-            done += 1
-            el = time.perf_counter() - t_start
-            if el >= args.cpu_seconds or el * (done + 1) / done > 3 * args.cpu_seconds:
-                break
-        cpu = {"value": round(B * T * done / el, 3), "unit": "tree tokens/s", "cores": 1,
-               "kind": "oracle",
-               "sample": f"{done} whole {args.workload} step(s) (all {B * T} nodes x "
-                         f"{w.Hq} heads, single thread), {el:.1f} s",
-               "us_per_step": round(el / done * 1e6, 1)}
-
-        # the same oracle on the host's cores (at most 16, the box's share): a
-        # step's attention rows spread over a thread pool (the oracle's C calls
-        # release the GIL); mask, top-k, verify and expand as above
-        import concurrent.futures as cf
-        nth = max(1, min(16, os.cpu_count() or 1))
-        rows_all = [(b, h, i) for b in range(B) for h in range(w.Hq) for i in range(T)]
-        chunks = [rows_all[j::nth] for j in range(nth)]
-
-        def rows_of(ch):
-            return O.attention_rows(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale, ch)
-
-        with cf.ThreadPoolExecutor(nth) as ex:
-            done_m, t_start = 0, time.perf_counter()
-            while True:
-                O.tree_mask(w.parent)
-                list(ex.map(rows_of, chunks))
-                r_am, r_idx, _ = O.topk(w.logits, k)
-                O.verify(r_am.reshape(B, -1), w.tokens, w.parent)
-                O.expand(w.parent, w.tokens, r_idx.reshape(B, T + 1, k), w.width, w.d_max,
-                         w.T_max)
-                done_m += 1
-                el_m = time.perf_counter() - t_start
-                if el_m >= args.cpu_seconds or el_m * (done_m + 1) / done_m > 3 * args.cpu_seconds:
-                    break
-        cpu["all_cores"] = {"value": round(B * T * done_m / el_m, 3), "unit": "tree tokens/s",
-                            "cores": nth,
-                            "sample": f"{done_m} whole step(s), attention rows over {nth} "
-                                      f"threads, {el_m:.1f} s"}
+        cpu = cpu_baseline(args, name, w)
 
     line = {
         "metric": "tree tokens/s (tree-attn + top-k + verify + expand step)",
@@ -397,20 +582,18 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic (seeded), cold cache: %d rotated input sets" % R,
-        "config": {"workload": args.workload, "B": B, "T": T, "Hq": w.Hq, "Hkv": w.Hkv,
-                   "D": w.D, "kv_len": int(w.kv_len.max()) if B == 1 else w.kv_len.tolist(),
-                   "V": w.V, "k": k},
+        "config": config,
         "attention_us": round(att_avg_s * 1e6, 3),
         "host_enqueue_us_per_step": round(host_step_s * 1e6, 1),
         "attention_timing": "ptd_tree_attention alone, %d back-to-back calls on the launch stream "
                             "(HIP events)" % K,
         "attention_TBps": round(achieved / 1000, 3),
-        "attention_mfma_frac": round(flops / att_avg_s / 2.5e15, 4),
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic,
-                     "kernel": "ptd_tree_attention (k_attn_mfma + k_attn_combine)",
-                     "alg_bytes_per_launch": alg["attention"]},
+        "attention_dense_flops_frac": round(flops / att_avg_s / 2.5e15, 4),
+        "attention_dense_flops_note": "4*T*Hq*(kv_len+T)*D per sequence (tree block counted "
+                                      "densely) / attention_us / 2.5 PFLOP/s; the MFMA busy "
+                                      "counter is under mfma_counters",
+        "mfma_counters": load_mfma(name),
+        "roofline": roofline,
         "cpu_baseline": cpu,
         "next_rows": {
             "tree_rope": next_row(rope_ms, rope_b, "ptd_tree_rope: positions kv_len+|pi(i)|-1, "
@@ -451,7 +634,9 @@ def main():
         "pool_retrieve": next_row(retrieve_ms, tree_b, "ptd_pool_retrieve of the candidate "
                                   "trees keyed by the bonus tokens, %d back-to-back calls" % K),
     })
-    print(json.dumps(line), flush=True)
+    del sets, base
+    torch.cuda.empty_cache()
+    return line
 
 
 if __name__ == "__main__":
