@@ -11,9 +11,10 @@
 // Kernels
 //   k_topk_row      one workgroup per (row, vocabulary slice), a slice being
 //                   at most 4096 chunks of 16 bytes (32768 bf16 or 16384
-//                   fp32 values) held in registers: a cheap lower bound of the
-//                   KMAX-th best value leaves a few candidates, ranked by
-//                   counting (details below).
+//                   fp32 values) held in registers (1024 threads x 4 chunks,
+//                   or 512 x 8 when there are many slices): a cheap lower
+//                   bound of the KMAX-th best value leaves a few candidates,
+//                   ranked by counting (details below).
 //   k_topk_scalar   rows that are not 16-byte aligned: one wave per (row,
 //                   slice) with element loads; each lane keeps a sorted list
 //                   of its KMAX best keys in registers.
@@ -131,8 +132,9 @@ __device__ __forceinline__ void store_part(uint64_t* part, int item, int kmax, i
   q[1] = key ? elem_bits<BF16>(row_base, key_index(key)) : 0u;
 }
 
-// One workgroup (16 waves) per (row, slice), a slice being at most one batch
-// of 4 chunks of 16 bytes per lane (64 KB), loaded straight into registers.
+// One workgroup of NT threads per (row, slice), a slice being at most one
+// batch of NL chunks of 16 bytes per lane (NT * NL * 16 bytes), loaded
+// straight into registers.
 //   1. Every lane takes the image of each of its chunks (bf16 images are 16
 //      bits wide and computed two at a time with packed 16-bit integer
 //      operations) and their maximum.
@@ -154,9 +156,6 @@ __device__ __forceinline__ void store_part(uint64_t* part, int item, int kmax, i
 // Only listed chunks pass through LDS, so the slice is read from memory once
 // and LDS carries a few KB.  The kernel's loops stay rolled, which keeps its
 // code small: its instructions are fetched once per CU, cold.
-constexpr int kRowThreads = 1024;
-constexpr int kBatchLoads = 4;                           // chunks per lane
-constexpr int kSliceChunks = kRowThreads * kBatchLoads;  // 64 KB
 constexpr int kCandCap = 256;                            // LDS candidate list
 constexpr int kListCap = 256;                            // LDS chunk list
 
@@ -239,14 +238,15 @@ __device__ __forceinline__ uint32_t group_max_min(uint32_t x) {
   return x;
 }
 
-template <int KMAX, bool BF16>
-__global__ void __launch_bounds__(kRowThreads)
+template <int KMAX, bool BF16, int NT, int NL>
+__global__ void __launch_bounds__(NT)
 k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int slice_len,
            int k, int32_t* __restrict__ argmax, int32_t* __restrict__ topk_idx,
            float* __restrict__ topk_val, uint64_t* __restrict__ part) {
   constexpr int E = BF16 ? 8 : 4;  // elements per 16-byte chunk
   constexpr int ES = BF16 ? 2 : 4;
-  constexpr int NW = kRowThreads / PTD_WAVE;
+  constexpr int NW = NT / PTD_WAVE;
+  static_assert(NT >= kCandCap && NW % 4 == 0 && NT * NL <= 65536, "workgroup shape");
   constexpr int GL = PTD_WAVE / KMAX;  // lanes per group
   __shared__ __attribute__((aligned(16))) uint4 s_ldata[kListCap];
   __shared__ uint64_t s_cand[kCandCap];
@@ -262,20 +262,20 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   const int v1 = min(V, v0 + slice_len);
   const char* rb = static_cast<const char*>(logits) + static_cast<size_t>(row) * ld * ES;
   const char* sb = rb + static_cast<size_t>(v0) * ES;  // the slice, 16-byte aligned
-  const int nfull = (v1 - v0) / E;  // whole chunks of the slice (at most kSliceChunks)
+  const int nfull = (v1 - v0) / E;  // whole chunks of the slice (at most NT * NL)
   const int vt = v0 + nfull * E + tid;  // the last partial chunk, one element per lane
   const bool tail = vt < v1;
 
-  // Chunk u of a lane is u * kRowThreads + tid (past the end: the slice's
+  // Chunk u of a lane is u * NT + tid (past the end: the slice's
   // last chunk, never examined); all loads are issued before any wait.
-  uint4 cw[kBatchLoads];
+  uint4 cw[NL];
   if (nfull > 0) {
     const uint4* src = reinterpret_cast<const uint4*>(sb);
 #pragma unroll
-    for (int u = 0; u < kBatchLoads; ++u) cw[u] = src[min(u * kRowThreads + tid, nfull - 1)];
+    for (int u = 0; u < NL; ++u) cw[u] = src[min(u * NT + tid, nfull - 1)];
   } else {
 #pragma unroll
-    for (int u = 0; u < kBatchLoads; ++u) cw[u] = make_uint4(0u, 0u, 0u, 0u);
+    for (int u = 0; u < NL; ++u) cw[u] = make_uint4(0u, 0u, 0u, 0u);
   }
   const uint32_t bt = tail ? elem_bits<BF16>(rb, vt) : 0u;
   if (tid < kCandCap) s_rank[tid] = 0;
@@ -285,11 +285,11 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   }
 
   // 1. chunk images and the lane maximum
-  uint32_t cm[kBatchLoads];
+  uint32_t cm[NL];
   uint32_t lm = tail ? elem_img<BF16>(bt) : 0u;
 #pragma unroll
-  for (int u = 0; u < kBatchLoads; ++u) {
-    cm[u] = u * kRowThreads + tid < nfull ? chunk_img<BF16>(cw[u]) : 0u;
+  for (int u = 0; u < NL; ++u) {
+    cm[u] = u * NT + tid < nfull ? chunk_img<BF16>(cw[u]) : 0u;
     lm = max(lm, cm[u]);
   }
   // 2. the bound: max over the lane groups, then min over the groups
@@ -313,12 +313,12 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
     }
   };
 #pragma unroll
-  for (int u = 0; u < kBatchLoads; ++u) {
+  for (int u = 0; u < NL; ++u) {
     if (cm[u] != 0 && cm[u] >= tc) {
       const int pos = atomicAdd(&s_nlist, 1);
       if (pos < kListCap) {
         s_ldata[pos] = cw[u];
-        s_list[pos] = static_cast<uint16_t>(u * kRowThreads + tid);
+        s_list[pos] = static_cast<uint16_t>(u * NT + tid);
       }
     }
   }
@@ -326,7 +326,7 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   ptd::lds_barrier();
   const int nl = s_nlist;
   if (nl <= kListCap) {  // uniform
-    for (int i0 = 0; i0 < nl; i0 += kRowThreads / E) {
+    for (int i0 = 0; i0 < nl; i0 += NT / E) {
       const int i = i0 + tid / E;
       if (i < nl) {
         const int c = s_list[i], e = tid & (E - 1);
@@ -343,7 +343,7 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   if (nl <= kListCap && n <= kCandCap) {  // uniform over the workgroup
     int n2 = PTD_WAVE;  // candidates per part-set: a power of two >= n
     while (n2 < n) n2 <<= 1;
-    const int parts = kRowThreads / n2;
+    const int parts = NT / n2;
     const int i = tid & (n2 - 1), p = tid / n2;  // p is uniform over a wave
     const int len = (n + parts - 1) / parts;
     const int j0 = p * len, j1 = min(n, j0 + len);
@@ -380,8 +380,8 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) l[j] = 0;
 #pragma unroll
-  for (int u = 0; u < kBatchLoads; ++u) {
-    const int c = u * kRowThreads + tid;
+  for (int u = 0; u < NL; ++u) {
+    const int c = u * NT + tid;
     if (c < nfull) {
       const int v = v0 + c * E;
 #pragma unroll
@@ -507,18 +507,37 @@ k_topk_merge(const void* __restrict__ logits, int V, long long ld, int slices, i
 
 struct TopkPlan {
   int kmax, slices, slice_len;
+  int nt, nl;  // k_topk_row: threads per workgroup, 16-byte chunks per lane
   bool vec;  // 16-byte aligned rows: k_topk_row, else k_topk_scalar
   size_t ws_bytes;
 };
+
+// Workgroup shape of k_topk_row for R rows of V elements (E per chunk).
+void topk_shape(int R, int V, int E, int* nt, int* nl) {
+  // Many slices (at least four per CU): 512 threads of 8 chunks each, three
+  // workgroups resident per CU and every lane's loads in flight at once
+  // (measured on 1040 rows x 128256 bf16: 53.2 us against 72.9 us for
+  // 1024 x 4).  Fewer: 1024 threads of 4 chunks, the shortest latency for a
+  // slice (65 rows x 32000: 5.1 us against 5.1-7.2 us for the others).
+  const long long slices_1024 = (static_cast<long long>(V) + 4096LL * E - 1) / (4096LL * E);
+  if (static_cast<long long>(R) * slices_1024 >= 4 * 256) {
+    *nt = 512;
+    *nl = 8;
+  } else {
+    *nt = 1024;
+    *nl = 4;
+  }
+}
 
 bool make_topk_plan(int R, int V, int k, int elem_bytes, bool vec, TopkPlan* p) {
   if (R < 1 || V < 1 || k < 1 || k > PTD_MAX_K || k > V) return false;
   p->kmax = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : k <= 8 ? 8 : 16;
   p->vec = vec;
   const int E = 16 / elem_bytes;
-  // A slice is at most kSliceChunks whole chunks (plus, for the last, a
-  // partial chunk): rows longer than that are split and merged afterwards.
-  const long long max_len = static_cast<long long>(kSliceChunks) * E;
+  topk_shape(R, V, E, &p->nt, &p->nl);
+  // A slice is at most nt * nl whole chunks (plus, for the last, a partial
+  // chunk): rows longer than that are split and merged afterwards.
+  const long long max_len = static_cast<long long>(p->nt) * p->nl * E;
   int s = static_cast<int>((V + max_len - 1) / max_len);
   int len = (V + s - 1) / s;
   len = (len + 7) & ~7;  // keep slice starts 16-byte aligned
@@ -534,10 +553,14 @@ template <int KMAX, bool BF16>
 void launch(const TopkPlan& pl, const void* logits, int R, int V, long long ld, int k,
             int32_t* am, int32_t* ti, float* tv, uint64_t* part, hipStream_t st) {
   constexpr int WPB = kThreads / PTD_WAVE;
-  if (pl.vec)
-    hipLaunchKernelGGL((k_topk_row<KMAX, BF16>), dim3(R * pl.slices), dim3(kRowThreads), 0, st,
+  if (pl.vec) {
+#define PTD_TOPK_ROW(nt_, nl_)                                                                   \
+  if (pl.nt == nt_ && pl.nl == nl_)                                                              \
+    hipLaunchKernelGGL((k_topk_row<KMAX, BF16, nt_, nl_>), dim3(R * pl.slices), dim3(nt_), 0, st, \
                        logits, V, ld, pl.slices, pl.slice_len, k, am, ti, tv, part);
-  else
+    PTD_TOPK_ROW(1024, 4) PTD_TOPK_ROW(512, 8)
+#undef PTD_TOPK_ROW
+  } else
     hipLaunchKernelGGL((k_topk_scalar<KMAX, BF16>), dim3((R * pl.slices + WPB - 1) / WPB),
                        dim3(kThreads), 0, st, logits, R, V, ld, pl.slices, pl.slice_len, k, am,
                        ti, tv, part);

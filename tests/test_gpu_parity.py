@@ -83,7 +83,7 @@ def _topk_case(P, arr, k, ld=None):
 @pytest.mark.parametrize("R,V,k", [(1, 1, 1), (3, 7, 5), (17, 1000, 4), (65, 32000, 4),
                                    (97, 32000, 5), (8, 32003, 16), (5, 128256, 8),
                                    (1100, 4099, 2), (3, 70001, 8), (2, 200003, 16),
-                                   (2, 300007, 4), (1, 600001, 16)])
+                                   (2, 300007, 4), (1, 600001, 16), (300, 128256, 8)])
 def test_topk_random(P, dtype, R, V, k):
     rng = np.random.default_rng(R * 7 + V + k)
     x = rng.standard_normal((R, V), dtype=np.float32) * np.float32(1.41)
@@ -125,6 +125,19 @@ def test_topk_many_ties_at_the_top(P, k):
         x[r, rng.choice(40000, n, replace=False)] = np.float32(9.0)
     _topk_case(P, x, k)
     _topk_case(P, W.f32_to_bf16_bits(x), k)
+
+
+def test_topk_many_slices_with_ties(P):
+    # enough slices for the 512-thread workgroups (four or more per CU), some
+    # rows with more ties at the top than the candidate lists hold
+    rng = np.random.default_rng(77)
+    R, V = 1100, 5000
+    x = rng.standard_normal((R, V), dtype=np.float32)
+    for r in range(0, R, 7):
+        x[r, rng.choice(V, 300 + r % 900, replace=False)] = np.float32(6.0)
+    for k in (1, 8, 16):
+        _topk_case(P, x, k)
+        _topk_case(P, W.f32_to_bf16_bits(x), k)
 
 
 @pytest.mark.parametrize("V", [32000, 3001])
