@@ -106,7 +106,9 @@ __device__ __forceinline__ float exp_term(float l, float m, float c_hi, float c_
   const float d_lo = (l - (d - bb)) + (-m - bb);
   const float x = d * c_hi;
   const float err = fmaf(d, c_hi, -x) + fmaf(d, c_lo, d_lo * c_hi);
-  return exp2f(x) * fmaf(err, 0.69314718f, 1.0f);
+  // (x <= 0 here; v_exp_f32 differs from exp2f only where 2^x is subnormal,
+  // terms negligible against a sum of at least 1)
+  return __builtin_amdgcn_exp2f(x) * fmaf(err, 0.69314718f, 1.0f);
 }
 
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
@@ -169,7 +171,8 @@ k_block_stats(const void* __restrict__ logits, int V, long long ld, int nblk, fl
   for (int j = 0; j < CPT; ++j)
     if (have[j])
 #pragma unroll
-      for (int e = 0; e < E; ++e) z += static_cast<double>(exp_term(x[j][e], m, c_hi, c_lo));
+      for (int e = 0; e < E; e += 2)  // pairs added in fp32 (one rounding, 2^-24), then fp64
+        z += static_cast<double>(exp_term(x[j][e], m, c_hi, c_lo) + exp_term(x[j][e + 1], m, c_hi, c_lo));
   for (int y = y0 + nch * E + tid; y < y1; y += kStatThreads)
     z += static_cast<double>(exp_term(logit<BF16>(row, y), m, c_hi, c_lo));
 #pragma unroll
