@@ -865,20 +865,22 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 // ===========================================================================
 // split-KV combine: out = sum_s w_s O_s / sum_s w_s l_s, w_s = 2^(mc_s - max mc),
 // one thread per (b, g, row, 4 columns), online in the split index (fixed
-// order, so the result is deterministic)
+// order, so the result is deterministic).  A workgroup covers 256 / (D/4)
+// consecutive rows of one (b, g): everything per (b, g) is uniform (scalar
+// loads and arithmetic) and a thread's row and columns are shifts of its id.
 // ===========================================================================
 template <int D, int U>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnParams p) {
-  const size_t idx = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   constexpr int D4 = D / 4;
-  const size_t total = static_cast<size_t>(p.B) * p.Hkv * p.M * D4;
-  if (idx >= total) return;
-  const int d4 = static_cast<int>(idx % D4);
-  size_t rest = idx / D4;
-  const int r = static_cast<int>(rest % p.M);
-  rest /= p.M;
-  const int g = static_cast<int>(rest % p.Hkv);
-  const int b = static_cast<int>(rest / p.Hkv);
+  constexpr int RPB = 256 / D4;  // rows per workgroup
+  const int nrb = (p.M + RPB - 1) / RPB;
+  const int bg = static_cast<int>(blockIdx.x) / nrb;  // uniform
+  const int rb = static_cast<int>(blockIdx.x) - bg * nrb;
+  const int b = bg / p.Hkv;
+  const int g = bg - b * p.Hkv;
+  const int d4 = threadIdx.x % D4;
+  const int r = rb * RPB + static_cast<int>(threadIdx.x) / D4;
+  if (r >= p.M) return;
   // The partials are loaded, U splits at a time, without waiting for kv_len
   // (the workspace holds all p.splits of them); the updates by empty splits,
   // whose partials were never written, are discarded with selects.
@@ -1108,6 +1110,8 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
     pl->splits = 1;
   }
   if (static_cast<long long>(s->B) * s->Hkv * pl->passes * pl->splits > 0x7FFFFFFFLL) return false;
+  // the combine's grid: one workgroup per 8 (D = 128) or 16 (D = 64) rows of a (b, g)
+  if (pl->splits > 1 && static_cast<long long>(s->B) * s->Hkv * ((M + 7) / 8) > 0x7FFFFFFFLL) return false;
   pl->needs_mask = !pl->mfma || T > 128;
   pl->partial_bytes = pl->splits > 1
       ? align256(static_cast<size_t>(pl->splits) * s->B * s->Hkv * M * (s->D + 2) * sizeof(float))
@@ -1251,8 +1255,9 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
     else if (shape->D == 128) launch_mfma<128, false>(pl, prm, st);
     else launch_mfma<64, false>(pl, prm, st);
     if (pl.splits > 1) {
-      const size_t total = static_cast<size_t>(prm.B) * prm.Hkv * prm.M * (shape->D / 4);
-      const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+      const int rpb = 256 / (shape->D / 4);  // rows per combine workgroup
+      const dim3 grid(static_cast<unsigned>(static_cast<long long>(prm.B) * prm.Hkv *
+                                            ((prm.M + rpb - 1) / rpb)));
       // U = splits loaded at once: the fewest of 2, 4, 8 covering them
       const int u = pl.splits <= 2 ? 2 : pl.splits <= 4 ? 4 : 8;
 #define PTD_COMBINE(d_, u_) \
