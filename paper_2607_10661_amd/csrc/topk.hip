@@ -247,13 +247,17 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   constexpr int ES = BF16 ? 2 : 4;
   constexpr int NW = NT / PTD_WAVE;
   static_assert(NT >= kCandCap && NW % 4 == 0 && NT * NL <= 65536, "workgroup shape");
-  constexpr int GL = PTD_WAVE / KMAX;  // lanes per group
+  constexpr int GL = PTD_WAVE / KMAX;  // lanes per group inside a wave
+  constexpr int GW = NT / KMAX;        // lanes per group across the workgroup
+  constexpr int GWL = GW < PTD_WAVE ? GW : PTD_WAVE;  // ... of them inside one wave
+  constexpr int WPG = GW / GWL;        // waves per workgroup-wide group
   __shared__ __attribute__((aligned(16))) uint4 s_ldata[kListCap];
   __shared__ uint64_t s_cand[kCandCap];
   __shared__ uint32_t s_bits[kCandCap];
   __shared__ uint32_t s_rank[kCandCap];
   __shared__ uint16_t s_list[kListCap];
   __shared__ __attribute__((aligned(16))) uint32_t s_tau[NW];
+  __shared__ __attribute__((aligned(16))) uint32_t s_tau2[NW];
   __shared__ int s_nlist, s_cnt;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -292,9 +296,18 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
     cm[u] = u * NT + tid < nfull ? chunk_img<BF16>(cw[u]) : 0u;
     lm = max(lm, cm[u]);
   }
-  // 2. the bound: max over the lane groups, then min over the groups
+  // 2. the bound, the larger of two: per wave, max over groups of GL lanes
+  //    then min over the wave's KMAX groups, and the largest of these over
+  //    the waves; and min over KMAX groups of NT / KMAX lanes spanning the
+  //    workgroup of the group maxima (much closer to the KMAX-th best value
+  //    of the slice, hence few candidates; the first stays positive where a
+  //    short slice leaves whole workgroup-wide groups empty)
   const uint32_t g = group_max_min<GL>(lm);
-  if (lane == 0) s_tau[wave] = g;
+  const uint32_t g2 = group_max_min<GWL>(lm);  // GWL = 64: the wave's maximum
+  if (lane == 0) {
+    s_tau[wave] = g;
+    s_tau2[wave] = g2;
+  }
   ptd::lds_barrier();
   uint32_t tau = 0;
 #pragma unroll
@@ -302,6 +315,15 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
     const uint4 t4 = *reinterpret_cast<const uint4*>(s_tau + i);
     tau = max(max(tau, max(t4.x, t4.y)), max(t4.z, t4.w));
   }
+  uint32_t tau2 = ~0u;
+#pragma unroll
+  for (int j = 0; j < NW / WPG; ++j) {
+    uint32_t gm = 0;
+#pragma unroll
+    for (int w = 0; w < WPG; ++w) gm = max(gm, s_tau2[j * WPG + w]);
+    tau2 = min(tau2, gm);
+  }
+  tau = max(tau, tau2);
   const uint32_t tc = cmp_bound<BF16>(tau);
 
   // 3. list the chunks that reach the bound, then examine them
