@@ -153,13 +153,15 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(u32x2 w) {
 
 // LDS layout of one 32-key sub-tile: K rows then V rows, each [32][D] of
 // ES-byte elements (bf16, or E4M3 for 8-bit caches), row-major with the
-// 16-byte chunks of row r stored XOR-permuted by f(r) (CH = D*ES/16 chunks
-// per row).  bf16, D = 128: f(r) = ((r mod 8) << 1) | bit 3 of r, a bijection
-// on 16 rows, so the K-operand reads (16 rows x one chunk per 16 lanes) hit
-// distinct banks, and f >> 1 is distinct over rows 0..7 and over rows 8..15,
-// so each half-wave of a V transpose read (8 rows x 2 adjacent chunks) covers
-// all 16 chunk positions once.  Otherwise (bf16 D = 64, E4M3 D = 128: 8
-// chunks) f(r) = r mod 8.
+// 16-byte chunks of row r stored XOR-permuted (CH = D*ES/16 chunks per row).
+// bf16, D = 128 (16 chunks): K rows by r mod 16, V rows by f(r) = ((r mod 8)
+// << 1) | bit 3 of r.  The K-operand reads (ds_read_b128: 16 rows x one
+// chunk per 16 lanes) are then conflict-free -- measured 205 B/clk per CU
+// against 113 with f, which leaves them 2-way bank-conflicted -- and f >> 1
+// is distinct over rows 0..7 and over rows 8..15, so each half-wave of a V
+// transpose read (8 rows x 2 adjacent chunks) covers all 16 chunk positions
+// once (177 B/clk).  Otherwise (bf16 D = 64, E4M3 D = 128: 8 chunks) both
+// use r mod 8.
 template <int D, int ES>
 struct Ring {
   static constexpr int RB = D * ES;                  // bytes per row
@@ -174,7 +176,8 @@ struct Ring {
   static constexpr int DPS = 2 * SUB * CH / kThreads;  // copies per thread per sub-tile
   static constexpr int BYTES = NS * SLOT;
   static_assert((DPS == 1 || DPS % 2 == 0) && (2 * SUB * CH) % kThreads == 0, "sub-tile split");
-  __device__ static int swz(int row, int chunk) {
+  __device__ static int swz_k(int row, int chunk) { return chunk ^ (row & (CH - 1)); }
+  __device__ static int swz_v(int row, int chunk) {
     if constexpr (CH == 16) return chunk ^ (((row & 7) << 1) | ((row >> 3) & 1));
     else return chunk ^ (row & (CH - 1));
   }
@@ -308,7 +311,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     cp_v[u] = (u * kThreads + wave * PTD_WAVE) / (R::SUB * R::CH) != 0;
     const int local = c % (R::SUB * R::CH);
     cp_row[u] = local / R::CH;
-    cp_off[u] = R::swz(cp_row[u], local % R::CH) * (16 / ES);  // elements
+    cp_off[u] = (cp_v[u] ? R::swz_v(cp_row[u], local % R::CH)
+                         : R::swz_k(cp_row[u], local % R::CH)) * (16 / ES);  // elements
     cp_voff[u] = static_cast<uint32_t>((cp_row[u] * D + cp_off[u]) * ES);
     cp_lds[u] = static_cast<uint32_t>((u * kThreads + wave * PTD_WAVE) * 16);
   }
@@ -390,20 +394,20 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     // the transpose read gives lane l16 the 8 keys' values at d = 16*dt + l16.
 #pragma unroll
     for (int db = 0; db < DB; ++db)
-      koff[db] = l16 * R::RB + R::swz(l16, 2 * db + (l4 >> 1)) * 16 + (l4 & 1) * 8;
+      koff[db] = l16 * R::RB + R::swz_k(l16, 2 * db + (l4 >> 1)) * 16 + (l4 & 1) * 8;
     const int j = l16 >> 1, h = l16 & 1;
     const int key0 = j < 4 ? 4 * l4 + j : 16 + 4 * l4 + (j - 4);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) voff[dt] = key0 * R::RB + R::swz(key0, dt) * 16 + h * 8;
+    for (int dt = 0; dt < DT; ++dt) voff[dt] = key0 * R::RB + R::swz_v(key0, dt) * 16 + h * 8;
   } else {
 #pragma unroll
     for (int db = 0; db < DB; ++db)
-      koff[db] = l16 * R::RB + R::swz(l16, db * 4 + l4) * 16;
+      koff[db] = l16 * R::RB + R::swz_k(l16, db * 4 + l4) * 16;
     const int tj = l16 >> 2, tq = l16 & 3;
     const int key0 = 4 * l4 + tj;  // this lane's source key for the transpose reads
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
-      voff[dt] = key0 * R::RB + R::swz(key0, 2 * dt + (tq >> 1)) * 16 + (tq & 1) * 8;
+      voff[dt] = key0 * R::RB + R::swz_v(key0, 2 * dt + (tq >> 1)) * 16 + (tq & 1) * 8;
   }
 
   struct Tile {
