@@ -414,29 +414,47 @@ k_verify_expand(const int32_t* __restrict__ argmax, const int32_t* __restrict__ 
 }
 
 // ===========================================================================
-// Trees of up to 64 nodes: one wave per sequence, node i on lane i, no
-// workgroup barriers.  Same results as the workgroup kernels above.
-//   - ancestor sets as 64-bit masks by pointer doubling over wave shuffles
-//     (anc = {i}, jump = parent; anc |= anc[jump], jump = jump[jump] until
-//     every jump is -1); depth = |anc|
+// Trees of up to 64 * NPL nodes (NPL = 1, 2): one wave per sequence, node
+// 64 x + lane in slot x of its lane, no workgroup barriers.  Same results as
+// the workgroup kernels above.
+//   - ancestor sets as NPL-word bit masks (word w: nodes 64 w .. 64 w + 63)
+//     by pointer doubling over wave shuffles (anc = {i}, jump = parent;
+//     anc |= anc[jump], jump = jump[jump] until every jump is -1);
+//     depth = |anc|
 //   - verification: a node is accepted iff anc contains no node whose edge is
-//     ineligible (one ballot), the terminal is the wave maximum of
+//     ineligible (one ballot per word), the terminal is the wave maximum of
 //     (depth, -index), and the path is the terminal's ancestor mask
 //   - expansion: children masks by LDS atomic OR; a node's added candidates
 //     as a bit set over its top-k row; breadth-first positions level by
 //     level: the nodes of a level write their child counts at their
-//     positions, a scan over the wave (DPP row shifts and broadcasts)
-//     gives every node its first child's position, and old children add
-//     their rank among their siblings to their parent's
+//     positions, a scan over the wave (DPP row shifts and broadcasts, one
+//     per 64 positions) gives every node its first child's position, and
+//     old children add their rank among their siblings to their parent's
 // Wave reductions use DPP and the gfx950 lane swaps (VALU only); gathers
 // from other lanes are the remaining LDS-latency steps.
 // ===========================================================================
 constexpr int kWaveNodes = 64;
+constexpr int kWaveTree = 2 * kWaveNodes;  // trees (and cuts) the one-wave kernel takes
 
 __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
   const uint32_t lo = __shfl(static_cast<uint32_t>(v), src, PTD_WAVE);
   const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src, PTD_WAVE);
   return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Value of node j (0 <= j < 64 * NPL) from per-slot lane values v[x] (node
+// 64 x + lane): lane j mod 64, slot j / 64.
+template <int NPL, typename T>
+__device__ __forceinline__ T gather_node(const T (&v)[NPL], int j) {
+  T r = T{};
+#pragma unroll
+  for (int x = 0; x < NPL; ++x) {
+    T t;
+    if constexpr (sizeof(T) == 8) t = shfl64(v[x], j & 63);
+    else t = __shfl(v[x], j & 63, PTD_WAVE);
+    if ((j >> 6) == x) r = t;
+  }
+  return r;
 }
 
 // Maximum over the wave: within quads (quad permutes), half-rows and rows
@@ -471,7 +489,16 @@ __device__ __forceinline__ int wave_excl_scan(int c, int* total) {
   return x - c;
 }
 
-template <bool VERIFY, bool EXPAND, int KM>
+// Members of the NPL-word set m with a lower index than node 64 x + lane.
+template <int NPL>
+__device__ __forceinline__ int rank_below(const uint64_t (&m)[NPL], int x, uint64_t below) {
+  int r = 0;
+#pragma unroll
+  for (int w = 0; w < NPL; ++w) r += w < x ? __popcll(m[w]) : w == x ? __popcll(m[w] & below) : 0;
+  return r;
+}
+
+template <bool VERIFY, bool EXPAND, int KM, int NPL>
 __global__ void __launch_bounds__(PTD_WAVE)
 k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ tokens,
             const int32_t* __restrict__ parent, const int32_t* __restrict__ tree_len, int T,
@@ -480,38 +507,61 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
             int32_t* __restrict__ out_tokens, int32_t* __restrict__ parent_next,
             int32_t* __restrict__ tokens_next, int32_t* __restrict__ tree_len_next,
             int32_t* dev_status) {
-  __shared__ int s_cnt[kWaveNodes];
-  __shared__ uint64_t s_cm[kWaveNodes];
-  __shared__ uint32_t s_dup[kWaveNodes];
+  constexpr int NN = NPL * kWaveNodes;  // nodes a wave holds
+  static_assert(PTD_MAX_DEPTH == kWaveNodes, "one width entry per lane");
+  __shared__ int s_cnt[NN];
+  __shared__ uint64_t s_cm[NN][NPL];
+  __shared__ uint32_t s_dup[NN];
   __shared__ int s_width[PTD_MAX_DEPTH];
   const int lane = threadIdx.x, b = blockIdx.x;
   const int n = live_nodes(tree_len, b, T);
-  const bool live = lane < n;
   const uint64_t below = (1ull << lane) - 1ull;
+  int node[NPL];
+  bool live[NPL];
+#pragma unroll
+  for (int x = 0; x < NPL; ++x) {
+    node[x] = x * kWaveNodes + lane;
+    live[x] = node[x] < n;
+  }
 
   // every global load first, none waiting for tree_len
-  const int par_in = lane < T ? parent[static_cast<size_t>(b) * T + lane] : -1;
-  const int tok_in = lane < T ? tokens[static_cast<size_t>(b) * T + lane] : 0;
-  int am_lo = 0, am_hi = 0;  // argmax rows lane and 64
-  if (VERIFY) {
-    const int32_t* am = argmax + static_cast<size_t>(b) * (T + 1);
-    am_lo = lane <= T ? am[lane] : 0;
-    am_hi = T >= kWaveNodes ? am[kWaveNodes] : 0;
-  }
-  int cand[KM];
-  if (EXPAND) {
-    const int32_t* row = topk_idx + (static_cast<size_t>(b) * (T + 1) + lane + 1) * k;
+  int par_in[NPL], tok_in[NPL];
 #pragma unroll
-    for (int r = 0; r < KM; ++r) cand[r] = (lane < T && r < k) ? row[r] : 0;
+  for (int x = 0; x < NPL; ++x) {
+    par_in[x] = node[x] < T ? parent[static_cast<size_t>(b) * T + node[x]] : -1;
+    tok_in[x] = node[x] < T ? tokens[static_cast<size_t>(b) * T + node[x]] : 0;
+  }
+  int am[NPL], am_last = 0;  // argmax rows 64 x + lane, and row NN
+  if (VERIFY) {
+    const int32_t* amb = argmax + static_cast<size_t>(b) * (T + 1);
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) am[x] = node[x] <= T ? amb[node[x]] : 0;
+    am_last = T >= NN ? amb[NN] : 0;
+  }
+  int cand[NPL][KM];
+  if (EXPAND) {
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      const int32_t* row = topk_idx + (static_cast<size_t>(b) * (T + 1) + node[x] + 1) * k;
+#pragma unroll
+      for (int r = 0; r < KM; ++r) cand[x][r] = (node[x] < T && r < k) ? row[r] : 0;
+    }
     s_width[lane] = ws.w[lane];
   }
-  const int par = live ? par_in : -1;
-  const int tok = live ? tok_in : 0;
-  s_cm[lane] = 0ull;
-  s_cnt[lane] = 0;
-  s_dup[lane] = 0u;
+  int par[NPL], tok[NPL];
+  bool bad = false;
+#pragma unroll
+  for (int x = 0; x < NPL; ++x) {
+    par[x] = live[x] ? par_in[x] : -1;
+    tok[x] = live[x] ? tok_in[x] : 0;
+    bad |= live[x] && (par[x] < -1 || par[x] >= node[x]);
+#pragma unroll
+    for (int w = 0; w < NPL; ++w) s_cm[node[x]][w] = 0ull;
+    s_cnt[node[x]] = 0;
+    s_dup[node[x]] = 0u;
+  }
 
-  if (__any(live && (par < -1 || par >= lane))) {  // not topological
+  if (__any(bad)) {  // not topological
     if (lane == 0) ptd::report(dev_status, PTD_ERR_BAD_TREE);
     if (VERIFY) verify_reject(b, T, accept_len, accept_nodes, out_tokens);
     if (EXPAND) expand_reject(b, T_max, parent_next, tokens_next, tree_len_next);
@@ -519,44 +569,102 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
   }
 
   // ancestor masks and depths
-  uint64_t anc = live ? (1ull << lane) : 0ull;
-  int jump = par;
-  while (__any(jump >= 0)) {
-    const int src = jump >= 0 ? jump : lane;
-    const uint64_t a2 = shfl64(anc, src);
-    const int j2 = __shfl(jump, src, PTD_WAVE);
-    if (jump >= 0) {
-      anc |= a2;
-      jump = j2;
-    }
+  uint64_t anc[NPL][NPL];
+  int jump[NPL], dep[NPL];
+#pragma unroll
+  for (int x = 0; x < NPL; ++x) {
+#pragma unroll
+    for (int w = 0; w < NPL; ++w) anc[x][w] = (live[x] && w == x) ? (1ull << lane) : 0ull;
+    jump[x] = par[x];
   }
-  const int dep = __popcll(anc);
+  for (;;) {
+    bool any_jump = false;
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) any_jump |= jump[x] >= 0;
+    if (!__any(any_jump)) break;
+    // gathers read the values before this round's updates
+    uint64_t a2[NPL][NPL];
+    int j2[NPL];
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      const int src = jump[x] >= 0 ? jump[x] : node[x];
+#pragma unroll
+      for (int w = 0; w < NPL; ++w) {
+        uint64_t col[NPL];
+#pragma unroll
+        for (int y = 0; y < NPL; ++y) col[y] = anc[y][w];
+        a2[x][w] = gather_node<NPL>(col, src);
+      }
+      j2[x] = gather_node<NPL>(jump, src);
+    }
+#pragma unroll
+    for (int x = 0; x < NPL; ++x)
+      if (jump[x] >= 0) {
+#pragma unroll
+        for (int w = 0; w < NPL; ++w) anc[x][w] |= a2[x][w];
+        jump[x] = j2[x];
+      }
+  }
+#pragma unroll
+  for (int x = 0; x < NPL; ++x) {
+    dep[x] = 0;
+#pragma unroll
+    for (int w = 0; w < NPL; ++w) dep[x] += __popcll(anc[x][w]);
+  }
 
   if (VERIFY) {
-    const int pa = par + 1;  // the parent's argmax row (0 for a root)
-    const int am_par_lo = __shfl(am_lo, pa & 63, PTD_WAVE);
-    const int am_par = pa < kWaveNodes ? am_par_lo : am_hi;
-    const uint64_t elig = __ballot(live && tok == am_par);
-    const bool accepted = live && (anc & ~elig) == 0ull;
-    const int key = wave_max_i32(accepted ? dep * 128 + (127 - lane) : -1);
-    const int klen = key < 0 ? 0 : key / 128;
-    const int best = key < 0 ? -1 : 127 - key % 128;
+    uint64_t elig[NPL];
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      const int pa = par[x] + 1;  // the parent's argmax row (0 for a root)
+      const int am_par = pa < NN ? gather_node<NPL>(am, pa) : am_last;
+      elig[x] = __ballot(live[x] && tok[x] == am_par);
+    }
+    int key = -1;
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      bool accepted = live[x];
+#pragma unroll
+      for (int w = 0; w < NPL; ++w) accepted &= (anc[x][w] & ~elig[w]) == 0ull;
+      key = max(key, accepted ? dep[x] * 256 + (255 - node[x]) : -1);
+    }
+    key = wave_max_i32(key);
+    const int klen = key < 0 ? 0 : key / 256;
+    const int best = key < 0 ? -1 : 255 - key % 256;
     // best is uniform over the wave (a wave maximum): read its lane directly
-    const int bsrc = __builtin_amdgcn_readfirstlane(best < 0 ? 0 : best);
-    const uint64_t path =
-        (static_cast<uint64_t>(__builtin_amdgcn_readlane(static_cast<uint32_t>(anc >> 32), bsrc)) << 32) |
-        __builtin_amdgcn_readlane(static_cast<uint32_t>(anc), bsrc);
+    const int bl = __builtin_amdgcn_readfirstlane(best < 0 ? 0 : best & 63);
+    const int bs = best < 0 ? 0 : best >> 6;
+    uint64_t path[NPL];
+#pragma unroll
+    for (int w = 0; w < NPL; ++w) {
+      path[w] = 0ull;
+#pragma unroll
+      for (int x = 0; x < NPL; ++x) {
+        // (readlane returns int: widen through uint32_t, never sign-extend)
+        const uint32_t phi = __builtin_amdgcn_readlane(static_cast<uint32_t>(anc[x][w] >> 32), bl);
+        const uint32_t plo = __builtin_amdgcn_readlane(static_cast<uint32_t>(anc[x][w]), bl);
+        const uint64_t pw = (static_cast<uint64_t>(phi) << 32) | plo;
+        if (bs == x) path[w] = pw;
+      }
+    }
     const int bt = best + 1;  // the terminal's argmax row: the bonus token
-    const int bonus_lo = __builtin_amdgcn_readlane(am_lo, __builtin_amdgcn_readfirstlane(bt & 63));
-    const int bonus = bt < kWaveNodes ? bonus_lo : am_hi;
+    int bonus = am_last;
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      const int v = __builtin_amdgcn_readlane(am[x], __builtin_amdgcn_readfirstlane(bt & 63));
+      if ((bt >> 6) == x) bonus = v;
+    }
     int32_t* an = accept_nodes + static_cast<size_t>(b) * T;
     int32_t* ot = out_tokens + static_cast<size_t>(b) * (T + 1);
-    const bool on_path = best >= 0 && live && ((path >> lane) & 1ull);
-    if (on_path) {
-      an[dep - 1] = lane;
-      ot[dep - 1] = tok;
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      const bool on_path = best >= 0 && live[x] && ((path[x] >> lane) & 1ull);
+      if (on_path) {
+        an[dep[x] - 1] = node[x];
+        ot[dep[x] - 1] = tok[x];
+      }
+      if (node[x] < T && node[x] >= klen) an[node[x]] = -1;
     }
-    if (lane < T && lane >= klen) an[lane] = -1;
     for (int t = lane; t <= T; t += PTD_WAVE) {
       if (t == klen) ot[t] = bonus;
       else if (t > klen) ot[t] = -1;
@@ -567,88 +675,131 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
   if (EXPAND) {
     // children masks, and each child marks the entries of its parent's top-k
     // row that repeat its own token (the parent's row gathered by shuffles)
-    uint32_t mydup = 0;
 #pragma unroll
-    for (int r = 0; r < KM; ++r) {
-      const int pc = __shfl(cand[r], par >= 0 ? par : lane, PTD_WAVE);
-      mydup |= (pc == tok) ? (1u << r) : 0u;
-    }
-    if (live && par >= 0) {
-      atomicOr(reinterpret_cast<unsigned long long*>(&s_cm[par]), 1ull << lane);
-      atomicOr(&s_dup[par], mydup);
-    }
-    ptd::lds_barrier();  // LDS only: the global stores need no wait
-    const uint64_t cm = s_cm[lane];
-    const int ncld = __popcll(cm);
-    // candidates added under this node (bit r: topk row entry r)
-    uint32_t sel = 0;
-    if (live && dep + 1 <= d_max) {
-      const int cap = s_width[dep];
-      const uint32_t dup = s_dup[lane];  // entries equal to an existing child's token
-      int have = ncld;
+    for (int x = 0; x < NPL; ++x) {
+      uint32_t mydup = 0;
+      const int psrc = par[x] >= 0 ? par[x] : node[x];
 #pragma unroll
       for (int r = 0; r < KM; ++r) {
-        bool d = (dup >> r) & 1u;
+        int col[NPL];
 #pragma unroll
-        for (int r2 = 0; r2 < r; ++r2) d |= cand[r2] == cand[r];
-        if (r < k && have < cap && !d) {
-          sel |= 1u << r;
-          ++have;
-        }
-        if (have >= cap) break;
+        for (int y = 0; y < NPL; ++y) col[y] = cand[y][r];
+        const int pc = gather_node<NPL>(col, psrc);
+        mydup |= (pc == tok[x]) ? (1u << r) : 0u;
+      }
+      if (live[x] && par[x] >= 0) {
+        atomicOr(reinterpret_cast<unsigned long long*>(&s_cm[par[x]][x]), 1ull << lane);
+        atomicOr(&s_dup[par[x]], mydup);
       }
     }
-    const int nnew = __popc(sel);
+    ptd::lds_barrier();  // LDS only: the global stores need no wait
+    int ncld[NPL], nnew[NPL], srank[NPL];
+    uint32_t sel[NPL];
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      ncld[x] = 0;
+#pragma unroll
+      for (int w = 0; w < NPL; ++w) ncld[x] += __popcll(s_cm[node[x]][w]);
+      // candidates added under this node (bit r: topk row entry r)
+      sel[x] = 0;
+      if (live[x] && dep[x] + 1 <= d_max) {
+        const int cap = s_width[dep[x]];
+        const uint32_t dup = s_dup[node[x]];  // entries equal to an existing child's token
+        int have = ncld[x];
+#pragma unroll
+        for (int r = 0; r < KM; ++r) {
+          bool d = (dup >> r) & 1u;
+#pragma unroll
+          for (int r2 = 0; r2 < r; ++r2) d |= cand[x][r2] == cand[x][r];
+          if (r < k && have < cap && !d) {
+            sel[x] |= 1u << r;
+            ++have;
+          }
+          if (have >= cap) break;
+        }
+      }
+      nnew[x] = __popc(sel[x]);
+      // an old child's rank among its siblings (children masks are complete)
+      uint64_t sib[NPL];
+#pragma unroll
+      for (int w = 0; w < NPL; ++w) sib[w] = live[x] && par[x] >= 0 ? s_cm[par[x]][w] : 0ull;
+      srank[x] = rank_below<NPL>(sib, x, below);
+    }
 
     int32_t* pn = parent_next + static_cast<size_t>(b) * T_max;
     int32_t* tn = tokens_next + static_cast<size_t>(b) * T_max;
-    const uint64_t roots = __ballot(live && par < 0);
-    int pos = -1;  // breadth-first position (-1: not placed, or cut at T_max)
-    if (live && par < 0) {
-      const int q = __popcll(roots & below);
-      if (q < T_max) {
-        pos = q;
-        pn[q] = -1;
-        tn[q] = tok;
-      }
-    }
-    // an old child's rank among its siblings (children masks are complete)
-    const int srank = live && par >= 0 ? __popcll(s_cm[par] & below) : 0;
-    int lo = 0, hi = min(__popcll(roots), T_max);
-    for (int level = 1; lo < hi; ++level) {
-      // positions [lo, hi) hold this level; lane p of the scan is position lo + p
-      const bool here = pos >= 0 && dep == level;
-      if (here) s_cnt[pos] = ncld + nnew;
-      ptd::lds_barrier();  // LDS only: the global stores need no wait
-      const int p = lo + lane;
-      int total;
-      const int first = hi + wave_excl_scan(p < hi ? s_cnt[p] : 0, &total);
-      const int start = __shfl(first, here ? pos - lo : 0, PTD_WAVE);  // valid where here
-      if (here) {  // added children: after the old ones, in candidate order
-        int q = start + ncld;
+    uint64_t roots[NPL];
+    int nroots = 0;
 #pragma unroll
-        for (int r = 0; r < KM; ++r) {
-          if ((sel >> r) & 1u) {
-            if (q < T_max) {
-              pn[q] = pos;
-              tn[q] = cand[r];
-            }
-            ++q;
-          }
+    for (int x = 0; x < NPL; ++x) {
+      roots[x] = __ballot(live[x] && par[x] < 0);
+      nroots += __popcll(roots[x]);
+    }
+    int pos[NPL];  // breadth-first position (-1: not placed, or cut at T_max)
+#pragma unroll
+    for (int x = 0; x < NPL; ++x) {
+      pos[x] = -1;
+      if (live[x] && par[x] < 0) {
+        const int q = rank_below<NPL>(roots, x, below);
+        if (q < T_max) {
+          pos[x] = q;
+          pn[q] = -1;
+          tn[q] = tok[x];
         }
       }
-      // the parent's first-child position and its own position in one
-      // gather (start < 2^16 and -1 <= pos < 2^15)
-      const int src = par >= 0 ? par : lane;
-      const int pk = __shfl((start & 0xFFFF) | ((pos + 1) << 16), src, PTD_WAVE);
-      const int pstart = pk & 0xFFFF;
-      const int ppos = (pk >> 16) - 1;
-      if (live && par >= 0 && dep == level + 1 && ppos >= 0) {  // the parent is on this level
-        const int q = pstart + srank;
-        if (q < T_max) {
-          pos = q;
-          pn[q] = ppos;
-          tn[q] = tok;
+    }
+    int lo = 0, hi = min(nroots, T_max);
+    for (int level = 1; lo < hi; ++level) {
+      // positions [lo, hi) hold this level; slot x of lane p is position
+      // lo + 64 x + p
+      bool here[NPL];
+#pragma unroll
+      for (int x = 0; x < NPL; ++x) {
+        here[x] = pos[x] >= 0 && dep[x] == level;
+        if (here[x]) s_cnt[pos[x]] = ncld[x] + nnew[x];
+      }
+      ptd::lds_barrier();  // LDS only: the global stores need no wait
+      int first[NPL], total = 0;
+#pragma unroll
+      for (int x = 0; x < NPL; ++x) {
+        const int p = lo + x * kWaveNodes + lane;
+        int t;
+        first[x] = hi + total + wave_excl_scan(p < hi ? s_cnt[p] : 0, &t);
+        total += t;
+      }
+      int pk[NPL];
+#pragma unroll
+      for (int x = 0; x < NPL; ++x) {
+        const int start = gather_node<NPL>(first, here[x] ? pos[x] - lo : 0);  // valid where here
+        if (here[x]) {  // added children: after the old ones, in candidate order
+          int q = start + ncld[x];
+#pragma unroll
+          for (int r = 0; r < KM; ++r) {
+            if ((sel[x] >> r) & 1u) {
+              if (q < T_max) {
+                pn[q] = pos[x];
+                tn[q] = cand[x][r];
+              }
+              ++q;
+            }
+          }
+        }
+        // the node's first-child position and its own position packed for
+        // one gather by its children (start < 2^16 and -1 <= pos < 2^15)
+        pk[x] = (start & 0xFFFF) | ((pos[x] + 1) << 16);
+      }
+#pragma unroll
+      for (int x = 0; x < NPL; ++x) {
+        const int pkp = gather_node<NPL>(pk, par[x] >= 0 ? par[x] : node[x]);
+        const int pstart = pkp & 0xFFFF;
+        const int ppos = (pkp >> 16) - 1;
+        if (live[x] && par[x] >= 0 && dep[x] == level + 1 && ppos >= 0) {  // the parent is on this level
+          const int q = pstart + srank[x];
+          if (q < T_max) {
+            pos[x] = q;
+            pn[q] = ppos;
+            tn[q] = tok[x];
+          }
         }
       }
       lo = hi;
@@ -663,20 +814,24 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
 }
 
 template <bool VERIFY, bool EXPAND>
-void launch_wave(int B, int T, int k, const int32_t* argmax, const int32_t* tokens,
+void launch_wave(int B, int T, int T_max, int k, const int32_t* argmax, const int32_t* tokens,
                  const int32_t* parent, const int32_t* tree_len, const int32_t* topk_idx,
-                 const WidthArg& ws, int d_max, int T_max, int32_t* accept_len,
+                 const WidthArg& ws, int d_max, int32_t* accept_len,
                  int32_t* accept_nodes, int32_t* out_tokens, int32_t* parent_next,
                  int32_t* tokens_next, int32_t* tree_len_next, int32_t* dev_status,
                  hipStream_t st) {
-#define PTD_WAVE_CASE(km)                                                                      \
-  hipLaunchKernelGGL((k_tree_wave<VERIFY, EXPAND, km>), dim3(B), dim3(PTD_WAVE), 0, st, argmax, \
-                     tokens, parent, tree_len, T, topk_idx, k, ws, d_max, T_max, accept_len,    \
-                     accept_nodes, out_tokens, parent_next, tokens_next, tree_len_next,         \
-                     dev_status)
-  if (!EXPAND || k <= 4) PTD_WAVE_CASE(4);
-  else if (k <= 8) PTD_WAVE_CASE(8);
-  else PTD_WAVE_CASE(16);
+  const int npl = (T <= kWaveNodes && T_max <= kWaveNodes) ? 1 : 2;
+#define PTD_WAVE_CASE(km, npl_)                                                                \
+  hipLaunchKernelGGL((k_tree_wave<VERIFY, EXPAND, km, npl_>), dim3(B), dim3(PTD_WAVE), 0, st,  \
+                     argmax, tokens, parent, tree_len, T, topk_idx, k, ws, d_max, T_max,        \
+                     accept_len, accept_nodes, out_tokens, parent_next, tokens_next,            \
+                     tree_len_next, dev_status)
+#define PTD_WAVE_NPL(km) \
+  if (npl == 1) PTD_WAVE_CASE(km, 1); else PTD_WAVE_CASE(km, 2);
+  if (!EXPAND || k <= 4) { PTD_WAVE_NPL(4) }
+  else if (k <= 8) { PTD_WAVE_NPL(8) }
+  else { PTD_WAVE_NPL(16) }
+#undef PTD_WAVE_NPL
 #undef PTD_WAVE_CASE
 }
 
@@ -703,9 +858,9 @@ extern "C" int ptd_verify(const int32_t* argmax, const int32_t* draft_tokens,
   PTD_RETURN_IF(B < 1 || T < 1 || T > PTD_MAX_T, PTD_ERR_SHAPE);
   static_assert(PTD_MAX_T <= 2048, "index packing in the best-node key");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (T <= kWaveNodes) {
-    launch_wave<true, false>(B, T, 1, argmax, draft_tokens, parent, tree_len, nullptr,
-                             WidthArg{}, 1, 1, accept_len, accept_nodes, out_tokens, nullptr,
+  if (T <= kWaveTree) {
+    launch_wave<true, false>(B, T, 1, 1, argmax, draft_tokens, parent, tree_len, nullptr,
+                             WidthArg{}, 1, accept_len, accept_nodes, out_tokens, nullptr,
                              nullptr, nullptr, dev_status, st);
   } else {
     hipLaunchKernelGGL(k_verify, dim3(B), dim3(kThreads), 0, st, argmax, draft_tokens, parent,
@@ -725,9 +880,9 @@ extern "C" int ptd_expand(const int32_t* parent, const int32_t* tokens,
                 PTD_ERR_NULL);
   PTD_RETURN_IF(!expand_args_ok(B, T, k, d_max, T_max), PTD_ERR_SHAPE);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (T <= kWaveNodes && T_max <= kWaveNodes) {
-    launch_wave<false, true>(B, T, k, nullptr, tokens, parent, tree_len, topk_idx,
-                             width_arg(width_sched, d_max), d_max, T_max, nullptr, nullptr,
+  if (T <= kWaveTree && T_max <= kWaveTree) {
+    launch_wave<false, true>(B, T, T_max, k, nullptr, tokens, parent, tree_len, topk_idx,
+                             width_arg(width_sched, d_max), d_max, nullptr, nullptr,
                              nullptr, parent_next, tokens_next, tree_len_next, dev_status, st);
   } else {
     hipLaunchKernelGGL(k_expand, dim3(B), dim3(kThreads), 0, st, parent, tokens, tree_len, T,
@@ -751,9 +906,9 @@ extern "C" int ptd_verify_expand(const int32_t* argmax, const int32_t* draft_tok
                 PTD_ERR_NULL);
   PTD_RETURN_IF(!expand_args_ok(B, T, k, d_max, T_max), PTD_ERR_SHAPE);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (T <= kWaveNodes && T_max <= kWaveNodes) {
-    launch_wave<true, true>(B, T, k, argmax, draft_tokens, parent, tree_len, topk_idx,
-                            width_arg(width_sched, d_max), d_max, T_max, accept_len,
+  if (T <= kWaveTree && T_max <= kWaveTree) {
+    launch_wave<true, true>(B, T, T_max, k, argmax, draft_tokens, parent, tree_len, topk_idx,
+                            width_arg(width_sched, d_max), d_max, accept_len,
                             accept_nodes, out_tokens, parent_next, tokens_next, tree_len_next,
                             dev_status, st);
   } else {

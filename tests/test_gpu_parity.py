@@ -306,7 +306,78 @@ def test_verify_expand_small_trees(P, seed):
             assert np.array_equal(g.cpu().numpy(), r), (seed, trial, T, k, d_max, T_max)
 
 
-@pytest.mark.parametrize("T", [9, 64, 100])
+@pytest.mark.parametrize("seed", range(4))
+def test_verify_expand_mid_trees(P, seed):
+    # trees of 65-128 nodes and cuts up to 128 (one wave, two nodes per
+    # lane), and small trees cut above 64: chains, stars, level-built and
+    # uniform trees, k up to 16, deep depth caps
+    rng = np.random.default_rng(300 + seed)
+    for trial in range(25):
+        B = int(rng.integers(1, 5))
+        T = int(rng.choice([7, 64, 65, 96, 127, 128]))
+        k = int(rng.integers(1, 17))
+        d_max = int(rng.integers(1, 65))
+        width = rng.integers(1, 6, d_max).astype(np.int32)
+        T_max = int(rng.integers(65, 129)) if T <= 64 else int(rng.integers(1, 129))
+        par = np.stack([_small_tree(rng, T) for _ in range(B)])
+        V = int(rng.choice([3, 8, 1000]))
+        tok = rng.integers(0, V, (B, T)).astype(np.int32)
+        am = rng.integers(0, V, (B, T + 1)).astype(np.int32)
+        if trial % 3 == 0:  # plant accepted chains: every node's token is its parent's argmax
+            for b in range(B):
+                for i in range(T):
+                    tok[b, i] = am[b, par[b, i] + 1]
+        ti = rng.integers(0, V, (B, T + 1, k)).astype(np.int32)
+        tl = rng.integers(0, T + 1, B).astype(np.int32) if trial % 2 else None
+        ref_v = O.verify(am, tok, par, tl)
+        ref_e = O.expand(par, tok, ti, width, d_max, T_max, tl)
+        got = P.verify_expand(cu(am), cu(tok), cu(par), cu(ti), width.tolist(), d_max, T_max,
+                              None if tl is None else cu(tl))
+        for j, (g, r) in enumerate(zip(got, ref_v + ref_e)):
+            g = g.cpu().numpy()
+            assert np.array_equal(g, r), f"{(seed, trial, T, k, d_max, T_max)} output {j}: {_diff(g, r)}"
+        got_v = P.verify(cu(am), cu(tok), cu(par), None if tl is None else cu(tl))
+        got_e = P.expand(cu(par), cu(tok), cu(ti), width.tolist(), d_max, T_max,
+                         None if tl is None else cu(tl))
+        for j, (g, r) in enumerate(zip(tuple(got_v) + tuple(got_e), ref_v + ref_e)):
+            g = g.cpu().numpy()
+            assert np.array_equal(g, r), f"{(seed, trial, T, k, d_max, T_max)} output {j}: {_diff(g, r)}"
+
+
+@pytest.mark.parametrize("T,top", [(40, 31), (64, 31), (110, 95), (128, 95)])
+def test_verify_path_through_bit_31(P, T, top):
+    # accepted chain 0..top (top = 31 or 95: bit 31 of a path-mask word) and
+    # live roots above it that are not accepted: the path mask of the
+    # terminal must not leak into the nodes above top
+    par = np.full((1, T), -1, np.int32)
+    par[0, 1:top + 1] = np.arange(top)
+    am = np.arange(1, T + 2, dtype=np.int32)[None, :] % 7
+    tok = np.empty((1, T), np.int32)
+    for i in range(T):
+        tok[0, i] = am[0, par[0, i] + 1] if i <= top else (am[0, 0] + 1) % 7
+    ref = O.verify(am, tok, par)
+    assert ref[0][0] == top + 1
+    got = P.verify(cu(am), cu(tok), cu(par))
+    for j, (g, r) in enumerate(zip(got, ref)):
+        g = g.cpu().numpy()
+        assert np.array_equal(g, r), f"output {j}: {_diff(g, r)}"
+    ti = np.zeros((1, T + 1, 2), np.int32)
+    ref_e = O.expand(par, tok, ti, np.array([2] * 8, np.int32), 8, T)
+    got = P.verify_expand(cu(am), cu(tok), cu(par), cu(ti), [2] * 8, 8, T)
+    for j, (g, r) in enumerate(zip(got, ref + ref_e)):
+        g = g.cpu().numpy()
+        assert np.array_equal(g, r), f"output {j}: {_diff(g, r)}"
+
+
+def _diff(got, ref):
+    """The first few differing positions as (index, got, expected)."""
+    if got.shape != ref.shape:
+        return ("shape", got.shape, ref.shape)
+    idx = np.argwhere(got != ref)[:6]
+    return [(tuple(int(v) for v in i), int(got[tuple(i)]), int(ref[tuple(i)])) for i in idx]
+
+
+@pytest.mark.parametrize("T", [9, 64, 100, 128, 129])
 def test_verify_expand_bad_tree_rejects(P, T):
     par = W.tree_chain(T)[0][None, :].copy()
     par[0, T // 2] = T // 2  # its own parent
