@@ -298,7 +298,8 @@ size_t ptd_topk_workspace_bytes(int32_t R, int32_t V, int32_t k);
  * Order: value descending; equal values by the lower index; -0.0 equals +0.0.
  * Logits are expected non-NaN (NaN ordering is unspecified); +-inf are ordered.
  * A workspace is needed when a row is split over several workgroups, that is
- * when V exceeds one workgroup's slice (32768 bf16 or 16384 fp32 values);
+ * when V exceeds one workgroup's slice (32768 bf16 or 16384 fp32 values, 1.5
+ * times that when R times the slices of a row would exceed 256);
  * ptd_topk_workspace_bytes gives its size (the larger of the bf16 and fp32
  * needs), 0 when none is needed.  It needs no initialisation, and calls
  * sharing one must not overlap.

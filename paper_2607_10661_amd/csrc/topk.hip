@@ -11,8 +11,9 @@
 // Kernels
 //   k_topk_row      one workgroup per (row, vocabulary slice), a slice being
 //                   at most 4096 chunks of 16 bytes (32768 bf16 or 16384
-//                   fp32 values) held in registers (1024 threads x 4 chunks,
-//                   or 512 x 8 when there are many slices): a cheap lower
+//                   fp32 values; 6144 chunks for a few long rows) held in
+//                   registers (1024 threads x 4 or 6 chunks, or 512 x 8 when
+//                   there are many slices): a cheap lower
 //                   bound of the KMAX-th best value leaves a few candidates,
 //                   ranked by counting (details below).
 //   k_topk_scalar   rows that are not 16-byte aligned: one wave per (row,
@@ -247,6 +248,7 @@ k_topk_row(const void* __restrict__ logits, int V, long long ld, int slices, int
   constexpr int ES = BF16 ? 2 : 4;
   constexpr int NW = NT / PTD_WAVE;
   static_assert(NT >= kCandCap && NW % 4 == 0 && NT * NL <= 65536, "workgroup shape");
+  static_assert((NT & (NT - 1)) == 0, "KMAX groups of NT / KMAX lanes");
   constexpr int GL = PTD_WAVE / KMAX;  // lanes per group inside a wave
   constexpr int GW = NT / KMAX;        // lanes per group across the workgroup
   constexpr int GWL = GW < PTD_WAVE ? GW : PTD_WAVE;  // ... of them inside one wave
@@ -540,14 +542,17 @@ void topk_shape(int R, int V, int E, int* nt, int* nl) {
   // workgroups resident per CU and every lane's loads in flight at once
   // (measured on 1040 rows x 128256 bf16: 53.2 us against 72.9 us for
   // 1024 x 4).  Fewer: 1024 threads of 4 chunks, the shortest latency for a
-  // slice (65 rows x 32000: 5.1 us against 5.1-7.2 us for the others).
-  const long long slices_1024 = (static_cast<long long>(V) + 4096LL * E - 1) / (4096LL * E);
-  if (static_cast<long long>(R) * slices_1024 >= 4 * 256) {
+  // slice (65 rows x 32000: 5.1 us against 5.1-7.2 us for the others), or of
+  // 6 chunks when that leaves one slice per CU where 4 chunks would not
+  // (65 rows x 128256: 3 slices per row, 9.2 against 9.9 us with the merge).
+  const long long s4 = (static_cast<long long>(V) + 4096LL * E - 1) / (4096LL * E);
+  if (static_cast<long long>(R) * s4 >= 4 * 256) {
     *nt = 512;
     *nl = 8;
   } else {
+    const long long s6 = (static_cast<long long>(V) + 6144LL * E - 1) / (6144LL * E);
     *nt = 1024;
-    *nl = 4;
+    *nl = (R * s4 > 256 && R * s6 <= 256) ? 6 : 4;
   }
 }
 
@@ -580,7 +585,7 @@ void launch(const TopkPlan& pl, const void* logits, int R, int V, long long ld, 
   if (pl.nt == nt_ && pl.nl == nl_)                                                              \
     hipLaunchKernelGGL((k_topk_row<KMAX, BF16, nt_, nl_>), dim3(R * pl.slices), dim3(nt_), 0, st, \
                        logits, V, ld, pl.slices, pl.slice_len, k, am, ti, tv, part);
-    PTD_TOPK_ROW(1024, 4) PTD_TOPK_ROW(512, 8)
+    PTD_TOPK_ROW(1024, 4) PTD_TOPK_ROW(1024, 6) PTD_TOPK_ROW(512, 8)
 #undef PTD_TOPK_ROW
   } else
     hipLaunchKernelGGL((k_topk_scalar<KMAX, BF16>), dim3((R * pl.slices + WPB - 1) / WPB),

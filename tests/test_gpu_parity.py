@@ -83,7 +83,8 @@ def _topk_case(P, arr, k, ld=None):
 @pytest.mark.parametrize("R,V,k", [(1, 1, 1), (3, 7, 5), (17, 1000, 4), (65, 32000, 4),
                                    (97, 32000, 5), (8, 32003, 16), (5, 128256, 8),
                                    (1100, 4099, 2), (3, 70001, 8), (2, 200003, 16),
-                                   (2, 300007, 4), (1, 600001, 16), (300, 128256, 8)])
+                                   (2, 300007, 4), (1, 600001, 16), (300, 128256, 8),
+                                   (70, 128256, 8), (16, 600001, 16)])
 def test_topk_random(P, dtype, R, V, k):
     rng = np.random.default_rng(R * 7 + V + k)
     x = rng.standard_normal((R, V), dtype=np.float32) * np.float32(1.41)
