@@ -13,8 +13,8 @@
 // the residual distribution with u_bonus[row].
 //
 // Kernels
-//   k_block_stats    one workgroup per (block of 2048 vocabulary entries,
-//                    logits row): the block maximum m_b and
+//   k_block_stats    one wave per (block of 2048 vocabulary entries, logits
+//                    row), four per workgroup: the block maximum m_b and
 //                    z_b = sum exp((l - m_b) / temperature) over the block,
 //                    each term an fp32 exponential with its argument's
 //                    rounding compensated (~1.2e-7 relative), added in fp64.
@@ -127,63 +127,58 @@ __device__ __forceinline__ void chunk_vals(const u32x4& c, float (&x)[BF16 ? 8 :
   }
 }
 
-// Block maximum, then the block's sum of terms relative to it.  A 16-byte
-// aligned row is read in 16-byte chunks (one or two per thread) plus a scalar
+// Block maximum, then the block's sum of terms relative to it: one wave per
+// (block, row), four blocks per workgroup, no workgroup barrier.  A 16-byte
+// aligned row is read in 16-byte chunks (4 per lane for bf16, 8 for fp32,
+// lane-interleaved and all issued before the first is used) plus a scalar
 // tail in the last block; other rows element by element.
 template <bool BF16>
 __global__ void __launch_bounds__(kStatThreads)
 k_block_stats(const void* __restrict__ logits, int V, long long ld, int nblk, float c_hi,
               float c_lo, RowStat* __restrict__ stats) {
   constexpr int E = BF16 ? 8 : 4;
-  constexpr int NW = kStatThreads / PTD_WAVE;
-  constexpr int CPT = kBlock / E / kStatThreads;  // chunks per thread: 1 (bf16) or 2
-  __shared__ float s_max[NW];
-  __shared__ double s_sum[NW];
-  const int blk = blockIdx.x, r = blockIdx.y, tid = threadIdx.x, lane = tid & 63,
-            wave = tid >> 6;
+  constexpr int CPL = kBlock / E / PTD_WAVE;  // chunks per lane: 4 (bf16) or 8 (fp32)
+  const int lane = threadIdx.x & 63;
+  const int blk = blockIdx.x * (kStatThreads / PTD_WAVE) + (threadIdx.x >> 6);
+  const int r = blockIdx.y;
+  if (blk >= nblk) return;  // whole wave
   const char* row = static_cast<const char*>(logits) + static_cast<size_t>(r) * ld * (BF16 ? 2 : 4);
   const int y0 = blk * kBlock, y1 = min(V, y0 + kBlock);
   const bool vec = (reinterpret_cast<uintptr_t>(row) & 15) == 0;
   const int nch = vec ? (y1 - y0) / E : 0;  // whole chunks of this block
   const u32x4* rc = reinterpret_cast<const u32x4*>(row) + y0 / E;
-  float x[CPT][E];
-  bool have[CPT];
+  u32x4 raw[CPL];
 #pragma unroll
-  for (int j = 0; j < CPT; ++j) {
-    const int c = tid + j * kStatThreads;
-    have[j] = c < nch;
-    if (have[j]) chunk_vals<BF16>(rc[c], x[j]);
+  for (int j = 0; j < CPL; ++j) {
+    const int c = j * PTD_WAVE + lane;
+    raw[j] = c < nch ? rc[c] : u32x4{0u, 0u, 0u, 0u};
   }
   float m = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < CPT; ++j)
-    if (have[j])
+  for (int j = 0; j < CPL; ++j)
+    if (j * PTD_WAVE + lane < nch) {
+      float x[E];
+      chunk_vals<BF16>(raw[j], x);
 #pragma unroll
-      for (int e = 0; e < E; ++e) m = fmaxf(m, x[j][e]);
-  for (int y = y0 + nch * E + tid; y < y1; y += kStatThreads) m = fmaxf(m, logit<BF16>(row, y));
+      for (int e = 0; e < E; ++e) m = fmaxf(m, x[e]);
+    }
+  for (int y = y0 + nch * E + lane; y < y1; y += PTD_WAVE) m = fmaxf(m, logit<BF16>(row, y));
   m = ptd::wave_max(m);
-  if (lane == 0) s_max[wave] = m;
-  __syncthreads();
-#pragma unroll
-  for (int w = 0; w < NW; ++w) m = fmaxf(m, s_max[w]);
   double z = 0.0;
 #pragma unroll
-  for (int j = 0; j < CPT; ++j)
-    if (have[j])
+  for (int j = 0; j < CPL; ++j)
+    if (j * PTD_WAVE + lane < nch) {
+      float x[E];
+      chunk_vals<BF16>(raw[j], x);
 #pragma unroll
       for (int e = 0; e < E; e += 2)  // pairs added in fp32 (one rounding, 2^-24), then fp64
-        z += static_cast<double>(exp_term(x[j][e], m, c_hi, c_lo) + exp_term(x[j][e + 1], m, c_hi, c_lo));
-  for (int y = y0 + nch * E + tid; y < y1; y += kStatThreads)
+        z += static_cast<double>(exp_term(x[e], m, c_hi, c_lo) + exp_term(x[e + 1], m, c_hi, c_lo));
+    }
+  for (int y = y0 + nch * E + lane; y < y1; y += PTD_WAVE)
     z += static_cast<double>(exp_term(logit<BF16>(row, y), m, c_hi, c_lo));
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) z += shfl_xor_f64(z, o);
-  if (lane == 0) s_sum[wave] = z;
-  __syncthreads();
-  if (tid == 0) {
-    double t = 0.0;
-    for (int w = 0; w < NW; ++w) t += s_sum[w];
-    stats[static_cast<size_t>(r) * nblk + blk] = RowStat{static_cast<double>(m), t};
-  }
+  if (lane == 0) stats[static_cast<size_t>(r) * nblk + blk] = RowStat{static_cast<double>(m), z};
 }
 
 struct SampleArgs {
@@ -497,7 +492,7 @@ extern "C" int ptd_verify_sample(const void* logits, ptd_dtype dtype, int32_t V,
   const int nblk = (V + kBlock - 1) / kBlock;
   SampleArgs a{logits, ld, V, T, draft_tokens, parent, tree_len, u_node, u_bonus, stats, nblk,
                1.0 / temperature, c_hi, c_lo, accept_len, accept_nodes, out_tokens, dev_status};
-  const dim3 sgrid(nblk, R);
+  const dim3 sgrid((nblk + kStatThreads / PTD_WAVE - 1) / (kStatThreads / PTD_WAVE), R);
   if (dtype == PTD_BF16) {
     hipLaunchKernelGGL(k_block_stats<true>, sgrid, dim3(kStatThreads), 0, st, logits, V, ld,
                        nblk, c_hi, c_lo, stats);
