@@ -24,8 +24,9 @@
 //                    LDS with sibling links, up to 64 at a time; thread j
 //                    merges every sub-tree whose root token keys staged tree
 //                    j, the sub-tree's nodes in index order (the trees are
-//                    independent and proceed together).  Trees, slots and the
-//                    tree count are written back.
+//                    independent and proceed together).  The appended nodes,
+//                    the trees' node counts, the new slots and the tree count
+//                    are written back (a merge never changes a stored node).
 //   k_pool_retrieve  one workgroup of 192 threads per sequence: 64 hash slots
 //                    from the token's home slot in one load, the tree's nodes
 //                    one per thread, breadth-first order by levels.
@@ -276,7 +277,8 @@ struct MergeLds {
   alignas(16) int key[kMaxSlots];
   alignas(16) int tree[kMaxSlots];
   // draft nodes
-  int par[kMaxNodes], tok[kMaxNodes];
+  int par[kMaxNodes];
+  alignas(16) int tok[kMaxNodes];
   int firstof[kMaxNodes];  // first node in index order with the same token
   int newid[kMaxNodes];    // tree id given to a missing token's first node
   int jof[kMaxNodes];      // index among the touched trees (first nodes)
@@ -290,7 +292,7 @@ struct MergeLds {
   uint64_t wm[2];                // per-wave ballots
   int ntrees, nd;
   // staged trees of one batch: node k of staged tree j at j * n_cap + k
-  int cnt[kStageTrees];
+  int cnt[kStageTrees], cnt0[kStageTrees];
   int ntok[kStageSlots];
   short npar[kStageSlots], fc[kStageSlots], ns[kStageSlots];
   short map[kStageTrees][kMaxNodes];  // draft node -> staged node (-1: dropped)
@@ -329,6 +331,8 @@ k_pool_merge(void* pool, PoolGeom g, const int32_t* __restrict__ parent,
   if (nodes) {
     L.gmask[tid][0] = 0ull;
     L.gmask[tid][1] = 0ull;
+    L.desc[tid][0] = 0ull;
+    L.desc[tid][1] = 0ull;
     L.newslot[tid] = -1;
   }
   {  // the hash table in 16-byte chunks, all of a thread's loads in flight
@@ -370,11 +374,16 @@ k_pool_merge(void* pool, PoolGeom g, const int32_t* __restrict__ parent,
         break;
       }
     }
-    for (int u = 0; u < tid; ++u)
-      if (L.tok[u] == t) {
-        first = u;
-        break;
-      }
+    // four tokens per LDS read (the draft tokens start 16-byte aligned)
+    const int4* tk4 = reinterpret_cast<const int4*>(L.tok);
+    for (int u4 = 0; 4 * u4 < tid && first == tid; ++u4) {
+      const int4 q = tk4[u4];
+      const int u = 4 * u4;
+      if (q.w == t && u + 3 < tid) first = u + 3;
+      if (q.z == t && u + 2 < tid) first = u + 2;
+      if (q.y == t && u + 1 < tid) first = u + 1;
+      if (q.x == t) first = u;
+    }
     L.firstof[tid] = first;
   }
   // new trees for the missing tokens, in index order of their first node
@@ -444,12 +453,13 @@ k_pool_merge(void* pool, PoolGeom g, const int32_t* __restrict__ parent,
     const int j = L.jof[first];
     atomicOr(&L.gmask[j][wave], 1ull << lane);
   }
-  // descendant masks: wave w writes word w of every node's mask
-  if (nodes) {
-    for (int u = 0; u < n; ++u) {
-      const uint64_t d = __ballot(((u < 64 ? anc0 : anc1) >> (u & 63)) & 1ull);
-      if (lane == 0) L.desc[u][wave] = d;
-    }
+  // descendant-or-self masks: every node sets its bit in the mask of each
+  // node of its ancestor-or-self set
+  if (live) {
+    for (uint64_t m = anc0; m; m &= m - 1ull)
+      atomicOr(reinterpret_cast<unsigned long long*>(&L.desc[__builtin_ctzll(m)][wave]), 1ull << lane);
+    for (uint64_t m = anc1; m; m &= m - 1ull)
+      atomicOr(reinterpret_cast<unsigned long long*>(&L.desc[64 + __builtin_ctzll(m)][wave]), 1ull << lane);
   }
   __syncthreads();
   const int nd = L.nd, n_cap = g.n_cap;
@@ -489,36 +499,29 @@ k_pool_merge(void* pool, PoolGeom g, const int32_t* __restrict__ parent,
         L.fc[i] = -1;
         L.ns[i] = -1;
       };
-      for (int i = tid; i < total; i += 2 * kMergeThreads) {
-        int2 va, vb;
-        int ca, cb;
-        load(i, va, ca);
-        load(i + kMergeThreads, vb, cb);
-        store(i, va, ca);
-        store(i + kMergeThreads, vb, cb);
+      constexpr int kInFlight = 8;  // loads of a thread issued before any is used
+      for (int i = tid; i < total; i += kInFlight * kMergeThreads) {
+        int2 v[kInFlight];
+        int c[kInFlight];
+#pragma unroll
+        for (int q = 0; q < kInFlight; ++q) load(i + q * kMergeThreads, v[q], c[q]);
+#pragma unroll
+        for (int q = 0; q < kInFlight; ++q) store(i + q * kMergeThreads, v[q], c[q]);
       }
     }
     __syncthreads();
-    // sibling links of the staged nodes, in insertion order
-    for (int i = tid; i < nb * n_cap; i += kMergeThreads) {
-      const int jl = i / n_cap, k = i - jl * n_cap, base = jl * n_cap, c = L.cnt[jl];
-      if (k == 0 || k >= c) continue;
-      const int p = L.npar[i];
-      if (p < 0) continue;  // parents precede their children
-      int nx = -1;
-      for (int k2 = k + 1; k2 < c; ++k2)
-        if (L.npar[base + k2] == p) {
-          nx = k2;
-          break;
-        }
-      L.ns[i] = static_cast<short>(nx);
-      bool firstk = true;
-      for (int k2 = k - 1; k2 >= 1; --k2)
-        if (L.npar[base + k2] == p) {
-          firstk = false;
-          break;
-        }
-      if (firstk) L.fc[base + p] = static_cast<short>(k);
+    // sibling links of the staged nodes, in insertion order: one thread per
+    // staged tree prepends every node to its parent's list, last node first
+    // (the staging left every link at -1)
+    if (tid < nb) {
+      const int base = tid * n_cap, c = L.cnt[tid];
+      L.cnt0[tid] = L.dnew[j0 + tid] ? 0 : c;  // records below cnt0 are unchanged
+      for (int k = c - 1; k >= 1; --k) {
+        const int p = L.npar[base + k];
+        if (p < 0) continue;  // parents precede their children
+        L.ns[base + k] = L.fc[base + p];
+        L.fc[base + p] = static_cast<short>(k);
+      }
     }
     __syncthreads();
 
@@ -572,7 +575,8 @@ k_pool_merge(void* pool, PoolGeom g, const int32_t* __restrict__ parent,
     for (int i = tid; i < nb * n_cap; i += kMergeThreads) {
       const int jl = i / n_cap, k = i - jl * n_cap;
       const int et = L.dtree[j0 + jl];
-      if (k < L.cnt[jl]) P.node[static_cast<size_t>(et) * n_cap + k] = make_int2(L.ntok[i], L.npar[i]);
+      if (k >= L.cnt0[jl] && k < L.cnt[jl])  // a merge only appends
+        P.node[static_cast<size_t>(et) * n_cap + k] = make_int2(L.ntok[i], L.npar[i]);
       if (k == 0) P.count[et] = L.cnt[jl];
     }
     __syncthreads();  // the staged arrays are reused by the next batch
