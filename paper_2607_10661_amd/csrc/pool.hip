@@ -102,10 +102,18 @@ __device__ __forceinline__ int level_rank(const uint64_t* s_lvl, const int* s_ke
   int rank = 0;
 #pragma unroll
   for (int w = 0; w < NW; ++w)
-    for (uint64_t m = s_lvl[w]; m; m &= m - 1ull) {
-      const int u = 64 * w + __builtin_ctzll(m);
-      const int ku = s_key[u];
-      if (ku < key || (ku == key && u < v)) ++rank;
+    for (uint64_t m = s_lvl[w]; m;) {  // eight members at a time, their keys read together
+      int u[8], ku[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        u[q] = m ? 64 * w + __builtin_ctzll(m) : -1;
+        m &= m - 1ull;
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) ku[q] = u[q] >= 0 ? s_key[u[q]] : 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (u[q] >= 0 && (ku[q] < key || (ku[q] == key && u[q] < v))) ++rank;
     }
   return rank;
 }
@@ -199,8 +207,17 @@ k_step_prune(const int32_t* __restrict__ parent, const int32_t* __restrict__ tok
   __syncthreads();
   int h = 0;
   if (live) {
-    int d = dep;  // v itself is in U[dep]
-    while (d < N && ((s_U[d + 1][wv] >> lane) & 1ull)) ++d;
+    int d = dep;  // v itself is in U[dep]; levels examined eight at a time
+    for (bool more = true; more;) {
+      bool in[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) in[q] = d + 1 + q <= N && ((s_U[min(d + 1 + q, N)][wv] >> lane) & 1ull);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        more &= in[q];
+        d += more ? 1 : 0;
+      }
+    }
     h = d - dep + 1;
   }
   s_h[v] = h;
