@@ -243,19 +243,39 @@ __global__ void __launch_bounds__(kWalkThreads) k_verify_sample(SampleArgs a) {
     my_tok = a.tokens[static_cast<size_t>(b) * T + tid];
     L.u[tid] = a.u_node[static_cast<size_t>(b) * T + tid];
   }
-  for (int r = tid; r <= T; r += kWalkThreads) {
-    const RowStat* bs = a.stats + (row0 + r) * a.nblk;
-    float m = -INFINITY;
-#pragma unroll 8
-    for (int k = 0; k < a.nblk; ++k) m = fmaxf(m, static_cast<float>(bs[k].m));
-    double z = 0.0;
-#pragma unroll 8
-    for (int k = 0; k < a.nblk; ++k) {
-      const RowStat st = bs[k];
-      z += st.z * static_cast<double>(exp_term(static_cast<float>(st.m), m, a.c_hi, a.c_lo));
+  // one wave per row, a lane per block (two above 64 blocks), the loads of
+  // four rows issued before any is used
+  static_assert(kMaxBlocks <= 2 * PTD_WAVE, "two blocks per lane");
+  constexpr int kRowsAtOnce = 4;
+  for (int r0 = wave; r0 <= T; r0 += kRowsAtOnce * kWalkWaves) {
+    RowStat st[kRowsAtOnce][2];
+#pragma unroll
+    for (int j = 0; j < kRowsAtOnce; ++j) {
+      const int r = r0 + j * kWalkWaves;
+      const RowStat* bs = a.stats + (row0 + min(r, T)) * a.nblk;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k = lane + h * PTD_WAVE;
+        st[j][h] = (r <= T && k < a.nblk) ? bs[k] : RowStat{-INFINITY, 0.0};
+      }
     }
-    L.rm[r] = m;
-    L.rz[r] = z;
+#pragma unroll
+    for (int j = 0; j < kRowsAtOnce; ++j) {
+      const int r = r0 + j * kWalkWaves;
+      if (r > T) break;  // uniform
+      const float m = ptd::wave_max(fmaxf(static_cast<float>(st[j][0].m), static_cast<float>(st[j][1].m)));
+      double z = 0.0;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (lane + h * PTD_WAVE < a.nblk)
+          z += st[j][h].z * static_cast<double>(exp_term(static_cast<float>(st[j][h].m), m, a.c_hi, a.c_lo));
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) z += shfl_xor_f64(z, o);
+      if (lane == 0) {
+        L.rm[r] = m;
+        L.rz[r] = z;
+      }
+    }
   }
   if (tid < n) {
     bad = my_par < -1 || my_par >= tid;
@@ -379,35 +399,42 @@ __global__ void __launch_bounds__(kWalkThreads) k_verify_sample(SampleArgs a) {
     return static_cast<double>(exp_term(logit<BF16>(rowp, y), L.bm[k], a.c_hi, a.c_lo)) *
            static_cast<double>(L.bscale[k]);
   };
-  if (tid == 0) {
-    for (int j = 0; j < nrej_t; ++j)  // the rejected tokens' terms leave their blocks
-      L.res[L.rej[j] / kBlock] -= L.p[j];
-    double total = 0.0;
-    for (int k = 0; k < a.nblk; ++k) total += L.res[k];
+  if (wave == 0) {
+    if (lane == 0)
+      for (int j = 0; j < nrej_t; ++j)  // the rejected tokens' terms leave their blocks
+        L.res[L.rej[j] / kBlock] -= L.p[j];
+    // running totals over the blocks (fp64 wave scans, two blocks per lane:
+    // k = lane and k = 64 + lane); the first block with residual mass whose
+    // running total passes the target; if rounding leaves none, the last
+    // block with residual mass
+    const double r0 = lane < a.nblk ? L.res[lane] : 0.0;
+    const double r1 = lane + PTD_WAVE < a.nblk ? L.res[lane + PTD_WAVE] : 0.0;
+    const double i0 = wave_incl_scan_f64(r0);
+    const double t0 = readlane_f64(i0, PTD_WAVE - 1);
+    const double i1 = t0 + wave_incl_scan_f64(r1);
+    const double total = readlane_f64(i1, PTD_WAVE - 1);
     const double target = a.u_bonus[row0 + r] * total;
-    // the first block whose running total passes the target; if rounding
-    // leaves none, the last block with residual mass
-    int xb = -1, lastb = -1;
-    double run = 0.0, before = 0.0, before_last = 0.0;
-    for (int k = 0; k < a.nblk; ++k) {
-      const double rk = L.res[k];
-      if (rk > 0.0) {
-        if (xb < 0 && run + rk > target) {
-          xb = k;
-          before = run;
-        }
-        lastb = k;
-        before_last = run;
-      }
-      run += rk;
+    const uint64_t h0 = __ballot(r0 > 0.0 && i0 > target), h1 = __ballot(r1 > 0.0 && i1 > target);
+    const uint64_t m0 = __ballot(r0 > 0.0), m1 = __ballot(r1 > 0.0);
+    int xb;
+    if (h0 | h1) xb = h0 ? __builtin_ctzll(h0) : PTD_WAVE + __builtin_ctzll(h1);
+    else if (m1 | m0) xb = m1 ? 2 * PTD_WAVE - 1 - __builtin_clzll(m1) : PTD_WAVE - 1 - __builtin_clzll(m0);
+    else xb = -1;
+    // the running total before block xb: the scans' exclusive values (the
+    // shuffles run on every lane; lane 0's results are replaced afterwards)
+    double e0 = shfl_up_f64(i0, 1);
+    double e1 = shfl_up_f64(i1, 1);
+    if (lane == 0) {
+      e0 = 0.0;
+      e1 = t0;
     }
-    if (xb < 0) {
-      xb = lastb;
-      before = before_last;
+    const int xl = xb < 0 ? 0 : xb & (PTD_WAVE - 1);
+    const double b0 = readlane_f64(e0, xl), b1 = readlane_f64(e1, xl);
+    if (lane == 0) {
+      L.xblk = total > 0.0 ? xb : -1;
+      L.before = xb >= PTD_WAVE ? b1 : b0;
+      L.target = target;
     }
-    L.xblk = total > 0.0 ? xb : -1;
-    L.before = before;
-    L.target = target;
   }
   __syncthreads();
   const int xb = L.xblk;

@@ -617,7 +617,9 @@ k_tree_wave(const int32_t* __restrict__ argmax, const int32_t* __restrict__ toke
 #pragma unroll
     for (int x = 0; x < NPL; ++x) {
       const int pa = par[x] + 1;  // the parent's argmax row (0 for a root)
-      const int am_par = pa < NN ? gather_node<NPL>(am, pa) : am_last;
+      // (the gather runs on every lane, outside the select)
+      const int am_g = gather_node<NPL>(am, pa < NN ? pa : 0);
+      const int am_par = pa < NN ? am_g : am_last;
       elig[x] = __ballot(live[x] && tok[x] == am_par);
     }
     int key = -1;
