@@ -1262,12 +1262,14 @@ int attention_impl(const void* q, const void* k_cache, const void* v_cache,
       const int rpb = 256 / (shape->D / 4);  // rows per combine workgroup
       const dim3 grid(static_cast<unsigned>(static_cast<long long>(prm.B) * prm.Hkv *
                                             ((prm.M + rpb - 1) / rpb)));
-      // U = splits loaded at once: the fewest of 2, 4, 8 covering them
-      const int u = pl.splits <= 2 ? 2 : pl.splits <= 4 ? 4 : 8;
+      // U = splits loaded at once: the fewest of 2, 4, 8, 16 covering them
+      // (16 splits in one group of loads rather than two: 72.4 against 76.4
+      // us per call on 8 KV heads x 256 rows x 32832 keys)
+      const int u = pl.splits <= 2 ? 2 : pl.splits <= 4 ? 4 : pl.splits <= 8 ? 8 : 16;
 #define PTD_COMBINE(d_, u_) \
   if (shape->D == d_ && u == u_) hipLaunchKernelGGL((k_attn_combine<d_, u_>), grid, dim3(256), 0, st, prm);
-      PTD_COMBINE(128, 2) PTD_COMBINE(128, 4) PTD_COMBINE(128, 8)
-      PTD_COMBINE(64, 2) PTD_COMBINE(64, 4) PTD_COMBINE(64, 8)
+      PTD_COMBINE(128, 2) PTD_COMBINE(128, 4) PTD_COMBINE(128, 8) PTD_COMBINE(128, 16)
+      PTD_COMBINE(64, 2) PTD_COMBINE(64, 4) PTD_COMBINE(64, 8) PTD_COMBINE(64, 16)
 #undef PTD_COMBINE
     }
   } else {
