@@ -120,6 +120,21 @@ def test_sample_configs(P, name):
                     rng.random((B, T + 1)))
 
 
+@pytest.mark.parametrize("B,T", [(2, 8), (8, 63)])
+def test_sample_wide_rows_f32(P, B, T):
+    # fp32 rows of more than 32 statistics blocks (the walk's wave-per-row
+    # forms), with few blocks per call and with many (8192 or more: the
+    # wave-per-block statistics)
+    rng = np.random.default_rng(11 + B)
+    V = 70001
+    par = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    x = (rng.standard_normal((B, T + 1, V)) * 2.0).astype(np.float32)
+    np.put_along_axis(x, np.argmax(x, axis=-1)[..., None],
+                      np.max(x, axis=-1, keepdims=True) + 6.0, axis=-1)
+    tok = likely_tokens(rng, x, par, top=2, p_random=0.1)
+    sample_case(P, x, tok, par, 1.0, rng.random((B, T)), rng.random((B, T + 1)))
+
+
 def test_sample_wide_star_with_duplicates(P):
     # one node with 1000 children (many rejections, repeated tokens): the
     # rejected-token bitmap and the residual CDF
