@@ -441,6 +441,7 @@ SMALL = [
     _spec(D=64, Hq=4, Hkv=2, T=9, kv_len=5000, L_pad=40),
     _spec(tree="chain", T=128, kv_len=40, Hq=2, Hkv=2),  # walks of 128 nodes
     _spec(Hq=2, Hkv=2, T=100, kv_len=3000),          # two words, many KV splits
+    _spec(Hq=1, Hkv=1, T=8, kv_len=12000),           # 47 KV splits: three combine groups
 ]
 
 
