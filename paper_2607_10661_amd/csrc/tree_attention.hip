@@ -730,38 +730,95 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     sc = qk(read_k(cs));
     mask_tile(sc, kg);
   }
-  for (int rd = 0; rd < nrounds; ++rd) {
-    const bool do_wait = PIPE ? rd + 1 < nrounds : rd >= 1;
-    if (do_wait) {
-      if (rd >= 1 && rd <= steady_end) {
-        wait_vmcnt<(R::NS - (2 + (PIPE ? 1 : 0)) * WK) * R::DPS>();
-      } else {
-        const int issued = min(ntiles, R::NS + max(0, rd - 1) * WK);
-        const int needed = min(ntiles, (rd + 1 + (PIPE ? 1 : 0)) * WK);
-        wait_vmcnt_le((issued - needed) * R::DPS);
-      }
-      lds_barrier();
-      if (rd >= 1) {
+  // a round in general: waits by the count of copies issued so far, refills
+  // (whole or last sub-tiles, contiguous or paged caches), masked sub-tiles
+  auto round = [&](int rd) __attribute__((always_inline)) {
+      const bool do_wait = PIPE ? rd + 1 < nrounds : rd >= 1;
+      if (do_wait) {
+        if (rd >= 1 && rd <= steady_end) {
+          wait_vmcnt<(R::NS - (2 + (PIPE ? 1 : 0)) * WK) * R::DPS>();
+        } else {
+          const int issued = min(ntiles, R::NS + max(0, rd - 1) * WK);
+          const int needed = min(ntiles, (rd + 1 + (PIPE ? 1 : 0)) * WK);
+          wait_vmcnt_le((issued - needed) * R::DPS);
+        }
+        lds_barrier();
+        if (rd >= 1) {
 #pragma unroll
-        for (int w = 0; w < WK; ++w) {
-          const int tt = R::NS + (rd - 1) * WK + w;
-          if (tt < ntiles) issue(tt, rs);
-          rs = rs + 1 == R::NS ? 0 : rs + 1;
+          for (int w = 0; w < WK; ++w) {
+            const int tt = R::NS + (rd - 1) * WK + w;
+            if (tt < ntiles) issue(tt, rs);
+            rs = rs + 1 == R::NS ? 0 : rs + 1;
+          }
         }
       }
+      int ns = cs + WK;
+      if (ns >= R::NS) ns -= R::NS;
+      const int j = rd * WK + kg;
+      if (wave_live && j < ntiles) {
+        float pv[QB][8], pm[QB];
+        if constexpr (PIPE) {
+          // next K reads in flight while this sub-tile's exponentials run (they
+          // overlap the previous round's PV MFMAs, still executing); then the
+          // next QK^T and this PV back to back on the matrix cores.  After the
+          // wave's last sub-tile the next-tile QK^T works on whatever the slot
+          // holds and its result is dropped: one code path keeps the register
+          // allocation of this loop within the two-waves-per-SIMD budget.
+          const KFrag kf = read_k(ns);
+          exp_tile(sc, pv, pm);
+          PFrag pf;
+          const unsigned precise = to_p(sc, pv, pm, pf);
+          Tile sn = qk(kf);
+          const VFrag vf = read_v(cs);
+          pv_acc(vf, pf, precise);
+          if (j + WK < ntiles) mask_tile(sn, j + WK);
+          sc = sn;
+        } else {
+          sc = qk(read_k(cs));
+          mask_tile(sc, j);
+          const VFrag vf = read_v(cs);
+          exp_tile(sc, pv, pm);
+          PFrag pf;
+          const unsigned precise = to_p(sc, pv, pm, pf);
+          pv_acc(vf, pf, precise);
+        }
+      }
+      cs = ns;
+  };
+  // Steady rounds (the software pipeline only): every refill of the round is
+  // a whole sub-tile of a contiguous cache below t_mask0, so the next
+  // sub-tiles need no masking either; the wait count is the constant, the
+  // tile address scalar arithmetic, and the general round's tests drop out.
+  // The scalar instructions of a round are issued by the CU's one scalar unit
+  // for every wave, and the two waves of a SIMD reach the refills together:
+  // measured on 8 KV heads x 256 rows x 32832 keys, 70.7 against 76.0 us per
+  // call; on ragged-16, 156.2 against 171.2.
+  const int steady_hi =
+      (PIPE && !paged && t_mask0 >= R::NS + WK) ? (t_mask0 - R::NS - WK) / WK + 1 : 0;
+  auto round_steady = [&](int rd) __attribute__((always_inline)) {
+    wait_vmcnt<(R::NS - 3 * WK) * R::DPS>();
+    lds_barrier();
+#pragma unroll
+    for (int w = 0; w < WK; ++w) {
+      const int tt = R::NS + (rd - 1) * WK + w;
+      const size_t tile = static_cast<size_t>(start + tt * R::SUB) * D;
+      const uint32_t slot_lds = ring + rs * R::SLOT;
+      if constexpr (R::DPS == 1) {
+        dma16_s((cp_v[0] ? vbase : kbase) + tile, cp_voff[0], slot_lds + cp_lds[0]);
+      } else {
+#pragma unroll
+        for (int u = 0; u < R::DPS; u += 2)
+          ptd::dma16_s2((cp_v[u] ? vbase : kbase) + tile, cp_voff[u], slot_lds + cp_lds[u],
+                        (cp_v[u + 1] ? vbase : kbase) + tile, cp_voff[u + 1],
+                        slot_lds + cp_lds[u + 1]);
+      }
+      rs = rs + 1 == R::NS ? 0 : rs + 1;
     }
     int ns = cs + WK;
     if (ns >= R::NS) ns -= R::NS;
-    const int j = rd * WK + kg;
-    if (wave_live && j < ntiles) {
-      float pv[QB][8], pm[QB];
-      if constexpr (PIPE) {
-        // next K reads in flight while this sub-tile's exponentials run (they
-        // overlap the previous round's PV MFMAs, still executing); then the
-        // next QK^T and this PV back to back on the matrix cores.  After the
-        // wave's last sub-tile the next-tile QK^T works on whatever the slot
-        // holds and its result is dropped: one code path keeps the register
-        // allocation of this loop within the two-waves-per-SIMD budget.
+    if constexpr (PIPE) {
+      if (wave_live) {
+        float pv[QB][8], pm[QB];
         const KFrag kf = read_k(ns);
         exp_tile(sc, pv, pm);
         PFrag pf;
@@ -769,20 +826,18 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         Tile sn = qk(kf);
         const VFrag vf = read_v(cs);
         pv_acc(vf, pf, precise);
-        if (j + WK < ntiles) mask_tile(sn, j + WK);
         sc = sn;
-      } else {
-        sc = qk(read_k(cs));
-        mask_tile(sc, j);
-        const VFrag vf = read_v(cs);
-        exp_tile(sc, pv, pm);
-        PFrag pf;
-        const unsigned precise = to_p(sc, pv, pm, pf);
-        pv_acc(vf, pf, precise);
       }
     }
     cs = ns;
+  };
+  int rd0 = 0;
+  if (steady_hi >= 1) {
+    round(0);
+    for (int rd = 1; rd <= steady_hi; ++rd) round_steady(rd);
+    rd0 = steady_hi + 1;
   }
+  for (int rd = rd0; rd < nrounds; ++rd) round(rd);
   wait_vmcnt<0>();
   lds_barrier();  // every copy landed and every wave is done with the ring
 
