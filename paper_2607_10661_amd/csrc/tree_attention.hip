@@ -559,15 +559,20 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   };
 
   // ---- online softmax state.  Scores become p = 2^(s*c - m*c) against a
-  //      reference maximum m per query row that moves lazily.  The partial
-  //      row sums of p, needed anyway, serve as the test: while no lane's sum
-  //      over a sub-tile exceeds 2^16, no p does, and O, l stay far inside the
-  //      fp32 range with m unchanged.  Otherwise (the first keys a row sees,
-  //      m still at its start value, or a score well above m) the rows'
-  //      maxima are formed, m moves up to them, O and l are rescaled and the
-  //      sub-tile's p are recomputed.
+  //      reference maximum m per query row that moves lazily: while no p of a
+  //      sub-tile exceeds 2^16, O and l stay far inside the fp32 range and m
+  //      is kept.  Otherwise (the first keys a row sees, m still at its start
+  //      value, or a score well above m) the rows' maxima are formed, m moves
+  //      up to them, O and l are rescaled and the sub-tile's p are recomputed.
+  //      The row sums l run on the matrix cores: an MFMA of the bf16 P
+  //      fragment with an all-ones A operand gives every output row the sums
+  //      of P's columns over the 32 keys, so each lane holds its query
+  //      column's l with no cross-lane reduction (two MFMAs per sub-tile
+  //      against about thirty vector instructions for dot products and
+  //      cross-lane sums).
   f32x4 o[QB][DT];
-  float m[QB], nmc[QB], lsum[QB];
+  float m[QB], nmc[QB];
+  f32x4 ls[QB];  // row sums of p (all four elements: the lane's query column)
   // score scale in the exp2 domain; 8-bit keys carry their head's scale
   const float c = F8 && p.k_scale ? p.c * p.k_scale[g] : p.c;
   const float vsc = F8 && p.v_scale ? p.v_scale[g] : 1.0f;  // value scale
@@ -575,7 +580,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   for (int qb = 0; qb < QB; ++qb) {
     m[qb] = kNegBig;
     nmc[qb] = -kNegBig * c;
-    lsum[qb] = 0.f;
+    ls[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[qb][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -592,18 +597,9 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
                      fmaxf(fmaxf(pv[qb][4], pv[qb][5]), fmaxf(pv[qb][6], pv[qb][7])));
     }
   };
-  // sum of the eight bf16 values of f added to acc (v_dot2 with ones; each
-  // pair taken by an explicit shuffle: element extraction through a bit cast
-  // of the packed vector fed the same dword to every v_dot2)
-  using bf16x2 = __bf16 __attribute__((ext_vector_type(2)));
-  const bf16x2 one2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);
-  auto rowsum = [&](float acc, bf16x8 f) __attribute__((always_inline)) -> float {
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 0, 1), one2, acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 2, 3), one2, acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 4, 5), one2, acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 6, 7), one2, acc, false);
-    return acc;
-  };
+  // bf16 ones: A operand of the row-sum MFMA (every output row = the sum of
+  // the B operand's column over the 32 keys)
+  const bf16x8 ones8 = __builtin_bit_cast(bf16x8, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
   // rare: move the reference of rows whose maximum passed it (uniform over
   // the row's four lanes)
   auto move_ref = [&](const Tile& x) __attribute__((always_inline)) {
@@ -616,7 +612,12 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         const float alpha = __builtin_amdgcn_exp2f((m[qb] - mx) * c);  // 0 for the first keys
         m[qb] = mx;
         nmc[qb] = -mx * c;
-        lsum[qb] *= alpha;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float v = ls[qb][e];
+          asm volatile("v_mul_f32 %0, %0, %1" : "+v"(v) : "v"(alpha));
+          ls[qb][e] = v;
+        }
         // in-place scaling of the accumulators (asm keeps the compiler from
         // duplicating them around this rarely taken path)
 #pragma unroll
@@ -643,8 +644,11 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       for (int qb = 0; qb < QB; ++qb)
         o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v.v[dt], f.hi[qb], o[qb][dt], 0, 0, 0);
 #pragma unroll
+    for (int qb = 0; qb < QB; ++qb) ls[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones8, f.hi[qb], ls[qb], 0, 0, 0);
+#pragma unroll
     for (int qb = 0; qb < QB; ++qb)
       if (precise & (1u << qb)) {
+        ls[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones8, f.lo[qb], ls[qb], 0, 0, 0);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
           o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v.v[dt], f.lo[qb], o[qb][dt], 0, 0, 0);
@@ -685,7 +689,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
     unsigned pmask = 0;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
-      pmask |= __any(!(pm[qb] <= kPreciseFrac * sum_xor32(sum_xor16(lsum[qb])))) ? (1u << qb) : 0u;
+      pmask |= __any(!(pm[qb] <= kPreciseFrac * ls[qb][0])) ? (1u << qb) : 0u;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       const bool precise = pmask & (1u << qb);
@@ -693,14 +697,12 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 #pragma unroll
       for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[qb][2 * w], pv[qb][2 * w + 1]);
       f.hi[qb] = __builtin_bit_cast(bf16x8, ph);
-      lsum[qb] = rowsum(lsum[qb], f.hi[qb]);
       if (precise) {
 #pragma unroll
         for (int w = 0; w < 4; ++w)
           pl[w] = ptd::cvt_pk_bf16(pv[qb][2 * w] - static_cast<float>(f.hi[qb][2 * w]),
                                    pv[qb][2 * w + 1] - static_cast<float>(f.hi[qb][2 * w + 1]));
         f.lo[qb] = __builtin_bit_cast(bf16x8, pl);
-        lsum[qb] = rowsum(lsum[qb], f.lo[qb]);
       }
     }
     return pmask;
@@ -792,7 +794,12 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   // The scalar instructions of a round are issued by the CU's one scalar unit
   // for every wave, and the two waves of a SIMD reach the refills together:
   // measured on 8 KV heads x 256 rows x 32832 keys, 70.7 against 76.0 us per
-  // call; on ragged-16, 156.2 against 171.2.
+  // call; on ragged-16, 156.2 against 171.2.  A steady round also splits the
+  // hi + lo P of the general round: the bf16 P and its PV and row-sum MFMAs
+  // always, the residues and their MFMAs after them in a rarely taken branch,
+  // so the main path is one block the scheduling groups below can interleave
+  // (the precise test still reads the row sums before this sub-tile, and
+  // every accumulator receives hi before lo as in the general round).
   const int steady_hi =
       (PIPE && !paged && t_mask0 >= R::NS + WK) ? (t_mask0 - R::NS - WK) / WK + 1 : 0;
   auto round_steady = [&](int rd) __attribute__((always_inline)) {
@@ -821,11 +828,67 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
         float pv[QB][8], pm[QB];
         const KFrag kf = read_k(ns);
         exp_tile(sc, pv, pm);
-        PFrag pf;
-        const unsigned precise = to_p(sc, pv, pm, pf);
         Tile sn = qk(kf);
+        // the K reads, a few exponentials, then one QK^T MFMA per three
+        // vector instructions (scheduling groups: 0x100 LDS reads, 0x002
+        // vector ALU, 0x008 MFMA)
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+#pragma unroll
+        for (int i = 0; i < 2 * QB * DB; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        }
+        bool over = false;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) over |= !(pm[qb] <= 65536.0f);
+        if (__any(over)) {
+          move_ref(sc);
+          exp_tile(sc, pv, pm);
+        }
+        unsigned pmask = 0;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          pmask |= __any(!(pm[qb] <= kPreciseFrac * ls[qb][0])) ? (1u << qb) : 0u;
+        PFrag pf;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          u32x4 ph;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) ph[w] = ptd::cvt_pk_bf16(pv[qb][2 * w], pv[qb][2 * w + 1]);
+          pf.hi[qb] = __builtin_bit_cast(bf16x8, ph);
+        }
         const VFrag vf = read_v(cs);
-        pv_acc(vf, pf, precise);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf.v[dt], pf.hi[qb], o[qb][dt], 0, 0, 0);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) ls[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones8, pf.hi[qb], ls[qb], 0, 0, 0);
+        // the V reads, then one PV MFMA per two vector instructions
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 1);
+#pragma unroll
+        for (int i = 0; i < DT * QB; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 1);
+        }
+        if (pmask) {
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            if (pmask & (1u << qb)) {
+              u32x4 pl;
+#pragma unroll
+              for (int w = 0; w < 4; ++w)
+                pl[w] = ptd::cvt_pk_bf16(pv[qb][2 * w] - static_cast<float>(pf.hi[qb][2 * w]),
+                                         pv[qb][2 * w + 1] - static_cast<float>(pf.hi[qb][2 * w + 1]));
+              pf.lo[qb] = __builtin_bit_cast(bf16x8, pl);
+              ls[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones8, pf.lo[qb], ls[qb], 0, 0, 0);
+#pragma unroll
+              for (int dt = 0; dt < DT; ++dt)
+                o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf.v[dt], pf.lo[qb], o[qb][dt], 0, 0, 0);
+            }
+        }
         sc = sn;
       }
     }
@@ -842,11 +905,10 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   lds_barrier();  // every copy landed and every wave is done with the ring
 
 
-  // ---- per-column totals of the softmax denominator
+  // ---- softmax denominators (each lane: its query column's)
+  float lsum[QB];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    lsum[qb] = sum_xor32(sum_xor16(lsum[qb]));
-  }
+  for (int qb = 0; qb < QB; ++qb) lsum[qb] = ls[qb][0];
 
   // ---- epilogue.  The key groups of a row group hold their fragments in the
   //      same lane layout (lane: query column l16, d = 16*dt + 4*l4 + 0..3), so
