@@ -804,7 +804,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   // every accumulator receives hi before lo as in the general round).
   const int steady_hi =
       (!paged && t_mask0 >= R::NS + WK) ? (t_mask0 - R::NS - WK) / WK + 1 : 0;
-  auto round_steady = [&](int rd, Tile& cur, Tile& nxt) __attribute__((always_inline)) {
+  auto round_steady = [&](int rd) __attribute__((always_inline)) {
     wait_vmcnt<(R::NS - (2 + (PIPE ? 1 : 0)) * WK) * R::DPS>();
     lds_barrier();
 #pragma unroll
@@ -829,8 +829,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
       if (wave_live) {
         float pv[QB][8], pm[QB];
         const KFrag kf = read_k(ns);
-        exp_tile(cur, pv, pm);
-        nxt = qk(kf);
+        exp_tile(sc, pv, pm);
+        Tile sn = qk(kf);
         // the K reads, a few exponentials, then one QK^T MFMA per three
         // vector instructions (scheduling groups: 0x100 LDS reads, 0x002
         // vector ALU, 0x008 MFMA)
@@ -845,8 +845,8 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) over |= !(pm[qb] <= 65536.0f);
         if (__any(over)) {
-          move_ref(cur);
-          exp_tile(cur, pv, pm);
+          move_ref(sc);
+          exp_tile(sc, pv, pm);
         }
         unsigned pmask = 0;
 #pragma unroll
@@ -891,16 +891,16 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
                 o[qb][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf.v[dt], pf.lo[qb], o[qb][dt], 0, 0, 0);
             }
         }
-
+        sc = sn;
       }
     } else {
       if (wave_live) {
         float pv[QB][8], pm[QB];
-        cur = qk(read_k(cs));
+        sc = qk(read_k(cs));
         const VFrag vf = read_v(cs);
-        exp_tile(cur, pv, pm);
+        exp_tile(sc, pv, pm);
         PFrag pf;
-        const unsigned precise = to_p(cur, pv, pm, pf);
+        const unsigned precise = to_p(sc, pv, pm, pf);
         pv_acc(vf, pf, precise);
       }
     }
@@ -909,20 +909,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   int rd0 = 0;
   if (steady_hi >= 1) {
     round(0);
-    // two rounds per iteration with the score tiles' roles swapped, so the
-    // next scores never have to be copied into the current ones (eight
-    // 64-bit moves per round: 64.2 against 65.2 us on 8B-long, 148.5 against
-    // 150.9 on ragged-16)
-    Tile sc2;
-    int rd = 1;
-    for (; rd + 1 <= steady_hi; rd += 2) {
-      round_steady(rd, sc, sc2);
-      round_steady(rd + 1, sc2, sc);
-    }
-    if (rd <= steady_hi) {
-      round_steady(rd, sc, sc2);
-      sc = sc2;
-    }
+    for (int rd = 1; rd <= steady_hi; ++rd) round_steady(rd);
     rd0 = steady_hi + 1;
   }
   for (int rd = rd0; rd < nrounds; ++rd) round(rd);
