@@ -92,12 +92,21 @@ __device__ inline int live_nodes(const AttnParams& p, int b) {
   return p.tree_len ? min(max(p.tree_len[b], 0), p.T) : p.T;
 }
 
-__device__ inline void logical_block(int nblocks, int& id) {
-  // Work items that share K/V and queries (the splits of one (b, g)) get
-  // consecutive logical ids; blocks are dealt round-robin over the 8 XCDs, so
-  // map each XCD to one contiguous range of logical ids (same L2).
+__device__ inline void logical_block(int nblocks, int npairs, bool by_size, int& id) {
+  // Workgroups are dealt round-robin over the 8 XCDs (block i to XCD i mod 8)
+  // and each XCD runs its share in block order.  The items of one (b, g) pair
+  // (its row passes and KV splits) share keys and query rows, so they stay on
+  // one XCD (one L2), consecutive.  With the sequences ordered by size
+  // (by_size), the pairs are dealt round-robin over the XCDs too (pair q to
+  // XCD q mod 8), so every XCD gets a like share of long and short sequences
+  // and runs its own largest first; otherwise each XCD takes a contiguous
+  // range of pairs.
   const int bid = blockIdx.x;
-  if ((nblocks & 7) == 0) {
+  if (by_size && (npairs & 7) == 0 && (nblocks & 7) == 0) {
+    const int ips = nblocks / npairs;  // items per pair
+    const int x = bid & 7, j = bid >> 3;
+    id = (x + 8 * (j / ips)) * ips + j % ips;
+  } else if ((nblocks & 7) == 0) {
     id = (bid & 7) * (nblocks >> 3) + (bid >> 3);
   } else {
     id = bid;
@@ -220,14 +229,32 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   const int l16 = lane & 15;
   const int l4 = lane >> 4;
 
+  // A batch of up to 64 sequences is taken largest first (size = committed
+  // keys + tree nodes; ties in index order): the longest workgroups start
+  // first and the short ones fill in at the end.  Work item b names the b-th
+  // largest sequence; each wave ranks the sizes with shuffles.
+  const bool by_size = p.B > 1 && p.B <= PTD_WAVE;
   int id;
-  logical_block(gridDim.x, id);
+  logical_block(gridDim.x, p.B * p.Hkv, by_size, id);
   const int split = id % p.splits;
   int rest = id / p.splits;
   const int pass = rest % p.passes;
   rest /= p.passes;
   const int g = rest % p.Hkv;
-  const int b = rest / p.Hkv;
+  int b = rest / p.Hkv;
+  if (by_size) {
+    const int bl = b;
+    int nl = -1;
+    if (lane < p.B) nl = p.kv_len[lane] + live_nodes(p, lane);
+    int rank = 0;
+    for (int j = 0; j < p.B; ++j) {
+      const int nj = __shfl(nl, j, PTD_WAVE);
+      rank += (nj > nl || (nj == nl && j < lane)) ? 1 : 0;
+    }
+    // the ranks of lanes < B are a permutation of 0 .. B-1: one lane hits
+    const uint64_t hit = __ballot(lane < p.B && rank == bl);
+    b = hit ? __builtin_ctzll(hit) : bl;
+  }
 
   const int n_kv = p.kv_len[b];
   const int tl = live_nodes(p, b);
