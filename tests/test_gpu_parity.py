@@ -442,6 +442,14 @@ SMALL = [
     _spec(tree="chain", T=128, kv_len=40, Hq=2, Hkv=2),  # walks of 128 nodes
     _spec(Hq=2, Hkv=2, T=100, kv_len=3000),          # two words, many KV splits
     _spec(Hq=1, Hkv=1, T=8, kv_len=12000),           # 47 KV splits: three combine groups
+    # batches taken largest first: 64 sequences (every lane ranks one; 64
+    # (b, g) pairs dealt over the XCDs), 12 with equal sizes (ties in index
+    # order; 24 pairs), 5 (pairs not a multiple of 8: contiguous XCD ranges),
+    # and 65 (beyond one wave: index order)
+    _spec(B=64, Hq=2, Hkv=1, T=8, kv_len=[(37 * i) % 300 for i in range(64)]),
+    _spec(B=12, Hq=4, Hkv=2, T=16, kv_len=[200, 50, 200, 200, 0, 50, 700, 700, 3, 200, 50, 700]),
+    _spec(B=5, Hq=2, Hkv=1, T=20, kv_len=[10, 900, 300, 900, 1]),
+    _spec(B=65, Hq=2, Hkv=1, T=4, kv_len=[(53 * i) % 400 for i in range(65)]),
 ]
 
 
