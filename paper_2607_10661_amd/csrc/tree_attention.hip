@@ -10,13 +10,15 @@
 //   k_attn_mfma    bf16 q/k/v.  One workgroup = (b, g, row pass, KV split);
 //                  8 waves (2 per SIMD), each owning up to 32 query rows.  K/V
 //                  stream HBM -> LDS with asynchronous copies into a ring of
-//                  nine 32-key sub-tiles (144 KB in flight), shared by every
+//                  ten 32-key sub-tiles (all 160 KB of LDS), shared by every
 //                  query row of the GQA group; V is read transposed straight
-//                  from its natural layout with ds_read_b64_tr_b16.  Scores are computed
-//                  transposed, S^T = K Q^T, and the output as O^T = V^T P^T,
-//                  so each lane owns one query column in both accumulators and
-//                  the online-softmax rescale is lane-local.  MFMA:
-//                  v_mfma_f32_16x16x32_bf16, fp32 accumulation.
+//                  from its natural layout with ds_read_b64_tr_b16.  Scores
+//                  are computed transposed, S^T = K Q^T, and the output as
+//                  O^T = V^T P^T, so each lane owns one query column in both
+//                  accumulators and the online-softmax rescale is lane-local;
+//                  the softmax row sums are one more MFMA of P with an
+//                  all-ones operand.  MFMA: v_mfma_f32_16x16x32_bf16, fp32
+//                  accumulation.
 //                  Trees of up to 128 nodes need no mask pass: each lane
 //                  holds two parent[] entries and walks its rows' ancestor
 //                  chains with wave shuffles.  With the keys split over
@@ -695,7 +697,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   //      The denominator adds the same bf16 p that enter O, so that O is
   //      the exact average of V under the rounded weights.  A query block
   //      of a tile in which some p exceeds kPreciseFrac of its row's sum so
-  //      far (this wave's keys, the four lanes of the query column added)
+  //      far (this wave's keys, from the row-sum accumulator)
   //      carries p as bf16 hi + lo (residue at most 2^-16 p instead of
   //      2^-8 p): every key carried as plain bf16 then weighs at most
   //      kPreciseFrac of its row's final sum, so the 2^-8 relative rounding
