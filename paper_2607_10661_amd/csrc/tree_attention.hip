@@ -630,34 +630,22 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   // the B operand's column over the 32 keys)
   const bf16x8 ones8 = __builtin_bit_cast(bf16x8, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
   // rare: move the reference of rows whose maximum passed it (uniform over
-  // the row's four lanes)
+  // the row's four lanes).  Every lane runs the same instructions (a factor
+  // of 1 where the reference stays): rescaling accumulators under a per-lane
+  // branch returned wrong row sums in some builds.
   auto move_ref = [&](const Tile& x) __attribute__((always_inline)) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float mx = fmaxf(fmaxf(fmaxf(x.s[0][qb][0], x.s[0][qb][1]), fmaxf(x.s[0][qb][2], x.s[0][qb][3])),
                        fmaxf(fmaxf(x.s[1][qb][0], x.s[1][qb][1]), fmaxf(x.s[1][qb][2], x.s[1][qb][3])));
       mx = max_xor32(max_xor16(mx));
-      if (mx > m[qb]) {
-        const float alpha = __builtin_amdgcn_exp2f((m[qb] - mx) * c);  // 0 for the first keys
-        m[qb] = mx;
-        nmc[qb] = -mx * c;
+      const bool up = mx > m[qb];
+      const float alpha = up ? __builtin_amdgcn_exp2f((m[qb] - mx) * c) : 1.0f;  // 0 for the first keys
+      m[qb] = up ? mx : m[qb];
+      nmc[qb] = up ? -mx * c : nmc[qb];
+      ls[qb] *= alpha;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float v = ls[qb][e];
-          asm volatile("v_mul_f32 %0, %0, %1" : "+v"(v) : "v"(alpha));
-          ls[qb][e] = v;
-        }
-        // in-place scaling of the accumulators (asm keeps the compiler from
-        // duplicating them around this rarely taken path)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float v = o[qb][dt][e];
-            asm volatile("v_mul_f32 %0, %0, %1" : "+v"(v) : "v"(alpha));
-            o[qb][dt][e] = v;
-          }
-      }
+      for (int dt = 0; dt < DT; ++dt) o[qb][dt] *= alpha;
     }
   };
   // p of a tile as bf16 MFMA operands (B of O^T += V^T P^T: lane holds its
