@@ -173,20 +173,21 @@ __device__ __forceinline__ bf16x8 e4m3x8_to_bf16(u32x2 w) {
 // transpose read (8 rows x 2 adjacent chunks) covers all 16 chunk positions
 // once (177 B/clk).  Otherwise (bf16 D = 64, E4M3 D = 128: 8 chunks) both
 // use r mod 8.
-template <int D, int ES>
+template <int D, int ES, int NT = kThreads>
 struct Ring {
   static constexpr int RB = D * ES;                  // bytes per row
   static constexpr int CH = RB / 16;                 // 16-byte chunks per row
   static constexpr int SUB = 32;                     // keys per sub-tile
   static constexpr int PART = SUB * RB;              // bytes of K (or V) per sub-tile
   static constexpr int SLOT = 2 * PART;              // K + V
-  // sub-tiles in the ring: all of LDS for bf16 (10); 10 for E4M3 as well
-  // (80 KB): a deeper ring, every slot requested at the start, made the first
-  // sub-tiles land later (measured 1-6 % slower calls)
-  static constexpr int NS = ES == 1 ? 10 : (160 * 1024) / SLOT;
-  static constexpr int DPS = 2 * SUB * CH / kThreads;  // copies per thread per sub-tile
+  // sub-tiles in the ring: all of LDS for bf16 with 512-thread workgroups
+  // (10), half of it with 256-thread ones (two workgroups per CU: 5); 10 for
+  // E4M3 (80 KB) either way: a deeper ring, every slot requested at the
+  // start, made the first sub-tiles land later (measured 1-6 % slower calls)
+  static constexpr int NS = ES == 1 ? 10 : (160 * 1024 / (kThreads / NT)) / SLOT;
+  static constexpr int DPS = 2 * SUB * CH / NT;  // copies per thread per sub-tile
   static constexpr int BYTES = NS * SLOT;
-  static_assert((DPS == 1 || DPS % 2 == 0) && (2 * SUB * CH) % kThreads == 0, "sub-tile split");
+  static_assert((DPS == 1 || DPS % 2 == 0) && (2 * SUB * CH) % NT == 0, "sub-tile split");
   __device__ static int swz_k(int row, int chunk) { return chunk ^ (row & (CH - 1)); }
   __device__ static int swz_v(int row, int chunk) {
     if constexpr (CH == 16) return chunk ^ (((row & 7) << 1) | ((row >> 3) & 1));
@@ -206,14 +207,14 @@ __device__ __forceinline__ u32x4 gload16(const void* p) {
 // Orders every later use of v after the preceding (volatile) wait.
 __device__ __forceinline__ void reg_fence(u32x4& v) { asm volatile("" : "+v"(v)); }
 
-template <int D, int QB, int WR, bool F8>
-__global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
+template <int D, int QB, int WR, bool F8, int NT = kThreads>
+__global__ void __launch_bounds__(NT, kThreads / NT) k_attn_mfma(AttnParams p) {
   // F8: keys and values are OCP E4M3 codes (scaled per KV head), widened to
   // bf16 exactly after the LDS reads; everything else is the bf16 kernel
   using KV = std::conditional_t<F8, uint8_t, uint16_t>;
   constexpr int ES = F8 ? 1 : 2;
-  using R = Ring<D, ES>;
-  constexpr int WK = (kThreads / PTD_WAVE) / WR;  // key groups: sub-tiles per round
+  using R = Ring<D, ES, NT>;
+  constexpr int WK = (NT / PTD_WAVE) / WR;  // key groups: sub-tiles per round
   constexpr int DB = D / 32;                      // 32-wide d blocks (QK^T k-dim)
   constexpr int DT = D / 16;                      // 16-wide d tiles (PV output rows)
   constexpr int PARK_O = WK > 1 ? WR * WK * QB * DT * 64 * 16 : 0;  // parked fragments
@@ -271,7 +272,7 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   if (start >= end) {  // empty split: the combine skips it
     if (p.splits == 1) {  // no keys at all (every node padding): zero rows
       const int r0 = pass * p.rows_per_pass, r1 = min(p.M, r0 + p.rows_per_pass);
-      for (int x = tid; x < (r1 - r0) * D; x += kThreads) {
+      for (int x = tid; x < (r1 - r0) * D; x += NT) {
         const int r = r0 + x / D, d = x % D;
         const size_t off = ((static_cast<size_t>(b) * p.T + r / p.G) * p.Hq + g * p.G + r % p.G) * D + d;
         if (p.out_bf16) static_cast<uint16_t*>(p.out)[off] = 0;
@@ -336,14 +337,14 @@ __global__ void __launch_bounds__(kThreads, 1) k_attn_mfma(AttnParams p) {
   bool cp_v[R::DPS];
 #pragma unroll
   for (int u = 0; u < R::DPS; ++u) {
-    const int c = u * kThreads + tid;
-    cp_v[u] = (u * kThreads + wave * PTD_WAVE) / (R::SUB * R::CH) != 0;
+    const int c = u * NT + tid;
+    cp_v[u] = (u * NT + wave * PTD_WAVE) / (R::SUB * R::CH) != 0;
     const int local = c % (R::SUB * R::CH);
     cp_row[u] = local / R::CH;
     cp_off[u] = (cp_v[u] ? R::swz_v(cp_row[u], local % R::CH)
                          : R::swz_k(cp_row[u], local % R::CH)) * (16 / ES);  // elements
     cp_voff[u] = static_cast<uint32_t>((cp_row[u] * D + cp_off[u]) * ES);
-    cp_lds[u] = static_cast<uint32_t>((u * kThreads + wave * PTD_WAVE) * 16);
+    cp_lds[u] = static_cast<uint32_t>((u * NT + wave * PTD_WAVE) * 16);
   }
   // element offset of key row `row0` (a multiple of 32): contiguous, or in
   // its page (a page holds a multiple of 32 rows, so the sub-tile's 32 rows
@@ -1200,6 +1201,7 @@ __global__ void __launch_bounds__(kValuThreads) k_attn_valu(AttnParams p) {
 struct Plan {
   bool mfma;
   int QB, WR, passes, rows_per_pass, splits;
+  int nt;  // threads per k_attn_mfma workgroup (512, or 256 with two workgroups per CU)
   bool needs_mask;  // mask rows read from memory (fp32 path, trees over 128 nodes)
   // workspace: [partials][mask rows], each 256-byte aligned
   size_t partial_bytes, mask_bytes, total_bytes;
@@ -1239,6 +1241,14 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
     // key; the passes share the keys through one XCD's L2 (measured on 8
     // KV heads x 256 rows x 32832 keys: 64.1 against 69.4 us).
     else { pl->WR = 4; pl->QB = 2; }
+    // A batch of sequences in 128-row passes runs 256-thread workgroups (the
+    // four row groups, one key group, a five-sub-tile ring in half of LDS),
+    // two resident per CU: one's prologue and tail overlap the other's rounds
+    // instead of following them, and their rounds drift apart instead of
+    // meeting at one barrier (measured on ragged-16: 136.5 against 146.2 us
+    // with three KV splits per sequence, 141.2 with two; a single sequence
+    // was not faster: 68.1 against 67.3 us on 8 KV heads x 32832 keys).
+    pl->nt = (pl->WR == 4 && s->B > 1) ? 256 : kThreads;
     pl->rows_per_pass = 16 * pl->QB * pl->WR;
     pl->passes = static_cast<int>((M + pl->rows_per_pass - 1) / pl->rows_per_pass);
     const long long items = static_cast<long long>(s->B) * s->Hkv * pl->passes;
@@ -1246,7 +1256,7 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
     // twice the workgroups, so the dispatcher can even out long and short
     // ones (measured on 16 sequences of 512-8192 keys: 151-158 against
     // 167-171 us; a single sequence was slower with it).
-    const int target = s->B > 1 ? 2 * kTargetBlocks : kTargetBlocks;
+    const int target = pl->nt == 256 ? 3 * kTargetBlocks : s->B > 1 ? 2 * kTargetBlocks : kTargetBlocks;
     int sp = static_cast<int>(target / items);
     const int max_by_len = (s->L_cap + 255) / 256;  // at least ~256 keys per split
     if (sp > max_by_len) sp = max_by_len;
@@ -1255,6 +1265,7 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
     pl->splits = sp;
   } else {
     pl->WR = pl->QB = 0;
+    pl->nt = kValuThreads;
     pl->rows_per_pass = kValuRows;
     pl->passes = static_cast<int>((M + kValuRows - 1) / kValuRows);
     pl->splits = 1;
@@ -1274,6 +1285,10 @@ bool make_plan(const ptd_attn_shape* s, int T, Plan* pl) {
 template <int D, bool F8>
 void launch_mfma(const Plan& pl, const AttnParams& prm, hipStream_t st) {
   const dim3 grid(prm.B * prm.Hkv * pl.passes * pl.splits);
+  if (pl.nt == 256) {
+    hipLaunchKernelGGL((k_attn_mfma<D, 2, 4, F8, 256>), grid, dim3(256), 0, st, prm);
+    return;
+  }
   const dim3 block(kThreads);
 #define PTD_MFMA_CASE(qb_, wr_) \
   if (pl.QB == qb_ && pl.WR == wr_) { hipLaunchKernelGGL((k_attn_mfma<D, qb_, wr_, F8>), grid, block, 0, st, prm); return; }
