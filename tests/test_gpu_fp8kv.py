@@ -94,6 +94,27 @@ def test_fp8kv_unit_scales_equal_bf16_kernel_on_decoded_caches(P):
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+def test_fp8kv_unit_scales_equal_bf16_kernel_batch_of_long_groups(P):
+    # 256 query rows per KV head in a batch: the 256-thread workgroups, two
+    # per CU, for both kernels
+    rng = np.random.default_rng(22)
+    B, T, L = 3, 64, 1500
+    q, kq, _, vq, _ = make(rng, B, T, 32, 8, L)
+    kv_len = np.array([L - T, 333, 1000], np.int32)
+    parent = np.stack([W.tree_uniform(rng, T)[0] for _ in range(B)])
+    a = run(P, q, kq, None, vq, None, kv_len, parent, out_dtype=torch.bfloat16)
+    kb = W.f32_to_bf16_bits(O.e4m3_decode(kq).astype(np.float32))
+    vb = W.f32_to_bf16_bits(O.e4m3_decode(vq).astype(np.float32))
+    b = P.tree_attention(cu(q), cu(kb), cu(vb), cu(kv_len), cu(parent))
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    # unit scales leave the codes' own range (up to 448): the bound relative
+    # to the values' scale, as for scaled caches
+    ref = O.tree_attention(q, kb, vb, kv_len, parent, 1.0 / np.sqrt(128))
+    got = run(P, q, kq, None, vq, None, kv_len, parent).cpu().numpy()
+    assert np.abs(got - ref).max() <= TOL * np.abs(ref).max() / 4
+
+
 def test_fp8kv_ragged_and_scales(P):
     rng = np.random.default_rng(21)
     B, T, L = 4, 20, 600

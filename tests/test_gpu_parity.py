@@ -450,6 +450,9 @@ SMALL = [
     _spec(B=12, Hq=4, Hkv=2, T=16, kv_len=[200, 50, 200, 200, 0, 50, 700, 700, 3, 200, 50, 700]),
     _spec(B=5, Hq=2, Hkv=1, T=20, kv_len=[10, 900, 300, 900, 1]),
     _spec(B=65, Hq=2, Hkv=1, T=4, kv_len=[(53 * i) % 400 for i in range(65)]),
+    # batches in 128-row passes (256-thread workgroups, two per CU), D = 64 too
+    _spec(B=2, Hq=8, Hkv=2, T=40, kv_len=[300, 1200]),
+    _spec(D=64, B=3, Hq=8, Hkv=2, T=40, kv_len=[1200, 0, 450]),
 ]
 
 
