@@ -248,7 +248,10 @@ __global__ void __launch_bounds__(NT, kThreads / NT) k_attn_mfma(AttnParams p) {
   if (by_size) {
     const int bl = b;
     int nl = -1;
-    if (lane < p.B) nl = p.kv_len[lane] + live_nodes(p, lane);
+    if (lane < p.B) {  // clamped: an invalid kv_len is reported below, not summed
+      const int kv = p.kv_len[lane];
+      nl = (kv < 0 ? -1 : min(kv, p.L_cap)) + live_nodes(p, lane);
+    }
     int rank = 0;
     for (int j = 0; j < p.B; ++j) {
       const int nj = __shfl(nl, j, PTD_WAVE);
@@ -261,7 +264,7 @@ __global__ void __launch_bounds__(NT, kThreads / NT) k_attn_mfma(AttnParams p) {
 
   const int n_kv = p.kv_len[b];
   const int tl = live_nodes(p, b);
-  if (n_kv < 0 || n_kv + tl > p.L_cap) {
+  if (n_kv < 0 || n_kv > p.L_cap - tl) {  // (no overflow near the int range)
     if (tid == 0) ptd::report(p.dev_status, PTD_ERR_KV_LEN);
     return;
   }
@@ -1050,8 +1053,8 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnParams p) {
   const int n_kv = p.kv_len[b];
   const int tl = live_nodes(p, b);
   load_group(0);
-  const bool valid = n_kv >= 0 && n_kv + tl <= p.L_cap;  // else reported by the attention kernel
-  const int N = n_kv + tl;
+  const bool valid = n_kv >= 0 && n_kv <= p.L_cap - tl;  // else reported by the attention kernel
+  const int N = valid ? n_kv + tl : 1;
   const int csz = chunk_size(max(N, 1), p.splits);
   const int nsp = (N + csz - 1) / csz;  // non-empty splits
   float mrun = kNegBig, den = 0.f;
@@ -1110,7 +1113,7 @@ __global__ void __launch_bounds__(kValuThreads) k_attn_valu(AttnParams p) {
   const int pass = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int n_kv = p.kv_len[b];
   const int tl = live_nodes(p, b);
-  if (n_kv < 0 || n_kv + tl > p.L_cap) {
+  if (n_kv < 0 || n_kv > p.L_cap - tl) {  // (no overflow near the int range)
     if (tid == 0) ptd::report(p.dev_status, PTD_ERR_KV_LEN);
     return;
   }

@@ -602,6 +602,25 @@ def test_attention_kv_len_too_long_reports(P):
     assert st.item() == 8
 
 
+@pytest.mark.parametrize("bad", [-5, 2 ** 31 - 1])
+def test_attention_bad_kv_len_in_a_batch(P, bad):
+    # a batch taken largest first with one invalid length (negative, or near
+    # the int range): reported, and the other sequences are still right
+    spec = _spec(B=4, Hq=32, Hkv=8, T=40, kv_len=[300, 40, 900, 120])
+    w = W.make_workload(spec, seed=11, logits=False)
+    ref = O.tree_attention(w.q, w.k_cache, w.v_cache, w.kv_len, w.parent, w.scale)
+    kvl = w.kv_len.copy()
+    kvl[1] = bad
+    st = status_buf()
+    got = P.tree_attention(cu(w.q), cu(w.k_cache), cu(w.v_cache), cu(kvl), cu(w.parent),
+                           out_dtype=torch.float32, dev_status=st)
+    torch.cuda.synchronize()
+    assert st.item() == 8
+    got = got.cpu().numpy()
+    for b in (0, 2, 3):
+        assert np.abs(got[b] - ref[b]).max() <= TOL["bf16"], b
+
+
 # ---------------------------------------------------------------------------
 # one whole step through the C ABI
 # ---------------------------------------------------------------------------
