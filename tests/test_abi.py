@@ -55,6 +55,17 @@ def test_attention_workspace_sizes():
     assert P.ptd_tree_attention_workspace_bytes(_shape(L=0), 64) == 0
 
 
+def test_attention_workspace_split_plans():
+    # the partial bytes follow the plan's KV splits: one sequence of 256-row
+    # groups: 16 splits (256 workgroups of 512 threads); a batch of them:
+    # three splits per sequence (two 256-thread workgroups per CU)
+    per = lambda B, splits: -(-splits * B * 8 * 256 * 130 * 4 // 256) * 256
+    one = P.ptd_tree_attention_workspace_bytes(_shape(B=1, Hq=32, Hkv=8, L=32832), 64)
+    assert one == per(1, 16)
+    batch = P.ptd_tree_attention_workspace_bytes(_shape(B=16, Hq=32, Hkv=8, L=7798), 64)
+    assert batch == per(16, 3)
+
+
 def test_topk_workspace_sizes():
     assert P.ptd_topk_workspace_bytes(65, 300000, 4) > 0    # several slices per row
     assert P.ptd_topk_workspace_bytes(65, 128256, 4) == 65 * 8 * 4 * 16   # 8 fp32 slices (bf16: 4)
